@@ -1,0 +1,136 @@
+"""Plain float64 CPU oracle for the subspace-network (SSN) stage-boundary codec.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import this module.  The product path (the
+HIP library and its Python binding) never calls it, and the two share no code.
+
+What the codec computes (paper section 4.1, "Pipeline-Parallel Communication
+with Reparameterized SSNs"):
+
+* Eq. (1) writes the residual stream after layer l as the embedding plus a sum
+  of attention/MLP output-projection contributions.  When every projection's
+  rows lie in span(U_k), U_k (d x k) orthonormal, the stream minus the fixed
+  embedding lies in that subspace.
+* Eq. (2): a stage subtracts the fixed token embedding (T_fixed, called E
+  here; Pluralis-8B uses rotary positions, so there is no additive positional
+  term) and sends the k coordinates (X - E[ids]) U_k per token.
+* The receiver rebuilds the activation with U_k^T: X' = E[ids] + Z U_k^T.
+* The backward pass uses the same compression: the gradient arriving at the
+  receiver's input is sent back as G U_k, and the sender expands it to
+  G_Z U_k^T (chain rule through Eq. (2)).
+* The original SSN keeps full-width output projections and, after every
+  optimizer step, projects them back into the subspace.  With PyTorch's
+  [out = d, in = n] weight layout the constrained index is the row index, so
+  the projection is W <- U (U^T W).
+
+Every function converts the stored inputs exactly to float64 (bf16 bits are
+widened by a shift, fp32 -> f64 is exact), evaluates the definition with
+numpy's float64 matmul as the only library primitive, and returns the
+unrounded float64 result.  Rows are processed in blocks of at most
+``ROW_BLOCK`` tokens so the V x d embedding table is never widened whole.
+
+Parity pins for every function live in tests/test_oracle_pins.py (exact
+rational brute force, closed forms and invariants fixed by the definitions).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+ROW_BLOCK = 4096
+
+
+def f64(a) -> np.ndarray:
+    """Exact float64 view of a stored array.
+
+    uint16 arrays are bfloat16 bit patterns (the top half of an IEEE binary32);
+    float32/float64 arrays are taken as they are.
+    """
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    if a.dtype in (np.float32, np.float64):
+        return a.astype(np.float64)
+    raise TypeError(f"unsupported stored dtype {a.dtype}")
+
+
+def compress(X, ids, E, U) -> np.ndarray:
+    """Eq. (2): Z = (X - E[ids]) U, one row per token.  X [N,d], ids [N],
+    E [V,d], U [d,k]  ->  Z [N,k] float64."""
+    X = np.asarray(X)
+    ids = np.asarray(ids)
+    U64 = f64(U)
+    N = X.shape[0]
+    Z = np.empty((N, U64.shape[1]), dtype=np.float64)
+    for r0 in range(0, N, ROW_BLOCK):
+        r1 = min(N, r0 + ROW_BLOCK)
+        D = f64(X[r0:r1]) - f64(np.asarray(E)[ids[r0:r1]])
+        Z[r0:r1] = D @ U64
+    return Z
+
+
+def decompress(Z, ids, E, U) -> np.ndarray:
+    """Receiver side of Eq. (2): X' = E[ids] + Z U^T.  With E and ids both
+    None this is the sender-side gradient expansion G_Z U^T."""
+    Z64 = f64(Z)
+    U64 = f64(U)
+    N = Z64.shape[0]
+    out = np.empty((N, U64.shape[0]), dtype=np.float64)
+    for r0 in range(0, N, ROW_BLOCK):
+        r1 = min(N, r0 + ROW_BLOCK)
+        out[r0:r1] = Z64[r0:r1] @ U64.T
+        if E is not None:
+            out[r0:r1] += f64(np.asarray(E)[np.asarray(ids)[r0:r1]])
+    return out
+
+
+def project_grad(G, U) -> np.ndarray:
+    """Backward compression: G_Z = G U.  G [N,d] -> [N,k] float64."""
+    G = np.asarray(G)
+    U64 = f64(U)
+    N = G.shape[0]
+    out = np.empty((N, U64.shape[1]), dtype=np.float64)
+    for r0 in range(0, N, ROW_BLOCK):
+        r1 = min(N, r0 + ROW_BLOCK)
+        out[r0:r1] = f64(G[r0:r1]) @ U64
+    return out
+
+
+def expand_grad(GZ, U) -> np.ndarray:
+    """Sender-side gradient expansion G_Z U^T (decompress without E)."""
+    return decompress(GZ, None, None, U)
+
+
+def project_weights(W, U) -> np.ndarray:
+    """Original-SSN re-projection W <- U (U^T W) for W [d, n] ([out, in])."""
+    U64 = f64(U)
+    W64 = f64(W)
+    T = U64.T @ W64
+    return U64 @ T
+
+
+def rel_frobenius(got, ref) -> float:
+    """||got - ref||_F / ||ref||_F in float64 (the parity metric)."""
+    g = f64(got) if np.asarray(got).dtype == np.uint16 else np.asarray(got, dtype=np.float64)
+    r = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(r)
+    num = np.linalg.norm(g - r)
+    if den == 0.0:
+        return float(num)
+    return float(num / den)
+
+
+# --------------------------------------------------------------------------
+# Wire sizes of a stage boundary (section 4.1 and the bandwidth estimate of
+# section 3.5).  Activations cross the wire in FP32.
+# --------------------------------------------------------------------------
+def boundary_bits(n_tokens: int, width: float, bits_per_value: int = 32) -> float:
+    """Bits of one boundary message carrying `width` values per token."""
+    return float(n_tokens) * float(width) * bits_per_value
+
+
+def bandwidth_floor_bits_per_s(a_f: float, a_b: float, seq_len: int, width: float,
+                               ar_bits: int, ar_payload_params: float, ar_time_s: float) -> float:
+    """Per-contributor bandwidth estimate of section 3.5: forward + backward
+    activation payloads in FP32 at the given wire width, plus one all-reduce
+    burst of `ar_payload_params` values of `ar_bits` bits every `ar_time_s`."""
+    return 32.0 * (a_f + a_b) * seq_len * width + ar_bits * ar_payload_params / ar_time_s

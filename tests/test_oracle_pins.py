@@ -1,0 +1,217 @@
+"""Pins for the float64 oracle, against facts fixed by the paper's definitions
+(section 4.1, Eq. (2) and the original-SSN re-projection) and by mathematics:
+exact rational brute force, closed forms, invariants and special bases.
+
+Each pin is chosen so that a plausible slip in the oracle -- a dropped or
+sign-flipped embedding term, a wrong gather index, a transposed basis, a
+missing second factor in the weight projection -- fails at least one test.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import exact
+from oracle import ssn_oracle as O
+from paper_2607_13332_amd import inputs as I
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand_case(dtype, N=5, d=12, k=3, V=7, n=4, seed=7):
+    r = np.random.default_rng(seed)
+    U = I.store(I.gaussian_orthonormal_basis(d, k, seed), dtype)
+    E = I.store(0.3 * r.standard_normal((V, d)), dtype)
+    X = I.store(r.standard_normal((N, d)), dtype)
+    G = I.store(r.standard_normal((N, d)), dtype)
+    W = I.store(r.standard_normal((d, n)), dtype)
+    ids = r.integers(0, V, size=N).astype(np.int32)
+    Z = r.standard_normal((N, k)).astype(np.float32)
+    return dict(U=U, E=E, X=X, G=G, W=W, ids=ids, Z=Z)
+
+
+def _rel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300)
+
+
+# ---------------------------------------------------------------- brute force
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_exact_bruteforce_all_ops(dtype):
+    c = _rand_case(dtype)
+    assert _rel(O.compress(c["X"], c["ids"], c["E"], c["U"]),
+                exact.to_float(exact.compress(c["X"], c["ids"], c["E"], c["U"]))) < 1e-14
+    assert _rel(O.decompress(c["Z"], c["ids"], c["E"], c["U"]),
+                exact.to_float(exact.decompress(c["Z"], c["ids"], c["E"], c["U"]))) < 1e-14
+    assert _rel(O.expand_grad(c["Z"], c["U"]),
+                exact.to_float(exact.decompress(c["Z"], None, None, c["U"]))) < 1e-14
+    assert _rel(O.project_grad(c["G"], c["U"]),
+                exact.to_float(exact.project_grad(c["G"], c["U"]))) < 1e-14
+    assert _rel(O.project_weights(c["W"], c["U"]),
+                exact.to_float(exact.project_weights(c["W"], c["U"]))) < 1e-14
+
+
+# ---------------------------------------------------------------- closed form
+def test_pythagorean_basis_worked_example():
+    """d=2, k=1, U=(3/5, 4/5)^T: every value below is computed by hand."""
+    U = np.array([[0.6], [0.8]])
+    E = np.array([[0.5, 0.5], [2.0, -1.0]])
+    X = np.array([[1.0, 2.0], [2.0, -1.0]])
+    ids = np.array([0, 1], dtype=np.int32)
+    # token 0: (1-0.5)*0.6 + (2-0.5)*0.8 = 0.3 + 1.2 = 1.5 ; token 1: X = E[1] -> 0
+    np.testing.assert_allclose(O.compress(X, ids, E, U), [[1.5], [0.0]], atol=1e-15)
+    # 0.5 + 1.5*0.6 = 1.4 ; 0.5 + 1.5*0.8 = 1.7
+    np.testing.assert_allclose(O.decompress(np.array([[1.5], [0.0]]), ids, E, U),
+                               [[1.4, 1.7], [2.0, -1.0]], atol=1e-15)
+    # G U = 1*0.6 + 2*0.8 = 2.2 ; expand 2.2 -> (1.32, 1.76)
+    np.testing.assert_allclose(O.project_grad(np.array([[1.0, 2.0]]), U), [[2.2]], atol=1e-15)
+    np.testing.assert_allclose(O.expand_grad(np.array([[2.2]]), U), [[1.32, 1.76]], atol=1e-15)
+    # W = e_1 (one column): U^T W = 0.6 -> U*0.6 = (0.36, 0.48)
+    np.testing.assert_allclose(O.project_weights(np.array([[1.0], [0.0]]), U), [[0.36], [0.48]],
+                               atol=1e-15)
+
+
+def test_structured_activation_recovers_coordinates():
+    """X = E[ids] + Z0 U^T (+ noise orthogonal to span U) compresses to Z0."""
+    d, k, V, N = 96, 8, 50, 40
+    r = np.random.default_rng(3)
+    U = I.gaussian_orthonormal_basis(d, k, 11)
+    E = 0.02 * r.standard_normal((V, d))
+    ids = r.integers(0, V, size=N).astype(np.int32)
+    Z0 = r.standard_normal((N, k))
+    X = np.array(E[ids])
+    for c in range(k):                       # column-by-column superposition
+        X += np.outer(Z0[:, c], U[:, c])
+    np.testing.assert_allclose(O.compress(X, ids, E, U), Z0, atol=1e-12)
+    # noise in the orthogonal complement (from a complete QR) is invisible
+    q, _ = np.linalg.qr(np.concatenate([U, r.standard_normal((d, d - k))], axis=1))
+    comp = q[:, k:]
+    eta = r.standard_normal((N, d - k)) @ comp.T
+    np.testing.assert_allclose(O.compress(X + eta, ids, E, U), Z0, atol=1e-11)
+    # generic noise moves Z by at most ||eta|| (U has orthonormal columns)
+    eta2 = 1e-3 * r.standard_normal((N, d))
+    dz = O.compress(X + eta2, ids, E, U) - Z0
+    assert np.linalg.norm(dz) <= np.linalg.norm(eta2) * (1 + 1e-12)
+
+
+def test_roundtrip_and_identities():
+    d, k, V, N = 64, 6, 20, 33
+    r = np.random.default_rng(5)
+    U = I.gaussian_orthonormal_basis(d, k, 2)
+    E = r.standard_normal((V, d)).astype(np.float32)
+    ids = r.integers(0, V, size=N).astype(np.int32)
+    Z = r.standard_normal((N, k))
+    # compress(decompress(Z)) == Z
+    np.testing.assert_allclose(O.compress(O.decompress(Z, ids, E, U), ids, E, U), Z, atol=1e-12)
+    # decompress(0) is exactly the gathered embedding rows
+    assert np.array_equal(O.decompress(np.zeros((N, k)), ids, E, U), E[ids].astype(np.float64))
+    # compress(E[ids]) is exactly zero
+    assert np.array_equal(O.compress(E[ids], ids, E, U), np.zeros((N, k)))
+    # the sender expansion is the adjoint of the gradient projection
+    G = r.standard_normal((N, d))
+    H = r.standard_normal((N, k))
+    lhs = np.sum(O.project_grad(G, U) * H)
+    rhs = np.sum(G * O.expand_grad(H, U))
+    assert abs(lhs - rhs) <= 1e-12 * abs(lhs)
+
+
+def test_linearity_and_cross_op_consistency():
+    c = _rand_case("f32", N=17, d=40, k=5, V=9)
+    r = np.random.default_rng(9)
+    G1, G2 = r.standard_normal((2, 17, 40))
+    a, b = 1.75, -0.5
+    np.testing.assert_allclose(O.project_grad(a * G1 + b * G2, c["U"]),
+                               a * O.project_grad(G1, c["U"]) + b * O.project_grad(G2, c["U"]),
+                               atol=1e-12)
+    # compress = project_grad(X) - project_grad(E[ids])
+    np.testing.assert_allclose(O.compress(c["X"], c["ids"], c["E"], c["U"]),
+                               O.project_grad(c["X"], c["U"]) - O.project_grad(c["E"][c["ids"]], c["U"]),
+                               atol=1e-12)
+
+
+# ---------------------------------------------------------------- special bases
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_selection_basis_is_exact(dtype):
+    d, k, V, N, n = 32, 5, 11, 19, 7
+    r = np.random.default_rng(13)
+    Uf = I.selection_basis(d, k, 4)
+    cols = np.argmax(Uf, axis=0)
+    U = I.store(Uf, dtype)
+    E = I.store(r.standard_normal((V, d)), dtype)
+    X = I.store(r.standard_normal((N, d)), dtype)
+    ids = r.integers(0, V, size=N).astype(np.int32)
+    Xd, Ed = O.f64(X), O.f64(E)
+    assert np.array_equal(O.compress(X, ids, E, U), (Xd - Ed[ids])[:, cols])
+    assert np.array_equal(O.project_grad(X, U), Xd[:, cols])
+    Z = r.standard_normal((N, k)).astype(np.float32)
+    ref = Ed[ids].copy()
+    ref[:, cols] += Z
+    assert np.array_equal(O.decompress(Z, ids, E, U), ref)
+    W = I.store(r.standard_normal((d, n)), dtype)
+    PW = np.zeros((d, n))
+    PW[cols] = O.f64(W)[cols]
+    assert np.array_equal(O.project_weights(W, U), PW)
+
+
+@pytest.mark.parametrize("d,k", [(256, 8), (4096, 64)])
+def test_hadamard_basis_exactly_orthonormal(d, k):
+    U = I.store(I.hadamard_basis(d, k, 1), "bf16")
+    U64 = O.f64(U)
+    assert np.array_equal(U64.T @ U64, np.eye(k))
+    r = np.random.default_rng(1)
+    Z = r.standard_normal((16, k))
+    ids = np.zeros(16, dtype=np.int32)
+    E = np.zeros((1, d), dtype=np.float32)
+    np.testing.assert_allclose(O.compress(O.decompress(Z, ids, E, U), ids, E, U), Z, atol=1e-12)
+
+
+# ---------------------------------------------------------------- weights
+def test_weight_projection_properties():
+    d, k, n = 48, 7, 10
+    r = np.random.default_rng(21)
+    U = I.gaussian_orthonormal_basis(d, k, 6)
+    W1, W2 = r.standard_normal((2, d, n))
+    P1 = O.project_weights(W1, U)
+    # idempotent
+    np.testing.assert_allclose(O.project_weights(P1, U), P1, atol=1e-12)
+    # self-adjoint
+    assert abs(np.sum(P1 * W2) - np.sum(W1 * O.project_weights(W2, U))) < 1e-10
+    # Pythagoras: ||W||^2 = ||PW||^2 + ||W - PW||^2
+    assert abs(np.sum(W1 ** 2) - np.sum(P1 ** 2) - np.sum((W1 - P1) ** 2)) < 1e-9
+    # rank <= k and columns inside span(U)
+    s = np.linalg.svd(P1, compute_uv=False)
+    assert np.all(s[k:] < 1e-12 * s[0])
+    # a matrix already in the subspace is unchanged; its complement is removed
+    A = r.standard_normal((k, n))
+    Win = sum(np.outer(U[:, c], A[c]) for c in range(k))
+    np.testing.assert_allclose(O.project_weights(Win, U), Win, atol=1e-12)
+    q, _ = np.linalg.qr(np.concatenate([U, r.standard_normal((d, d - k))], axis=1))
+    Wout = q[:, k:] @ r.standard_normal((d - k, n))
+    assert np.linalg.norm(O.project_weights(Wout, U)) < 1e-12 * np.linalg.norm(Wout)
+
+
+def test_bf16_widening_is_exact():
+    bits = np.array([0x0000, 0x3F80, 0xBF80, 0x4049, 0x0001, 0x7F7F], dtype=np.uint16)
+    vals = O.f64(bits)
+    assert vals[0] == 0.0 and vals[1] == 1.0 and vals[2] == -1.0
+    assert vals[3] == 3.140625                       # 0x4049 = 1.5703125 * 2
+    assert vals[4] == 2.0 ** -133                     # smallest bf16 subnormal
+    assert vals[5] == (2 - 2 ** -7) * 2.0 ** 127      # largest finite bf16
+
+
+# ---------------------------------------------------------------- paper figures
+def test_paper_wire_figures():
+    """Printed message sizes of the stage boundary (fixtures cite the passage)."""
+    with open(os.path.join(GOLDEN, "paper_figures.json")) as f:
+        fig = json.load(f)
+    b = fig["uncompressed_boundary_mbit"]
+    bits = O.boundary_bits(b["tokens"], b["d"], 32)
+    assert round(bits / 1e6) == b["value"]
+    c8 = fig["compression_8b"]
+    assert c8["d"] / c8["rate"] == pytest.approx(c8["wire_width"])
+    c1 = fig["compression_1b"]
+    assert round(c1["d"] / c1["rank"]) == c1["rate"]
+    # the codec message is 1/rate of the uncompressed one (activations in FP32)
+    assert O.boundary_bits(b["tokens"], c8["wire_width"], 32) == pytest.approx(bits / c8["rate"])
