@@ -1,0 +1,268 @@
+#!/usr/bin/env python3
+"""Benchmark of the subspace-network stage-boundary codec on one MI355X.
+
+One step = one microbatch through every codec operation of a pipeline stage
+boundary, on the 8B-stage-shaped workload (N = 16 x 2048 = 32768 tokens,
+d = 4096, k = 64, V = 131072, bf16 storage, fp32 coordinates):
+
+    decompress (incoming coordinates -> activation), project_grad (gradient
+    leaving through the input boundary), compress (activation leaving through
+    the output boundary), expand_grad (incoming gradient coordinates).
+
+Two independent microbatch input sets alternate between steps so that
+consecutive steps gather different embedding rows.  Inputs are resident in
+HBM before the timed region starts.  The once-per-optimizer-step weight
+re-projection (4 layers x (4096x4096 + 4096x14336)) is timed separately and
+reported under "weights".
+
+Prints ONE JSON line (rank 0).  `--gpus` above 1 is refused: this build runs
+on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["paper_2607_13332_amd/csrc/codec_kernels.hip",
+                  "paper_2607_13332_amd/csrc/weights_kernels.hip",
+                  "paper_2607_13332_amd/csrc/ssn_device.h"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def parse_args():
+    p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-weights", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="target CPU time of the oracle baseline sample")
+    p.add_argument("--tokens", type=int, default=0, help="override N (testing only)")
+    return p.parse_args()
+
+
+def algorithmic_bytes(op: str, N: int, d: int, k: int, u: int, s: int = 2) -> int:
+    """Bytes each op must move: activations/gradients once, distinct embedding
+    rows once, coordinates once, the basis and ids once."""
+    U = d * k * s
+    if op == "compress":
+        return N * d * s + u * d * s + N * k * 4 + U + 4 * N
+    if op == "decompress":
+        return N * k * 4 + u * d * s + N * d * s + U + 4 * N
+    if op in ("project_grad", "expand_grad"):
+        return N * d * s + N * k * 4 + U
+    raise ValueError(op)
+
+
+def load_traffic(kernel_key: str):
+    """HBM bytes per launch measured by rocprofv3 PMC counters, if the stored
+    measurement was taken on the current kernel sources."""
+    path = os.path.join(PROFILES, "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    ent = t.get("kernels", {}).get(kernel_key)
+    return None if ent is None else ent.get("bytes_per_launch")
+
+
+def cpu_baseline(sample, cfg, seconds: float):
+    """The float64 oracle on a bounded token sample, on this host's cores."""
+    from oracle import ssn_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    n = sample["X"].shape[0]
+    done, t0 = 0, time.perf_counter()
+    while True:
+        O.decompress(sample["Zin"], sample["ids"], sample["E"], sample["U"])
+        O.project_grad(sample["G"], sample["U"])
+        O.compress(sample["X"], sample["ids"], sample["E"], sample["U"])
+        O.expand_grad(sample["GZin"], sample["U"])
+        done += n
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": done / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} of the {cfg.N} tokens of one microbatch (d={cfg.d}, k={cfg.k}), "
+                      f"all four codec ops in float64, repeated {done // n}x over {el:.1f} s"}
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the codec shards over tokens with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2607_13332_amd import inputs as I
+    from paper_2607_13332_amd import ssn
+
+    ssn.lib()   # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = I.STAGE8B if args.tokens == 0 else I.with_tokens(I.STAGE8B, args.tokens)
+    N, d, k, V = cfg.N, cfg.d, cfg.k, cfg.V
+
+    # ---------------- inputs, resident in HBM ----------------
+    base = I.codec_inputs_device(cfg, dev, need=("U", "E"))
+    U, E = base["U"], base["E"]
+    sets = []
+    for j in range(2):
+        c = I.with_tokens(cfg, N, seed=cfg.seed + 17 * j)
+        inp = I.codec_inputs_device(c, dev, need=("ids", "X", "G"))
+        inp["Zin"] = I.coords_device(N, k, c.seed + 1, dev)
+        inp["GZin"] = I.coords_device(N, k, c.seed + 2, dev)
+        inp["Z"] = torch.empty((N, k), dtype=torch.float32, device=dev)
+        inp["GZ"] = torch.empty((N, k), dtype=torch.float32, device=dev)
+        inp["Y"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        inp["GX"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        inp["u"] = int(torch.unique(inp["ids"]).numel())
+        sets.append(inp)
+    torch.cuda.synchronize()
+
+    ops = ["decompress", "project_grad", "compress", "expand_grad"]
+
+    def step(s, evs=None):
+        if evs is not None:
+            evs[0].record()
+        ssn.decompress(s["Zin"], s["ids"], E, U, out=s["Y"])
+        if evs is not None:
+            evs[1].record()
+        ssn.project_grad(s["G"], U, out=s["GZ"])
+        if evs is not None:
+            evs[2].record()
+        ssn.compress(s["X"], s["ids"], E, U, out=s["Z"])
+        if evs is not None:
+            evs[3].record()
+        ssn.expand_grad(s["GZin"], U, out=s["GX"])
+        if evs is not None:
+            evs[4].record()
+
+    for i in range(args.warmup):
+        step(sets[i % 2])
+    torch.cuda.synchronize()
+
+    # ---------------- timed region ----------------
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(sets[i % 2], events[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+
+    per_op_ms = {op: 0.0 for op in ops}
+    for i in range(args.steps):
+        for j, op in enumerate(ops):
+            per_op_ms[op] += events[i][j].elapsed_time(events[i][j + 1]) / args.steps
+    per_op = {}
+    for op in ops:
+        byts = np.mean([algorithmic_bytes(op, N, d, k, s["u"]) for s in sets])
+        per_op[op] = {"ms": round(per_op_ms[op], 5),
+                      "tokens_per_s": round(N / (per_op_ms[op] * 1e-3), 1),
+                      "algorithmic_GBps": round(byts / (per_op_ms[op] * 1e-3) / 1e9, 1),
+                      "frac_hbm_peak": round(byts / (per_op_ms[op] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                      "bytes_per_launch": int(byts)}
+    dom = max(ops, key=lambda o: per_op_ms[o])
+    achieved = per_op[dom]["algorithmic_GBps"]
+    traffic = load_traffic(dom)
+    step_bytes = sum(per_op[o]["bytes_per_launch"] for o in ops)
+
+    result = {
+        "metric": "codec tokens/s at d=4096,k=64 bf16 + achieved HBM GB/s as % of peak",
+        "value": round(N / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "stage-boundary codec of an 8B-shaped pipeline stage: "
+                               "decompress + project_grad + compress + expand_grad per microbatch",
+                   "N": N, "B": cfg.B, "S": cfg.S, "d": d, "k": k, "V": V, "ids": cfg.ids_dist,
+                   "storage": "bf16", "coords": "fp32", "parallelism": "none (1 GPU)"},
+        "step_algorithmic_GBps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "step_frac_hbm_peak": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "per_op": per_op,
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic},
+        "kernel_source_hash": kernel_source_hash(),
+    }
+
+    # ---------------- weight re-projection (once per optimizer step) ----------------
+    if not args.no_weights:
+        wc = I.WEIGHTS
+        Ws = []
+        for layer in range(wc.layers):
+            for j, (dd, n) in enumerate(wc.shapes):
+                Ws.append(I.weights_device(dd, n, wc.seed * 100 + 10 * layer + j, dev))
+        Uw = I.to_device(I.store(I.gaussian_orthonormal_basis(wc.d, wc.k, wc.seed), "bf16"), "bf16", dev)
+        for _ in range(2):
+            ssn.project_weights_batched(Ws, Uw)
+        torch.cuda.synchronize()
+        reps = max(3, args.steps // 5)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record()
+        for r in range(reps):
+            ssn.project_weights_batched(Ws, Uw)
+            ev[r + 1].record()
+        torch.cuda.synchronize()
+        wms = sum(ev[r].elapsed_time(ev[r + 1]) for r in range(reps)) / reps
+        wbytes = sum(2 * W.numel() * 2 for W in Ws) + wc.d * wc.k * 2
+        wflops = sum(4.0 * wc.d * wc.k * W.shape[1] for W in Ws)
+        result["weights"] = {
+            "workload": "W <- U(U^T W) for 4 layers x (W_o 4096x4096, W_down 4096x14336) bf16, k=64, one launch",
+            "ms": round(wms, 5),
+            "algorithmic_GBps": round(wbytes / (wms * 1e-3) / 1e9, 1),
+            "frac_hbm_peak": round(wbytes / (wms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "mfma_TFLOPs": round(wflops / (wms * 1e-3) / 1e12, 2),
+            "frac_mfma_peak": round(wflops / (wms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": load_traffic("project_weights"),
+        }
+        del Ws
+
+    # ---------------- CPU baseline: the oracle on a bounded sample ----------------
+    if not args.no_cpu_baseline:
+        s = sets[0]
+        ns = min(N, 2048)
+        rows = torch.arange(ns, device=dev)
+        sample = {
+            "X": I.to_host(s["X"][rows]), "G": I.to_host(s["G"][rows]),
+            "Zin": I.to_host(s["Zin"][rows]), "GZin": I.to_host(s["GZin"][rows]),
+            "E": I.to_host(E.index_select(0, s["ids"][rows].long())),
+            "ids": np.arange(ns, dtype=np.int32), "U": I.to_host(U),
+        }
+        result["cpu_baseline"] = cpu_baseline(sample, cfg, args.cpu_seconds)
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,160 @@
+/*
+ * ssn.h -- C ABI of the MI355X (gfx950) subspace-network stage-boundary codec.
+ *
+ * The operations follow section 4.1 of the paper ("Pipeline-Parallel
+ * Communication with Reparameterized SSNs").  A pipeline stage sends, per
+ * token, the k coordinates of its residual-stream activation in a fixed
+ * orthonormal basis U (d x k) after subtracting the fixed token embedding
+ * E[ids] that both sides of the boundary hold (Eq. (2)); the receiver rebuilds
+ * the activation with U^T; gradients travel back through the same compression;
+ * and the original SSN re-projects its full-width output projections into
+ * span(U) after every optimizer step.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensor pointers are DEVICE pointers (hipMalloc / torch CUDA memory),
+ *    row-major and contiguous.  The caller owns every buffer; the library
+ *    allocates no device memory and keeps no state between calls.
+ *  - `dtype` (ssn_dtype_t) is the storage type of X, E, U, G, W and of the
+ *    decompressed output.  Coordinates Z and projected gradients G_Z are always
+ *    float32 (the paper counts boundary activations in FP32).  All arithmetic
+ *    accumulates in float32; bf16 results are rounded to nearest-even once.
+ *  - ids are int32 in [0, V).  Ids outside that range are a contract
+ *    violation: the kernels clamp them into range (so memory stays in bounds)
+ *    and the corresponding output rows are unspecified.
+ *  - Every call only enqueues work on `stream` (a hipStream_t; NULL is the
+ *    default stream) and returns once the launch is accepted.  Device faults
+ *    surface at the caller's next synchronisation.
+ *  - Host-side validation runs before any HIP call.  A call with N == 0 (or
+ *    n == 0) is a valid no-op that touches no pointer.
+ *  - Outputs must not overlap inputs (SSN_ERR_ALIAS), except W, which is
+ *    updated in place.  Concurrent calls on different streams are safe.
+ *  - Every pointer must be aligned to its element size (SSN_ERR_ALIGN); the
+ *    fast paths additionally use 16-byte vector accesses when rows allow it.
+ */
+#ifndef SSN_H_
+#define SSN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SSN_ABI_VERSION 1
+/* Largest matrix count accepted by ssn_project_weights_batched. */
+#define SSN_MAX_BATCH 16
+
+typedef enum { SSN_F32 = 0, SSN_BF16 = 1 } ssn_dtype_t;
+
+typedef enum {
+  SSN_OK = 0,
+  SSN_ERR_NULL = 1,        /* a required pointer is NULL                      */
+  SSN_ERR_SHAPE = 2,       /* a size is out of range (negative, k > d, ...)  */
+  SSN_ERR_DTYPE = 3,       /* unknown dtype                                   */
+  SSN_ERR_ALIGN = 4,       /* pointer not aligned to its element size         */
+  SSN_ERR_UNSUPPORTED = 5, /* a shape no kernel handles (see each entry)      */
+  SSN_ERR_LAUNCH = 6,      /* the HIP launch failed (hipGetLastError)         */
+  SSN_ERR_ALIAS = 7        /* an output overlaps an input                     */
+} ssn_status_t;
+
+typedef enum {
+  SSN_OP_COMPRESS = 0,
+  SSN_OP_DECOMPRESS = 1,
+  SSN_OP_PROJECT_GRAD = 2,
+  SSN_OP_PROJECT_WEIGHTS = 3
+} ssn_op_t;
+
+/* Returns SSN_ABI_VERSION. */
+int ssn_abi_version(void);
+
+/* Static, human-readable name of a status code (never NULL). */
+const char *ssn_status_string(int status);
+
+/*
+ * Name of the kernel family ("mfma" or "generic") that `op` uses for this
+ * dtype and shape when every pointer is 16-byte aligned; "invalid" for an
+ * unknown op.  Pure host function (no HIP call), for tests and reports.
+ * The MFMA kernels cover bf16 with: compress / project_grad d % 32 == 0 and
+ * k <= 128; decompress d % 64 == 0, k % 8 == 0, k <= 128; project_weights
+ * d % 32 == 0, k % 8 == 0, k <= 128.  Everything else runs the generic
+ * kernels (fp32 arithmetic, one wavefront per token / one block per column).
+ */
+const char *ssn_kernel_family(ssn_op_t op, ssn_dtype_t dtype, int64_t d, int64_t k);
+
+/*
+ * ssn_compress -- sender side of Eq. (2), section 4.1.
+ *   Z[i, :] = (X[i, :] - E[ids[i], :]) . U           for i in [0, N)
+ *   X   [N, d]  dtype      activations leaving the stage
+ *   ids [N]     int32      token ids of those rows
+ *   E   [V, d]  dtype      fixed token-embedding table
+ *   U   [d, k]  dtype      orthonormal basis (used as stored)
+ *   Z   [N, k]  float32    output coordinates
+ * Requires 1 <= k <= d, V >= 1.  The subtraction is distributed over the
+ * contraction on the MFMA path (X.U and E[ids].U accumulate by identical
+ * fp32 sequences and are subtracted once); the generic path subtracts in fp32
+ * first.  On both, compress(E[ids]) is exactly zero.
+ */
+ssn_status_t ssn_compress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
+                          const void *X, const int32_t *ids, const void *E, const void *U,
+                          float *Z, void *stream);
+
+/*
+ * ssn_decompress -- receiver side of Eq. (2), section 4.1 (reconstruction
+ * with U^T), and the sender-side gradient expansion.
+ *   Xout[i, :] = E[ids[i], :] + Z[i, :] . U^T        (E, ids non-NULL)
+ *   Xout[i, :] =                Z[i, :] . U^T        (E == ids == NULL)
+ *   Z    [N, k] float32     coordinates (or projected gradient G_Z)
+ *   ids  [N]    int32 / NULL
+ *   E    [V, d] dtype / NULL
+ *   U    [d, k] dtype
+ *   Xout [N, d] dtype       output, rounded once to dtype
+ * With N > 0, passing exactly one of E / ids as NULL is SSN_ERR_NULL (with
+ * N == 0 every pointer may be NULL, as for the other entries).  The second form is
+ * the chain rule through Eq. (2): the gradient w.r.t. the sender's activation
+ * is G_Z U^T.
+ */
+ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
+                            const float *Z, const int32_t *ids, const void *E, const void *U,
+                            void *Xout, void *stream);
+
+/*
+ * ssn_project_grad -- backward compression, section 4.1 ("the backward pass
+ * uses the same compression"): the receiver sends G_Z = G . U back.
+ *   G  [N, d] dtype      gradient w.r.t. the decompressed activation
+ *   U  [d, k] dtype
+ *   GZ [N, k] float32    output
+ */
+ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k,
+                              const void *G, const void *U, float *GZ, void *stream);
+
+/*
+ * ssn_project_weights -- original-SSN re-projection after an optimizer step
+ * (section 4.1, and section 6.1 which contrasts it with the reparameterized
+ * form): the rows of every output projection are pulled back into span(U).
+ * With PyTorch's [out = d, in = n] layout this is
+ *   W <- U . (U^T . W)        in place, W [d, n] dtype, U [d, k] dtype
+ * U^T W is accumulated in fp32 and never leaves the chip; W is read once and
+ * written once.  Requires 1 <= k <= d.  k > 1024 is SSN_ERR_UNSUPPORTED.
+ */
+ssn_status_t ssn_project_weights(ssn_dtype_t dtype, int64_t d, int64_t n, int64_t k,
+                                 void *W, const void *U, void *stream);
+
+/*
+ * ssn_project_weights_batched -- the same re-projection for `count` matrices
+ * that share d and U (e.g. every attention and MLP output projection of a
+ * pipeline stage), in one launch.
+ *   W[b] [d, n[b]] dtype, in place, for b in [0, count)
+ *   W and n are HOST arrays of `count` entries; 1 <= count <= SSN_MAX_BATCH.
+ * Matrices must not overlap each other.
+ */
+ssn_status_t ssn_project_weights_batched(ssn_dtype_t dtype, int64_t count, int64_t d,
+                                         const int64_t *n, int64_t k, void *const *W,
+                                         const void *U, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSN_H_ */

@@ -1,0 +1,84 @@
+// Device-side helpers shared by the codec kernels (gfx950 / CDNA4 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ssn {
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// Round-to-nearest-even float -> bf16 (hardware v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
+}
+
+// Two floats -> one dword of packed bf16 (lo in bits 0..15).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+}
+
+// Low / high bf16 of a packed dword, widened to float.
+__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// 16x16x32 bf16 MFMA, fp32 accumulate.  Operand layout (64 lanes):
+//   A (16 x 32): lane l holds row l%16, K elements 8*(l/16) .. 8*(l/16)+7
+//   B (32 x 16): lane l holds column l%16, the same K elements
+//   C (16 x 16): lane l holds rows 4*(l/16) .. +3 of column l%16
+// Only the pairing of K elements between A and B matters for the result, so
+// the kernels are free to choose which physical index each K slot carries.
+__device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// Split 8 floats into bf16 hi + lo parts with x ~= hi + lo to ~2^-17 relative:
+// two MFMAs on (hi, lo) carry a float32 operand at close to fp32 accuracy.
+__device__ __forceinline__ void split_bf16x8(const float* v, u32x4& hi, u32x4& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    uint32_t h0 = f32_to_bf16(v[2 * m]), h1 = f32_to_bf16(v[2 * m + 1]);
+    float r0 = v[2 * m] - __uint_as_float(h0 << 16);
+    float r1 = v[2 * m + 1] - __uint_as_float(h1 << 16);
+    h[m] = h0 | (h1 << 16);
+    l[m] = pack_bf16x2(r0, r1);
+  }
+  hi = u32x4{h[0], h[1], h[2], h[3]};
+  lo = u32x4{l[0], l[1], l[2], l[3]};
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
+template <typename T>
+__device__ __forceinline__ float load_as_f32(const T* p);
+template <>
+__device__ __forceinline__ float load_as_f32<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float load_as_f32<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+
+template <typename T>
+__device__ __forceinline__ void store_from_f32(T* p, float v);
+template <>
+__device__ __forceinline__ void store_from_f32<float>(float* p, float v) { *p = v; }
+template <>
+__device__ __forceinline__ void store_from_f32<uint16_t>(uint16_t* p, float v) { *p = (uint16_t)f32_to_bf16(v); }
+
+__device__ __forceinline__ int64_t clamp_id(int32_t id, int64_t V) {
+  int64_t i = id;
+  return i < 0 ? 0 : (i >= V ? V - 1 : i);
+}
+
+}  // namespace ssn

@@ -1,0 +1,28 @@
+// Host-side launchers implemented next to their kernels; the C ABI in
+// ssn_api.hip validates arguments and then calls these.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ssn {
+
+constexpr int kF32 = 0;
+constexpr int kBF16 = 1;
+constexpr int kMaxBatch = 16;
+
+bool compress_uses_mfma(int dtype, int64_t d, int64_t k);
+bool decompress_uses_mfma(int dtype, int64_t d, int64_t k);
+bool weights_use_mfma(int dtype, int64_t d, int64_t k);
+
+hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
+                           const int32_t* ids, const void* E, const void* U, float* Z,
+                           hipStream_t st);
+hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const float* Z,
+                             const int32_t* ids, const void* E, const void* U, void* Y,
+                             hipStream_t st);
+// count matrices W[b] [d, n[b]] sharing U [d, k], re-projected in place.
+hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t* n, int64_t k,
+                                  void* const* W, const void* U, hipStream_t st);
+
+}  // namespace ssn

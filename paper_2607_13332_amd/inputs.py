@@ -218,6 +218,11 @@ def codec_inputs_host(cfg: CodecConfig, basis: str = "gaussian") -> Dict[str, np
     return out
 
 
+def coords_host(N: int, k: int, seed: int) -> np.ndarray:
+    """float32 N(0,1) coordinates Z [N, k] (inputs of decompress / expansion)."""
+    return rng(seed, "Z0").standard_normal((N, k), dtype=np.float32)
+
+
 def weights_host(d: int, n: int, seed: int, dtype: str = "bf16", std: float = 0.02) -> np.ndarray:
     return store(std * rng(seed, "W").standard_normal((d, n), dtype=np.float32), dtype)
 
@@ -269,6 +274,12 @@ def codec_inputs_device(cfg: CodecConfig, device, need=("U", "E", "ids", "X", "G
             g = _gen(device, cfg.seed, key)
             out[key] = torch.randn((cfg.N, cfg.d), generator=g, device=device).to(tdt)
     return out
+
+
+def coords_device(N: int, k: int, seed: int, device):
+    """float32 N(0,1) coordinates Z [N, k] drawn on the device."""
+    import torch
+    return torch.randn((N, k), generator=_gen(device, seed, "Z0"), device=device)
 
 
 def weights_device(d: int, n: int, seed: int, device, dtype: str = "bf16", std: float = 0.02):

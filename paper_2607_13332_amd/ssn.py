@@ -1,0 +1,213 @@
+"""Thin ctypes binding over libssn.so (the C ABI declared in include/ssn.h).
+
+Argument marshalling only: dtype / shape / device checks on torch tensors,
+device pointers and the current HIP stream go to the C entry points, and every
+step of the computation runs in the library's HIP kernels.  There is no
+fallback: if libssn.so is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libssn.so")
+
+SSN_F32, SSN_BF16 = 0, 1
+OPS = {"compress": 0, "decompress": 1, "project_grad": 2, "project_weights": 3}
+MAX_BATCH = 16
+
+_c_i64 = ctypes.c_int64
+_c_p = ctypes.c_void_p
+
+
+class SSNError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn} failed with status {status} ({msg})")
+        self.status = status
+
+
+def _declare(lib):
+    lib.ssn_abi_version.restype = ctypes.c_int
+    lib.ssn_abi_version.argtypes = []
+    lib.ssn_status_string.restype = ctypes.c_char_p
+    lib.ssn_status_string.argtypes = [ctypes.c_int]
+    lib.ssn_kernel_family.restype = ctypes.c_char_p
+    lib.ssn_kernel_family.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64]
+    lib.ssn_compress.restype = ctypes.c_int
+    lib.ssn_compress.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
+                                 _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_decompress.restype = ctypes.c_int
+    lib.ssn_decompress.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
+                                   _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_project_grad.restype = ctypes.c_int
+    lib.ssn_project_grad.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_project_weights.restype = ctypes.c_int
+    lib.ssn_project_weights.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]
+    lib.ssn_project_weights_batched.restype = ctypes.c_int
+    lib.ssn_project_weights_batched.argtypes = [ctypes.c_int, _c_i64, _c_i64,
+                                                ctypes.POINTER(_c_i64), _c_i64,
+                                                ctypes.POINTER(_c_p), _c_p, _c_p]
+    return lib
+
+
+_lib = None
+
+
+def lib():
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2607_13332_amd.build`")
+        _lib = _declare(ctypes.CDLL(LIB_PATH))
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().ssn_status_string(status).decode()
+
+
+def kernel_family(op: str, dtype, d: int, k: int) -> str:
+    return lib().ssn_kernel_family(OPS[op], _dt_code(dtype), d, k).decode()
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise SSNError(fn, status, status_string(status))
+
+
+def _dt_code(dtype) -> int:
+    if dtype in (torch.bfloat16, "bf16", SSN_BF16):
+        return SSN_BF16
+    if dtype in (torch.float32, "f32", SSN_F32):
+        return SSN_F32
+    raise TypeError(f"unsupported storage dtype {dtype}")
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (the codec has no CPU path)")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
+    return t.data_ptr()
+
+
+def _same_device(*ts):
+    devs = {t.device for t in ts if t is not None}
+    if len(devs) > 1:
+        raise ValueError(f"tensors are on different devices: {devs}")
+
+
+def compress(X: torch.Tensor, ids: torch.Tensor, E: torch.Tensor, U: torch.Tensor,
+             out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Z = (X - E[ids]) U  (float32 [N, k])."""
+    N, d = X.shape
+    V, k = E.shape[0], U.shape[1]
+    if E.shape[1] != d or U.shape[0] != d or ids.shape != (N,):
+        raise ValueError(f"shape mismatch X{tuple(X.shape)} ids{tuple(ids.shape)} "
+                         f"E{tuple(E.shape)} U{tuple(U.shape)}")
+    if out is None:
+        out = torch.empty((N, k), dtype=torch.float32, device=X.device)
+    _same_device(X, ids, E, U, out)
+    t = X.dtype
+    _check("ssn_compress", lib().ssn_compress(
+        _dt_code(t), N, d, k, V, _dev(X, "X", t, 2), _dev(ids, "ids", torch.int32, 1),
+        _dev(E, "E", t, 2), _dev(U, "U", t, 2), _dev(out, "out", torch.float32, 2), _stream(stream)))
+    return out
+
+
+def decompress(Z: torch.Tensor, ids: Optional[torch.Tensor], E: Optional[torch.Tensor],
+               U: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """X' = E[ids] + Z U^T (storage dtype of U); with ids = E = None, Z U^T."""
+    N, k = Z.shape
+    d = U.shape[0]
+    if U.shape[1] != k:
+        raise ValueError(f"shape mismatch Z{tuple(Z.shape)} U{tuple(U.shape)}")
+    if (E is None) != (ids is None):
+        raise ValueError("pass both ids and E, or neither")
+    t = U.dtype
+    V = 0
+    if E is not None:
+        V = E.shape[0]
+        if E.shape[1] != d or ids.shape != (N,):
+            raise ValueError(f"shape mismatch E{tuple(E.shape)} ids{tuple(ids.shape)}")
+    if out is None:
+        out = torch.empty((N, d), dtype=t, device=Z.device)
+    _same_device(Z, ids, E, U, out)
+    _check("ssn_decompress", lib().ssn_decompress(
+        _dt_code(t), N, d, k, V, _dev(Z, "Z", torch.float32, 2),
+        None if ids is None else _dev(ids, "ids", torch.int32, 1),
+        None if E is None else _dev(E, "E", t, 2), _dev(U, "U", t, 2),
+        _dev(out, "out", t, 2), _stream(stream)))
+    return out
+
+
+def expand_grad(GZ: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """Sender-side gradient G_Z U^T (decompress without the embedding)."""
+    return decompress(GZ, None, None, U, out=out, stream=stream)
+
+
+def project_grad(G: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] = None,
+                 stream=None) -> torch.Tensor:
+    """G_Z = G U (float32 [N, k])."""
+    N, d = G.shape
+    k = U.shape[1]
+    if U.shape[0] != d:
+        raise ValueError(f"shape mismatch G{tuple(G.shape)} U{tuple(U.shape)}")
+    if out is None:
+        out = torch.empty((N, k), dtype=torch.float32, device=G.device)
+    _same_device(G, U, out)
+    t = G.dtype
+    _check("ssn_project_grad", lib().ssn_project_grad(
+        _dt_code(t), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2),
+        _dev(out, "out", torch.float32, 2), _stream(stream)))
+    return out
+
+
+def project_weights(W: torch.Tensor, U: torch.Tensor, stream=None) -> torch.Tensor:
+    """In place: W <- U (U^T W) for W [d, n]."""
+    d, n = W.shape
+    if U.shape[0] != d:
+        raise ValueError(f"shape mismatch W{tuple(W.shape)} U{tuple(U.shape)}")
+    _same_device(W, U)
+    t = W.dtype
+    _check("ssn_project_weights", lib().ssn_project_weights(
+        _dt_code(t), d, n, U.shape[1], _dev(W, "W", t, 2), _dev(U, "U", t, 2), _stream(stream)))
+    return W
+
+
+def project_weights_batched(Ws: Sequence[torch.Tensor], U: torch.Tensor, stream=None):
+    """In place, one launch: W <- U (U^T W) for every W [d, n_b] in Ws."""
+    count = len(Ws)
+    if not 1 <= count <= MAX_BATCH:
+        raise ValueError(f"1 <= len(Ws) <= {MAX_BATCH}")
+    d, k = U.shape
+    t = U.dtype
+    ns = (_c_i64 * count)()
+    ps = (_c_p * count)()
+    for b, W in enumerate(Ws):
+        if W.dim() != 2 or W.shape[0] != d:
+            raise ValueError(f"W[{b}] has shape {tuple(W.shape)}, expected ({d}, n)")
+        ns[b] = W.shape[1]
+        ps[b] = _dev(W, f"W[{b}]", t, 2)
+    _same_device(U, *Ws)
+    _check("ssn_project_weights_batched", lib().ssn_project_weights_batched(
+        _dt_code(t), count, d, ns, k, ps, _dev(U, "U", t, 2), _stream(stream)))
+    return Ws

@@ -1,0 +1,151 @@
+"""CPU checks of the C ABI: the library loads, exports every symbol that
+include/ssn.h declares, and rejects bad arguments on the host before any HIP
+call (fake device addresses are never dereferenced on these paths)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ssn.h")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_ALIGN, ERR_UNSUPPORTED, ERR_LAUNCH, ERR_ALIAS = range(8)
+
+
+@pytest.fixture(scope="module")
+def ssn():
+    from paper_2607_13332_amd import ssn as mod
+    if not os.path.exists(mod.LIB_PATH):
+        from paper_2607_13332_amd import build
+        build.build(verbose=False)
+    mod.lib()
+    return mod
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ssn_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_four_codec_operations():
+    names = declared_functions()
+    for n in ("ssn_compress", "ssn_decompress", "ssn_project_grad", "ssn_project_weights"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(ssn):
+    out = subprocess.run(["nm", "-D", "--defined-only", ssn.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(l.split()[-1] for l in out.splitlines() if l.strip())
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+    for n in declared_functions():
+        assert hasattr(ssn.lib(), n)
+
+
+def test_version_and_status_strings(ssn):
+    L = ssn.lib()
+    assert L.ssn_abi_version() == 1
+    assert L.ssn_status_string(OK) == b"ok"
+    assert L.ssn_status_string(ERR_ALIAS) == b"output overlaps an input"
+    assert L.ssn_status_string(99) == b"unknown status"
+
+
+def test_kernel_family_rules(ssn):
+    kf = ssn.kernel_family
+    assert kf("compress", "bf16", 4096, 64) == "mfma"
+    assert kf("compress", "bf16", 4096, 128) == "mfma"
+    assert kf("compress", "bf16", 4096, 129) == "generic"
+    assert kf("compress", "bf16", 4100, 64) == "generic"
+    assert kf("compress", "f32", 256, 8) == "generic"
+    assert kf("project_grad", "bf16", 2048, 32) == "mfma"
+    assert kf("decompress", "bf16", 4096, 64) == "mfma"
+    assert kf("decompress", "bf16", 4096, 51) == "generic"
+    assert kf("decompress", "bf16", 4064, 64) == "generic"
+    assert kf("project_weights", "bf16", 4096, 64) == "mfma"
+    assert kf("project_weights", "f32", 4096, 64) == "generic"
+    assert ssn.lib().ssn_kernel_family(9, 1, 4096, 64) == b"invalid"
+
+
+# Fake, never-dereferenced device addresses (16-byte aligned, far apart).
+A = 0x7F0000000000
+B = 0x7F1000000000
+C = 0x7F2000000000
+D = 0x7F3000000000
+F = 0x7F4000000000
+
+
+def test_compress_validation(ssn):
+    f = ssn.lib().ssn_compress
+    assert f(7, 10, 64, 8, 100, A, B, C, D, F, None) == ERR_DTYPE
+    assert f(1, -1, 64, 8, 100, A, B, C, D, F, None) == ERR_SHAPE
+    assert f(1, 10, 64, 65, 100, A, B, C, D, F, None) == ERR_SHAPE      # k > d
+    assert f(1, 10, 64, 0, 100, A, B, C, D, F, None) == ERR_SHAPE
+    assert f(1, 10, 64, 8, 0, A, B, C, D, F, None) == ERR_SHAPE        # V < 1
+    assert f(1, 1 << 40, 1 << 30, 8, 100, A, B, C, D, F, None) == ERR_SHAPE   # overflow
+    assert f(1, 0, 64, 8, 100, None, None, None, None, None, None) == OK   # N == 0 no-op
+    assert f(1, 10, 64, 8, 100, None, B, C, D, F, None) == ERR_NULL
+    assert f(1, 10, 64, 8, 100, A, B, C, D, None, None) == ERR_NULL
+    assert f(1, 10, 64, 8, 100, A + 1, B, C, D, F, None) == ERR_ALIGN   # bf16 needs 2 B
+    assert f(0, 10, 64, 8, 100, A + 2, B, C, D, F, None) == ERR_ALIGN   # fp32 needs 4 B
+    assert f(1, 10, 64, 8, 100, A, B + 2, C, D, F, None) == ERR_ALIGN   # ids int32
+    # Z overlapping X / U / E
+    assert f(1, 10, 64, 8, 100, A, B, C, D, A + 64, None) == ERR_ALIAS
+    assert f(1, 10, 64, 8, 100, A, B, C, D, D + 16, None) == ERR_ALIAS
+    assert f(1, 10, 64, 8, 100, A, B, C, D, C + 100 * 64 * 2 - 4, None) == ERR_ALIAS
+
+
+def test_decompress_validation(ssn):
+    f = ssn.lib().ssn_decompress
+    assert f(1, 10, 64, 8, 100, A, B, None, D, F, None) == ERR_NULL     # ids without E
+    assert f(1, 10, 64, 8, 100, A, None, C, D, F, None) == ERR_NULL     # E without ids
+    assert f(1, 0, 64, 8, 100, None, None, None, None, None, None) == OK
+    assert f(1, 0, 64, 8, 100, None, None, C, None, None, None) == OK   # empty ids tensor
+    assert f(1, 10, 64, 8, 0, A, B, C, D, F, None) == ERR_SHAPE         # V < 1 with E
+    assert f(1, 10, 64, 80, 100, A, B, C, D, F, None) == ERR_SHAPE
+    assert f(1, 10, 64, 8, 100, A, B, C, D, A + 16, None) == ERR_ALIAS  # out overlaps Z
+    assert f(1, 10, 64, 8, 100, A, B, C, D, F + 1, None) == ERR_ALIGN
+    assert f(2, 10, 64, 8, 100, A, B, C, D, F, None) == ERR_DTYPE
+
+
+def test_project_grad_validation(ssn):
+    f = ssn.lib().ssn_project_grad
+    assert f(1, 0, 64, 8, None, None, None, None) == OK
+    assert f(1, 10, 64, 8, None, D, F, None) == ERR_NULL
+    assert f(1, 10, 64, 100, A, D, F, None) == ERR_SHAPE
+    assert f(1, 10, 64, 8, A, D, A + 8, None) == ERR_ALIAS
+
+
+def test_project_weights_validation(ssn):
+    L = ssn.lib()
+    f = L.ssn_project_weights
+    assert f(1, 64, 0, 8, None, None, None) == OK
+    assert f(1, 64, 10, 8, None, D, None) == ERR_NULL
+    assert f(1, 64, 10, 0, A, D, None) == ERR_SHAPE
+    assert f(1, 4096, 10, 2048, A, D, None) == ERR_UNSUPPORTED          # k > 1024
+    assert f(1, 64, 10, 8, A, A + 64, None) == ERR_ALIAS                # W overlaps U
+    assert f(1, 64, 10, 8, A + 1, D, None) == ERR_ALIGN
+    g = L.ssn_project_weights_batched
+    n = (ctypes.c_int64 * 2)(16, 16)
+    w = (ctypes.c_void_p * 2)(A, A + 64)                                  # overlapping matrices
+    assert g(1, 2, 64, n, 8, w, D, None) == ERR_ALIAS
+    assert g(1, 0, 64, n, 8, w, D, None) == ERR_SHAPE
+    assert g(1, 17, 64, n, 8, w, D, None) == ERR_SHAPE
+    assert g(1, 2, 64, None, 8, w, D, None) == ERR_NULL
+    n0 = (ctypes.c_int64 * 2)(0, 0)
+    assert g(1, 2, 64, n0, 8, w, None, None) == OK                        # all empty: no-op
+
+
+def test_binding_refuses_cpu_tensors_and_missing_library(ssn, monkeypatch):
+    import torch
+    x = torch.zeros(4, 64, dtype=torch.bfloat16)
+    ids = torch.zeros(4, dtype=torch.int32)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        ssn.compress(x, ids, x, torch.zeros(64, 8, dtype=torch.bfloat16))
+    monkeypatch.setattr(ssn, "_lib", None)
+    monkeypatch.setattr(ssn, "LIB_PATH", "/nonexistent/libssn.so")
+    with pytest.raises(RuntimeError, match="not built"):
+        ssn.lib()

@@ -1,0 +1,263 @@
+"""GPU parity: the HIP path (called through the C ABI binding) against the
+float64 oracle on the same seeded inputs.
+
+Bar: relative Frobenius error <= 1e-5 for fp32 storage and <= 2e-2 for bf16
+storage with fp32 accumulation (helpers.TOL), plus the tighter bounds that the
+kernels' own arithmetic guarantees (helpers.DESIGN).  Full-size workloads are
+checked on seeded row / column samples that the oracle computes directly.
+"""
+import numpy as np
+import pytest
+import torch
+
+from helpers import DESIGN, TOL, rand_coords, rel, sample_rows, structured_inputs
+from oracle import ssn_oracle as O
+from paper_2607_13332_amd import inputs as I
+from paper_2607_13332_amd import ssn
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def dev(a, dtype):
+    return I.to_device(a, dtype, DEV)
+
+
+def host(t):
+    return I.to_host(t)
+
+
+def check(name, got, ref, dtype, kind):
+    err = rel(got, ref)
+    print(f"[parity] {name}: rel={err:.3e}", flush=True)
+    assert err <= TOL[dtype], f"{name}: rel {err:.3e} above the parity bar {TOL[dtype]}"
+    assert err <= DESIGN[(dtype, kind)], f"{name}: rel {err:.3e} above design bound"
+    return err
+
+
+def test_library_is_the_in_tree_build():
+    L = ssn.lib()
+    assert L._name == ssn.LIB_PATH
+    assert torch.cuda.is_available()
+    assert "gfx950" in torch.cuda.get_device_properties(0).gcnArchName
+
+
+# ---------------------------------------------------------------- configs 1, 2
+@pytest.mark.parametrize("cfg", [I.TINY, I.MID], ids=lambda c: c.name)
+def test_structured_config_all_ops(cfg):
+    t = cfg.dtype
+    h = structured_inputs(cfg)
+    X, ids, E, U, G = dev(h["X"], t), dev(h["ids"], t), dev(h["E"], t), dev(h["U"], t), dev(h["G"], t)
+    Z = ssn.compress(X, ids, E, U)
+    check(f"{cfg.name} compress", host(Z), O.compress(h["X"], h["ids"], h["E"], h["U"]), t, "f32out")
+    # the structured activation gives back its coordinates up to noise/rounding
+    assert rel(host(Z), h["Z0"]) < 0.05
+    Zin = rand_coords(cfg.N, cfg.k, cfg.seed + 1)
+    Y = ssn.decompress(dev(Zin, "f32"), ids, E, U)
+    kind = "bf16out" if t == "bf16" else "f32out_dec"
+    check(f"{cfg.name} decompress", host(Y), O.decompress(Zin, h["ids"], h["E"], h["U"]), t, kind)
+    GZ = ssn.project_grad(G, U)
+    check(f"{cfg.name} project_grad", host(GZ), O.project_grad(h["G"], h["U"]), t, "f32out")
+    GX = ssn.expand_grad(dev(Zin, "f32"), U)
+    check(f"{cfg.name} expand_grad", host(GX), O.expand_grad(Zin, h["U"]), t, kind)
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- full-size codec
+def _sampled_codec_check(cfg, nsample=384):
+    t = cfg.dtype
+    print(f"[case] {cfg.name} N={cfg.N} d={cfg.d} k={cfg.k} V={cfg.V}", flush=True)
+    inp = I.codec_inputs_device(cfg, DEV)
+    X, ids, E, U, G = inp["X"], inp["ids"], inp["E"], inp["U"], inp["G"]
+    Zin = I.coords_device(cfg.N, cfg.k, cfg.seed, DEV)
+    Z = ssn.compress(X, ids, E, U)
+    Y = ssn.decompress(Zin, ids, E, U)
+    GZ = ssn.project_grad(G, U)
+    GX = ssn.expand_grad(Zin, U)
+    torch.cuda.synchronize()
+    rows = sample_rows(cfg.N, nsample, cfg.seed)
+    r = torch.from_numpy(rows).to(DEV)
+    Xs, Gs, ids_s = host(X[r]), host(G[r]), host(ids[r])
+    Es = host(E.index_select(0, ids[r].long()))
+    Us, Zs = host(U), host(Zin[r])
+    loc = np.arange(len(rows), dtype=np.int32)
+    check(f"{cfg.name} compress", host(Z[r]), O.compress(Xs, loc, Es, Us), t, "f32out")
+    check(f"{cfg.name} decompress", host(Y[r]), O.decompress(Zs, loc, Es, Us), t, "bf16out")
+    check(f"{cfg.name} project_grad", host(GZ[r]), O.project_grad(Gs, Us), t, "f32out")
+    check(f"{cfg.name} expand_grad", host(GX[r]), O.expand_grad(Zs, Us), t, "bf16out")
+    # every row was written (no NaN / untouched garbage anywhere)
+    assert torch.isfinite(Z).all() and torch.isfinite(Y.float()).all()
+    assert torch.isfinite(GZ).all() and torch.isfinite(GX.float()).all()
+    del inp, X, E, G, Z, Y, GZ, GX
+    torch.cuda.empty_cache()
+
+
+def test_stage8b_full_size_sampled():
+    _sampled_codec_check(I.STAGE8B)
+
+
+@pytest.mark.parametrize("cfg", I.sweep_configs(), ids=lambda c: c.name)
+def test_sweep_full_size_sampled(cfg):
+    _sampled_codec_check(cfg, nsample=256)
+
+
+# ---------------------------------------------------------------- config 4
+def test_weight_reprojection_stage_sampled():
+    wc = I.WEIGHTS
+    print(f"[case] {wc.name}", flush=True)
+    U = I.to_device(I.store(I.gaussian_orthonormal_basis(wc.d, wc.k, wc.seed), "bf16"), "bf16", DEV)
+    Ws, cols, before = [], [], []
+    for layer in range(wc.layers):
+        for j, (d, n) in enumerate(wc.shapes):
+            W = I.weights_device(d, n, wc.seed * 100 + 10 * layer + j, DEV)
+            c = sample_rows(n, 96, layer * 7 + j)
+            Ws.append(W)
+            cols.append(c)
+            before.append(host(W[:, torch.from_numpy(c).to(DEV)]))
+    ref_single = [W.clone() for W in Ws[:2]]
+    ssn.project_weights_batched(Ws, U)
+    for W in ref_single:
+        ssn.project_weights(W, U)
+    torch.cuda.synchronize()
+    Uh = host(U)
+    for b, W in enumerate(Ws):
+        got = host(W[:, torch.from_numpy(cols[b]).to(DEV)])
+        check(f"weights matrix {b} {tuple(W.shape)}", got, O.project_weights(before[b], Uh), "bf16", "bf16out")
+    # one launch for the batch gives the same bits as one launch per matrix
+    for b in range(2):
+        assert torch.equal(Ws[b], ref_single[b])
+    # re-projecting a projected matrix moves it by about its own rounding only
+    W2 = Ws[0].clone()
+    ssn.project_weights(W2, U)
+    assert rel(host(W2), O.f64(host(Ws[0]))) < 4e-3
+
+
+# ---------------------------------------------------------------- shape coverage
+CODEC_SHAPES = [  # (N, d, k): tiles, ragged tails, every k bucket, both families
+    (1, 256, 64), (17, 256, 64), (1000, 160, 40), (333, 96, 17), (77, 4128, 128),
+    (50, 512, 1), (64, 512, 15), (65, 512, 16), (300, 512, 48), (129, 512, 129),
+    (200, 100, 10), (10, 2048, 51), (4099, 1024, 96), (70, 4096, 24), (33, 128, 8),
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("N,d,k", CODEC_SHAPES)
+def test_codec_shapes(N, d, k, dtype):
+    V = 97
+    seed = N * 131 + d * 7 + k
+    print(f"[case] codec N={N} d={d} k={k} {dtype} families="
+          f"{ssn.kernel_family('compress', dtype, d, k)}/{ssn.kernel_family('decompress', dtype, d, k)}",
+          flush=True)
+    r = np.random.default_rng(seed)
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), dtype)
+    Eh = I.store(0.02 * r.standard_normal((V, d)), dtype)
+    Xh = I.store(r.standard_normal((N, d)), dtype)
+    ids_h = r.integers(0, V, size=N).astype(np.int32)
+    ids_h[0] = 0
+    ids_h[-1] = V - 1
+    Zin = rand_coords(N, k, seed)
+    X, E, U, ids = dev(Xh, dtype), dev(Eh, dtype), dev(Uh, dtype), dev(ids_h, dtype)
+    outkind = "bf16out" if dtype == "bf16" else "f32out_dec"
+    check("compress", host(ssn.compress(X, ids, E, U)), O.compress(Xh, ids_h, Eh, Uh), dtype, "f32out")
+    check("project_grad", host(ssn.project_grad(X, U)), O.project_grad(Xh, Uh), dtype, "f32out")
+    check("decompress", host(ssn.decompress(dev(Zin, "f32"), ids, E, U)),
+          O.decompress(Zin, ids_h, Eh, Uh), dtype, outkind)
+    check("expand_grad", host(ssn.expand_grad(dev(Zin, "f32"), U)), O.expand_grad(Zin, Uh), dtype, outkind)
+
+
+WEIGHT_SHAPES = [  # (d, n, k)
+    (256, 1, 64), (256, 100, 64), (512, 200, 40), (4096, 64, 128), (512, 197, 8), (96, 70, 32),
+    (128, 300, 51), (64, 33, 16), (2048, 130, 96), (1024, 4096, 64),
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("d,n,k", WEIGHT_SHAPES)
+def test_weight_shapes(d, n, k, dtype):
+    seed = d * 3 + n * 5 + k
+    print(f"[case] weights d={d} n={n} k={k} {dtype} family="
+          f"{ssn.kernel_family('project_weights', dtype, d, k)}", flush=True)
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), dtype)
+    Wh = I.weights_host(d, n, seed, dtype)
+    W = dev(Wh, dtype)
+    ssn.project_weights(W, dev(Uh, dtype))
+    check("project_weights", host(W), O.project_weights(Wh, Uh), dtype,
+          "bf16out" if dtype == "bf16" else "f32out")
+
+
+# ---------------------------------------------------------------- exact cases
+@pytest.mark.parametrize("d,k", [(4096, 64), (256, 8), (100, 10)])
+def test_exact_special_cases(d, k):
+    """compress(E[ids]) == 0 and decompress(0) == E[ids] bitwise; a selection
+    basis reproduces the selected coordinates exactly."""
+    N, V = 300, 50
+    r = np.random.default_rng(d + k)
+    Eh = I.store(0.02 * r.standard_normal((V, d)), "bf16")
+    ids_h = r.integers(0, V, size=N).astype(np.int32)
+    U = dev(I.store(I.gaussian_orthonormal_basis(d, k, 3), "bf16"), "bf16")
+    E, ids = dev(Eh, "bf16"), dev(ids_h, "bf16")
+    Xe = E[ids.long()].contiguous()
+    Z = ssn.compress(Xe, ids, E, U)
+    assert torch.count_nonzero(Z).item() == 0
+    Y = ssn.decompress(torch.zeros((N, k), device=DEV), ids, E, U)
+    assert np.array_equal(host(Y), Eh[ids_h])
+    # selection basis
+    Us = I.selection_basis(d, k, 5)
+    cols = np.argmax(Us, axis=0)
+    Ush = I.store(Us, "bf16")
+    Xh = I.store(r.standard_normal((N, d)), "bf16")
+    Zs = host(ssn.compress(dev(Xh, "bf16"), ids, E, dev(Ush, "bf16")))
+    ref = (O.f64(Xh) - O.f64(Eh)[ids_h])[:, cols].astype(np.float32)
+    assert np.array_equal(Zs, ref)
+    Wh = I.weights_host(d, 70, 9, "bf16")
+    W = dev(Wh, "bf16")
+    ssn.project_weights(W, dev(Ush, "bf16"))
+    want = np.zeros_like(Wh)
+    want[cols] = Wh[cols]
+    assert np.array_equal(host(W), want)
+
+
+def test_empty_batch_is_a_no_op():
+    U = torch.randn(256, 64, device=DEV).to(torch.bfloat16)
+    X = torch.empty((0, 256), device=DEV, dtype=torch.bfloat16)
+    ids = torch.empty((0,), device=DEV, dtype=torch.int32)
+    E = torch.randn(10, 256, device=DEV).to(torch.bfloat16)
+    Z = ssn.compress(X, ids, E, U)
+    assert Z.shape == (0, 64)
+    Y = ssn.decompress(torch.empty((0, 64), device=DEV), ids, E, U)
+    assert Y.shape == (0, 256)
+    W = torch.empty((256, 0), device=DEV, dtype=torch.bfloat16)
+    ssn.project_weights(W, U)
+    torch.cuda.synchronize()
+
+
+def test_non_default_stream_and_determinism():
+    cfg = I.with_tokens(I.MID, 4096)
+    h = structured_inputs(cfg)
+    t = cfg.dtype
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        X, ids, E, U = dev(h["X"], t), dev(h["ids"], t), dev(h["E"], t), dev(h["U"], t)
+        Z1 = ssn.compress(X, ids, E, U)
+        Z2 = ssn.compress(X, ids, E, U, stream=s)
+        Y1 = ssn.decompress(Z1, ids, E, U)
+    s.synchronize()
+    assert torch.equal(Z1, Z2)
+    check("stream compress", host(Z1), O.compress(h["X"], h["ids"], h["E"], h["U"]), t, "f32out")
+    Z1h = host(Z1)
+    check("stream decompress", host(Y1), O.decompress(Z1h, h["ids"], h["E"], h["U"]), t, "bf16out")
+
+
+def test_cross_op_consistency():
+    """compress(X) == project_grad(X) - project_grad(E[ids]) within fp32 rounding."""
+    N, d, k, V = 2048, 4096, 64, 1000
+    r = np.random.default_rng(77)
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, 77), "bf16")
+    Eh = I.store(0.02 * r.standard_normal((V, d)), "bf16")
+    Xh = I.store(r.standard_normal((N, d)), "bf16")
+    ids_h = r.integers(0, V, size=N).astype(np.int32)
+    X, E, U, ids = dev(Xh, "bf16"), dev(Eh, "bf16"), dev(Uh, "bf16"), dev(ids_h, "bf16")
+    Z = ssn.compress(X, ids, E, U)
+    P = ssn.project_grad(X, U) - ssn.project_grad(E[ids.long()].contiguous(), U)
+    assert rel(host(Z), host(P)) < 1e-6
