@@ -56,6 +56,9 @@ def parse_args():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle baseline sample")
     p.add_argument("--tokens", type=int, default=0, help="override N (testing only)")
+    p.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
+                   help="before the timed region, run a plain device copy of MIB MiB three times "
+                        "(a known-size kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     return p.parse_args()
 
 
@@ -163,6 +166,14 @@ def main():
         ssn.expand_grad(s["GZin"], U, out=s["GX"])
         if evs is not None:
             evs[4].record()
+
+    if args.copy_calib:
+        src = torch.empty(args.copy_calib << 20, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for i in range(args.warmup):
         step(sets[i % 2])

@@ -76,6 +76,64 @@ __device__ __forceinline__ void store_from_f32<float>(float* p, float v) { *p = 
 template <>
 __device__ __forceinline__ void store_from_f32<uint16_t>(uint16_t* p, float v) { *p = (uint16_t)f32_to_bf16(v); }
 
+// Loads the 8 x KP bf16 block M[row0 .. row0+7][col0 .. col0+KP-1] of a
+// row-major matrix with `ld` columns into packed dwords (two columns per
+// dword).  FULL: the block never crosses column `ncols` and rows are aligned
+// for vector loads (ld == 16*KP-style layouts); otherwise each element is
+// loaded under a bounds predicate and missing columns read as zero.
+template <int KP, bool FULL>
+__device__ __forceinline__ void load_block8(const uint16_t* __restrict__ M, int64_t row0, int col0,
+                                            int ld, int ncols, uint32_t (&w)[8][(KP + 1) / 2]) {
+  constexpr int KW = (KP + 1) / 2;
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const uint16_t* p = M + (row0 + r) * (int64_t)ld + col0;
+    if constexpr (FULL && KP == 8) {
+      const u32x4 v = *(const u32x4*)p;
+      w[r][0] = v[0]; w[r][1] = v[1]; w[r][2] = v[2]; w[r][3] = v[3];
+    } else if constexpr (FULL && KP == 4) {
+      const u32x2 v = *(const u32x2*)p;
+      w[r][0] = v[0]; w[r][1] = v[1];
+    } else if constexpr (FULL && (KP % 2) == 0) {
+#pragma unroll
+      for (int q = 0; q < KW; ++q) w[r][q] = ((const uint32_t*)p)[q];
+    } else {
+#pragma unroll
+      for (int q = 0; q < KW; ++q) {
+        const uint32_t lo = (col0 + 2 * q < ncols) ? (uint32_t)p[2 * q] : 0u;
+        const uint32_t hi = (2 * q + 1 < KP && col0 + 2 * q + 1 < ncols) ? (uint32_t)p[2 * q + 1] : 0u;
+        w[r][q] = lo | (hi << 16);
+      }
+    }
+  }
+}
+
+// Column i of a block loaded by load_block8, as one MFMA operand fragment:
+// 8 consecutive rows of that column, two bf16 per dword.
+template <int KP>
+__device__ __forceinline__ u32x4 block8_column(const uint32_t (&w)[8][(KP + 1) / 2], int i) {
+  uint32_t f[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const uint32_t a = w[2 * m][i >> 1], b = w[2 * m + 1][i >> 1];
+    f[m] = (i & 1) ? ((a >> 16) | (b & 0xFFFF0000u)) : ((a & 0xFFFFu) | (b << 16));
+  }
+  return u32x4{f[0], f[1], f[2], f[3]};
+}
+
+// 16-byte global load / store; NT marks streaming data (non-temporal hint) so
+// that it does not displace data the kernel re-reads from L2.
+template <bool NT>
+__device__ __forceinline__ u32x4 ldg(const uint16_t* p) {
+  if constexpr (NT) return __builtin_nontemporal_load((const u32x4*)p);
+  else return *(const u32x4*)p;
+}
+template <bool NT>
+__device__ __forceinline__ void stg(uint16_t* p, u32x4 v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, (u32x4*)p);
+  else *(u32x4*)p = v;
+}
+
 __device__ __forceinline__ int64_t clamp_id(int32_t id, int64_t V) {
   int64_t i = id;
   return i < 0 ? 0 : (i >= V ? V - 1 : i);
