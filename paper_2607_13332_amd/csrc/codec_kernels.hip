@@ -166,44 +166,181 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
 }
 
 // ===========================================================================
-// decompress / gradient expansion, bf16 storage, MFMA.
+// compress / project_grad, variant with row-contiguous activation loads.
 //
-// Computes Y^T tiles [16 d x 16 tokens] = U_rows [16 d x k] . Z^T [k x 16 tok]
-// so that U is used in its natural [d][k] layout (A fragment = 16 contiguous
-// bytes of one U row) and Z rows are B fragments.  Z (fp32) is split into bf16
-// hi + lo parts, two MFMAs each, which keeps ~fp32 accuracy.  The accumulator
-// starts from E[ids] (widened to fp32) -- the embedding add is fused and the
-// result is rounded to bf16 once.
-//
-// Block = 4 waves sharing 16*TG tokens; the waves split d in steps of 64
-// (wave w takes steps w, w+4, ...).  A 64-wide d step uses 4 MFMA tiles whose
-// rows are permuted so that lane (token n, group g) ends with d offsets
-// 8g..8g+7 (tiles 0, 1) and 32+8g..32+8g+7 (tiles 2, 3) of one token: each
-// E load and Y store instruction then covers 64 contiguous bytes of 16 rows.  The U fragments and E values of the
-// wave's next step are loaded while the current step computes (two register
-// buffers).
+// Same MFMA scheme as compress_mfma_bf16 (U staged per 128-wide d chunk in
+// B-fragment order, X.U and E[ids].U in separate fp32 accumulators), but each
+// wave loads its 16 X rows and 16 E[ids] rows for a chunk as 4 instructions
+// of 4 rows x 256 contiguous bytes (8 whole 128-byte lines per instruction,
+// instead of 16 half lines), parks them in a wave-private XOR-swizzled LDS
+// tile, and reads its A fragments from there.  The next chunk's rows are
+// loaded into registers while the current chunk computes.
 // ===========================================================================
-template <int KS2, int TG, bool HAS_E, bool KFULL32, bool ROT = false, bool NT = false>
-__global__ __launch_bounds__(256) void decompress_mfma_bf16(
-    const float* __restrict__ Zc, const int32_t* __restrict__ ids,
+template <int KP, bool HAS_E, bool KFULL, int WAVES = 8>
+__global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
+    const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
-    uint16_t* __restrict__ Y, int64_t N, int d, int k, int64_t V) {
+    float* __restrict__ Z, int64_t N, int d, int k, int64_t V) {
+  constexpr int KS = 4, DC = 128;
+  constexpr int KW = (KP + 1) / 2;
+  constexpr int TASKS = KS * kWave;              // U staging tasks per chunk (256)
+  __shared__ u32x4 lds[2][KS * KP * kWave];      // U B fragments, double buffered
+  __shared__ u32x4 tile[WAVES][HAS_E ? 2 : 1][16 * 16];   // [wave][X/E][row * 16 + cell ^ row]
+
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int n16 = lane & 15, g = lane >> 4;
-  const int64_t tokb = (int64_t)blockIdx.x * (16 * TG);
+  const int64_t tok0 = ((int64_t)blockIdx.x * WAVES + wave) * 16;
 
-  u32x4 zhi[TG][KS2], zlo[TG][KS2];
-  const uint16_t* erow[TG];
-  uint16_t* yrow[TG];
-  bool tok_ok[TG];
+  // row-contiguous loads: instruction i covers rows 4i + lane/16, cell lane%16
+  const int lc = lane & 15;
+  const uint16_t* xr[4];
+  const uint16_t* er[4];
 #pragma unroll
-  for (int tg = 0; tg < TG; ++tg) {
-    int64_t t = tokb + tg * 16 + n16;
-    tok_ok[tg] = t < N;
+  for (int i = 0; i < 4; ++i) {
+    const int r = 4 * i + (lane >> 4);
+    int64_t t = tok0 + r;
     t = t < N ? t : N - 1;
-    yrow[tg] = Y + t * d + 8 * g;
-    erow[tg] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * g : nullptr;
+    xr[i] = X + t * d + 8 * lc;
+    er[i] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * lc : nullptr;
+  }
+  u32x4 xv[4], ev[4];
+  auto load_rows = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      xv[i] = *(const u32x4*)(xr[i] + c * DC);
+      if constexpr (HAS_E) ev[i] = *(const u32x4*)(er[i] + c * DC);
+    }
+  };
+  u32x4* tx = tile[wave][0];
+  u32x4* te = tile[wave][HAS_E ? 1 : 0];
+  auto park_rows = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * i + (lane >> 4);
+      tx[r * 16 + (lc ^ r)] = xv[i];
+      if constexpr (HAS_E) te[r * 16 + (lc ^ r)] = ev[i];
+    }
+  };
+
+  const bool stager = tid < TASKS;
+  const int srow = 32 * (tid >> 6) + 8 * ((tid >> 4) & 3);
+  const int scol = (tid & 15) * KP;
+  const int sidx = (tid >> 6) * KP * kWave + (tid & 63);
+  uint32_t uw[8][KW];
+  auto load_u = [&](int c) {
+    if (stager) load_block8<KP, KFULL>(U, (int64_t)c * DC + srow, scol, k, k, uw);
+  };
+  auto store_u = [&](int buf) {
+    if (stager) {
+#pragma unroll
+      for (int i = 0; i < KP; ++i) lds[buf][sidx + i * kWave] = block8_column<KP>(uw, i);
+    }
+  };
+
+  f32x4 accX[KP], accE[KP];
+#pragma unroll
+  for (int i = 0; i < KP; ++i) {
+    accX[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    accE[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const int nch = d / DC;
+  load_rows(0);
+  load_u(0);
+  store_u(0);
+  for (int c = 0; c < nch; ++c) {
+    park_rows();
+    const int cn = c + 1 < nch ? c + 1 : c;
+    load_rows(cn);
+    load_u(cn);
+    __syncthreads();
+    const u32x4* fr = lds[c & 1];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int cell = (4 * s + g) ^ n16;
+      const u32x4 xa = tx[n16 * 16 + cell];
+      u32x4 ea;
+      if constexpr (HAS_E) ea = te[n16 * 16 + cell];
+      u32x4 bfr[KP];
+#pragma unroll
+      for (int i = 0; i < KP; ++i) bfr[i] = fr[(s * KP + i) * kWave + lane];
+#pragma unroll
+      for (int i = 0; i < KP; ++i) {
+        accX[i] = mfma16x16x32(xa, bfr[i], accX[i]);
+        if constexpr (HAS_E) accE[i] = mfma16x16x32(ea, bfr[i], accE[i]);
+      }
+    }
+    store_u((c + 1) & 1);
+  }
+
+  const int col0 = n16 * KP;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t tj = tok0 + 4 * g + j;
+    if (tj < N) {
+      float v[KP];
+#pragma unroll
+      for (int i = 0; i < KP; ++i) v[i] = HAS_E ? accX[i][j] - accE[i][j] : accX[i][j];
+      float* zp = Z + tj * k + col0;
+      if constexpr (KFULL && KP % 4 == 0) {
+#pragma unroll
+        for (int i = 0; i < KP; i += 4) *(f32x4*)(zp + i) = f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
+      } else {
+#pragma unroll
+        for (int i = 0; i < KP; ++i)
+          if (col0 + i < k) zp[i] = v[i];
+      }
+    }
+  }
+}
+
+// ===========================================================================
+// decompress / gradient expansion, bf16 storage, MFMA.
+//
+// Computes Y^T tiles [16 d x 16 tokens] = U_rows [16 d x k] . Z^T [k x 16 tok]
+// so that U is used in its natural [d][k] layout (an A fragment is 16
+// contiguous bytes of one U row) and Z rows are B fragments.  Z (fp32) is
+// split into bf16 hi + lo parts, two MFMAs each, which keeps ~fp32 accuracy.
+//
+// Block = 4 waves x 16 tokens.  d is walked in 128-wide chunks, every block
+// starting at its own rotated offset (spreads concurrent requests over HBM
+// channels).  Per chunk the 256 threads stage the chunk's U rows into LDS in
+// A-fragment order (double buffered, one barrier per chunk); each wave runs 8
+// MFMA tiles for its 16 tokens and parks the fp32 results in a wave-private,
+// XOR-swizzled LDS tile [16 tokens x 128 d].  The epilogue then reads that
+// tile back row-wise, adds E[ids] (loaded one chunk ahead, 256 contiguous
+// bytes of 4 rows per load instruction), rounds once to bf16, and stores 256
+// contiguous bytes of 4 rows per instruction.
+// ===========================================================================
+constexpr int kDecompressDC = 64;
+
+template <int KS2, bool HAS_E, bool KFULL32, int DC = kDecompressDC, int PF = 1, int DSPLIT = 1,
+          int TW = 4>
+__global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
+    const float* __restrict__ Zc, const int32_t* __restrict__ ids,
+    const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
+    uint16_t* __restrict__ Y, int64_t N, int d, int k, int64_t V) {
+  static_assert(DC == 64 || DC == 128, "chunk of 64 or 128 d");
+  constexpr int NT = DC / 16;                     // MFMA tiles per chunk
+  constexpr int FR = NT * KS2 * kWave;            // A fragments per chunk
+  constexpr int PT = 64 * TW;                      // stager threads per part
+  constexpr int FPT = (FR + PT - 1) / PT;         // staged per thread (last round partial)
+  __shared__ u32x4 ufr[2][DSPLIT * FR];           // [buffer][part * FR + fragment]
+  __shared__ f32x4 stage[TW * DSPLIT][16 * (DC / 4)];  // [wave][token * DC/4 + cell ^ token]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int n16 = lane & 15, g = lane >> 4;
+  // wave = part * TW + token tile: DSPLIT parts of d run side by side
+  const int part = wave / TW;
+  const int64_t tok0 = (int64_t)blockIdx.x * (16 * TW) + (wave % TW) * 16;
+
+  // Z^T B fragments of this wave's 16 tokens
+  u32x4 zhi[KS2], zlo[KS2];
+  {
+    int64_t t = tok0 + n16;
+    t = t < N ? t : N - 1;
     const float* zp = Zc + t * k;
 #pragma unroll
     for (int s = 0; s < KS2; ++s) {
@@ -218,82 +355,118 @@ __global__ __launch_bounds__(256) void decompress_mfma_bf16(
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = 0.f;   // k % 8 == 0 on this path
       }
-      split_bf16x8(v, zhi[tg][s], zlo[tg][s]);
+      split_bf16x8(v, zhi[s], zlo[s]);
     }
   }
 
-  const int m4 = n16 >> 2, mr = n16 & 3;
-  // A rows of tile tt: d = dbase + 32*(tt/2) + 8*(n16/4) + 4*(tt%2) + n16%4
-  const uint16_t* ubase = U + (int64_t)(8 * m4 + mr) * k + 8 * g;
-  const int nsteps = d >> 6;
+  // epilogue rows of this lane: LPR lanes per row, each 8 d (16 bytes);
+  // RPI = 64 / LPR rows per store instruction, NQ instructions per chunk
+  constexpr int LPR = DC / 8, RPI = 64 / LPR, NQ = 16 / RPI;
+  const int ec = lane % LPR;
+  const uint16_t* erow[NQ];
+  uint16_t* yrow[NQ];
+  bool ok[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    int64_t t = tok0 + RPI * q + lane / LPR;
+    ok[q] = t < N;
+    t = t < N ? t : N - 1;
+    yrow[q] = Y + t * d + 8 * ec;
+    erow[q] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * ec : nullptr;
+  }
 
-  u32x4 ua[2][4][KS2], ev[2][TG][2];
-  auto load_step = [&](int ds, u32x4(&uo)[4][KS2], u32x4(&eo)[TG][2]) {
-    const int dbase = ds * 64;
+  // U staging: thread tid stages fragments of part tid/PT; fragment
+  // f = tid%PT + PT*q -> tile f/(KS2*64), K step (f/64)%KS2, lane position
+  // f%64 = 16*g' + m: row 16*tile + m, columns 32*s + 8*g'
+  const int spart = tid / PT, stid = tid % PT;
+  int srow[FPT], scol[FPT];
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt) {
-      const uint16_t* up = ubase + (int64_t)(dbase + (tt >= 2 ? 32 : 0) + 4 * (tt & 1)) * k;
+  for (int q = 0; q < FPT; ++q) {
+    const int f = stid + PT * q;
+    const int l = f & 63;
+    srow[q] = 16 * (f / (KS2 * kWave)) + (l & 15);
+    scol[q] = 32 * ((f / kWave) % KS2) + 8 * (l >> 4);
+  }
+  u32x4 ust[FPT];
+  auto load_u = [&](int c) {
 #pragma unroll
-      for (int s = 0; s < KS2; ++s)
-        uo[tt][s] = (KFULL32 || 32 * s + 8 * g < k) ? *(const u32x4*)(up + 32 * s)
-                                                   : u32x4{0u, 0u, 0u, 0u};
-    }
+    for (int q = 0; q < FPT; ++q)
+      if (stid + PT * q < FR)
+        ust[q] = (KFULL32 || scol[q] < k)
+                     ? *(const u32x4*)(U + (int64_t)(c * DC + srow[q]) * k + scol[q])
+                     : u32x4{0u, 0u, 0u, 0u};
+  };
+  auto store_u = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < FPT; ++q)
+      if (stid + PT * q < FR) ufr[buf][spart * FR + stid + PT * q] = ust[q];
+  };
+  u32x4 ering[PF + 1][NQ];
+  auto load_e = [&](int c, u32x4(&eo)[NQ]) {
     if constexpr (HAS_E) {
 #pragma unroll
-      for (int tg = 0; tg < TG; ++tg) {
-        eo[tg][0] = ldg<NT>(erow[tg] + dbase);
-        eo[tg][1] = ldg<NT>(erow[tg] + dbase + 32);
-      }
-    }
-  };
-  auto compute_step = [&](int ds, const u32x4(&ui)[4][KS2], const u32x4(&ei)[TG][2]) {
-    const int dbase = ds * 64;
-#pragma unroll
-    for (int tg = 0; tg < TG; ++tg) {
-      f32x4 acc[4];
-      if constexpr (HAS_E) {
-        const u32x4 e0 = ei[tg][0], e1 = ei[tg][1];
-        acc[0] = f32x4{lo_bf16(e0[0]), hi_bf16(e0[0]), lo_bf16(e0[1]), hi_bf16(e0[1])};
-        acc[1] = f32x4{lo_bf16(e0[2]), hi_bf16(e0[2]), lo_bf16(e0[3]), hi_bf16(e0[3])};
-        acc[2] = f32x4{lo_bf16(e1[0]), hi_bf16(e1[0]), lo_bf16(e1[1]), hi_bf16(e1[1])};
-        acc[3] = f32x4{lo_bf16(e1[2]), hi_bf16(e1[2]), lo_bf16(e1[3]), hi_bf16(e1[3])};
-      } else {
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt) acc[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-        for (int s = 0; s < KS2; ++s) {
-          acc[tt] = mfma16x16x32(ui[tt][s], zhi[tg][s], acc[tt]);
-          acc[tt] = mfma16x16x32(ui[tt][s], zlo[tg][s], acc[tt]);
-        }
-      if (tok_ok[tg]) {
-        const u32x4 o0 = u32x4{pack_bf16x2(acc[0][0], acc[0][1]), pack_bf16x2(acc[0][2], acc[0][3]),
-                               pack_bf16x2(acc[1][0], acc[1][1]), pack_bf16x2(acc[1][2], acc[1][3])};
-        const u32x4 o1 = u32x4{pack_bf16x2(acc[2][0], acc[2][1]), pack_bf16x2(acc[2][2], acc[2][3]),
-                               pack_bf16x2(acc[3][0], acc[3][1]), pack_bf16x2(acc[3][2], acc[3][3])};
-        stg<NT>(yrow[tg] + dbase, o0);
-        stg<NT>(yrow[tg] + dbase + 32, o1);
-      }
+      for (int q = 0; q < NQ; ++q) eo[q] = *(const u32x4*)(erow[q] + c * DC);
     }
   };
 
-  // The block visits the d steps as a rotation of [0, nsteps) starting at its
-  // own offset (spreads concurrent requests over HBM channels); wave w takes
-  // positions w, w+4, ... of that sequence.
-  const int rot = ROT ? (int)(blockIdx.x % (unsigned)nsteps) : 0;
-  auto step_at = [&](int i) { const int x = i + rot; return x < nsteps ? x : x - nsteps; };
-  int i = wave;
-  if (i < nsteps) load_step(step_at(i), ua[0], ev[0]);
-  for (; i < nsteps; i += 8) {
-    const int i1 = i + 4;
-    load_step(step_at(i1 < nsteps ? i1 : i), ua[1], ev[1]);
-    compute_step(step_at(i), ua[0], ev[0]);
-    if (i1 >= nsteps) break;
-    const int i2 = i + 8;
-    load_step(step_at(i2 < nsteps ? i2 : i1), ua[0], ev[0]);
-    compute_step(step_at(i1), ua[1], ev[1]);
+  // part p walks chunks [p*nch, (p+1)*nch) of d (nch per part), rotated
+  const int nch = d / (DC * DSPLIT);
+  const int rot = (int)(blockIdx.x % (unsigned)nch);
+  auto chunk_of = [&](int p, int i) { const int x = i + rot; return p * nch + (x < nch ? x : x - nch); };
+  auto chunk = [&](int i) { return chunk_of(part, i); };
+  f32x4* st = stage[wave];
+
+  // the stager threads of part spart load that part's chunks of U
+  auto load_u_part = [&](int i) { load_u(chunk_of(spart, i)); };
+
+  load_u_part(0);
+  store_u(0);
+#pragma unroll
+  for (int b = 0; b < PF; ++b) load_e(chunk(b < nch ? b : nch - 1), ering[b]);
+  for (int i0 = 0; i0 < nch; i0 += PF + 1) {
+#pragma unroll
+    for (int b = 0; b <= PF; ++b) {
+      const int i = i0 + b;
+      if (i < nch) {
+        const int c = chunk(i);
+        load_u_part(i + 1 < nch ? i + 1 : i);
+        // E of chunk i + PF into the ring slot freed by chunk i - 1
+        load_e(chunk(i + PF < nch ? i + PF : nch - 1), ering[(b + PF) % (PF + 1)]);
+        __syncthreads();
+        const u32x4* fr = ufr[i & 1] + part * FR;
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) {
+          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < KS2; ++s) {
+            const u32x4 a = fr[(tt * KS2 + s) * kWave + lane];
+            acc = mfma16x16x32(a, zhi[s], acc);
+            acc = mfma16x16x32(a, zlo[s], acc);
+          }
+          // lane (token n16, group g) holds d = 16*tt + 4*g + 0..3 of its token
+          st[n16 * (DC / 4) + ((4 * tt + g) ^ n16)] = acc;
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+          const int tl = RPI * q + lane / LPR;
+          const f32x4 a = st[tl * (DC / 4) + ((2 * ec) ^ tl)];
+          const f32x4 bb = st[tl * (DC / 4) + ((2 * ec + 1) ^ tl)];
+          float v[8] = {a[0], a[1], a[2], a[3], bb[0], bb[1], bb[2], bb[3]};
+          if constexpr (HAS_E) {
+            const u32x4 e = ering[b][q];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              v[2 * m] += lo_bf16(e[m]);
+              v[2 * m + 1] += hi_bf16(e[m]);
+            }
+          }
+          if (ok[q])
+            *(u32x4*)(yrow[q] + c * DC) = u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+        }
+        store_u((i + 1) & 1);
+      }
+    }
   }
 }
 
@@ -361,7 +534,7 @@ bool compress_uses_mfma(int dtype, int64_t d, int64_t k) {
 }
 
 bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) {
-  return dtype == kBF16 && d % 64 == 0 && d <= INT32_MAX && k % 8 == 0 && k >= 8 && k <= 128;
+  return dtype == kBF16 && d % (2 * kDecompressDC) == 0 && d <= INT32_MAX && k % 8 == 0 && k >= 8 && k <= 128;
 }
 
 template <int KP, bool HAS_E, bool KFULL, int WAVES, int KS>
@@ -375,13 +548,30 @@ static hipError_t launch_compress_v(int64_t N, int d, int k, int64_t V, const vo
   return hipGetLastError();
 }
 
-// 8 waves (128 tokens) per block share each staged slice of U; d chunks of
-// 256 when d allows, else 128.
+template <int KP, bool KFULL>
+static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const void* X,
+                                       const int32_t* ids, const void* E, const void* U, float* Z,
+                                       hipStream_t st) {
+  constexpr int WAVES = 4;
+  const int64_t blocks = (N + 16 * WAVES - 1) / (16 * WAVES);
+  hipLaunchKernelGGL((compress_rows_bf16<KP, true, KFULL, WAVES>), dim3((unsigned)blocks),
+                     dim3(64 * WAVES), 0, st, (const uint16_t*)X, ids, (const uint16_t*)E,
+                     (const uint16_t*)U, Z, N, d, k, V);
+  return hipGetLastError();
+}
+
+// compress (with the embedding) uses the row-contiguous variant; the gradient
+// projection (one stream) the direct-fragment variant with 8 waves (128
+// tokens) per block sharing each staged slice of U, in 256-d chunks when d
+// allows, else 128.
 template <int KP, bool HAS_E>
 static hipError_t launch_compress_kp(int64_t N, int d, int k, int64_t V, const void* X,
                                      const int32_t* ids, const void* E, const void* U, float* Z,
                                      hipStream_t st) {
   const bool kfull = (k == 16 * KP);
+  if constexpr (HAS_E)
+    return kfull ? launch_compress_rows<KP, true>(N, d, k, V, X, ids, E, U, Z, st)
+                 : launch_compress_rows<KP, false>(N, d, k, V, X, ids, E, U, Z, st);
   if (d % 256 == 0)
     return kfull ? launch_compress_v<KP, HAS_E, true, 8, 8>(N, d, k, V, X, ids, E, U, Z, st)
                  : launch_compress_v<KP, HAS_E, false, 8, 8>(N, d, k, V, X, ids, E, U, Z, st);
@@ -439,21 +629,21 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
   return hipGetLastError();
 }
 
+// 8 token tiles (128 tokens) x 2 halves of d per block (16 waves)
 template <int KS2, bool HAS_E>
 static hipError_t launch_decompress_ks(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
                                        hipStream_t st) {
-  constexpr int TG = (KS2 > 2) ? 2 : 4;
-  const int64_t per_block = 16 * TG;
-  const int64_t blocks = (N + per_block - 1) / per_block;
+  constexpr int TW = 8, DS = 2;
+  const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
   if (k == 32 * KS2)
-    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, TG, HAS_E, true, true>), dim3((unsigned)blocks),
-                       dim3(256), 0, st, Zc, ids, (const uint16_t*)E, (const uint16_t*)U,
-                       (uint16_t*)Y, N, d, k, V);
+    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, true, kDecompressDC, 1, DS, TW>),
+                       dim3((unsigned)blocks), dim3(64 * TW * DS), 0, st, Zc, ids,
+                       (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
   else
-    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, TG, HAS_E, false, true>), dim3((unsigned)blocks),
-                       dim3(256), 0, st, Zc, ids, (const uint16_t*)E, (const uint16_t*)U,
-                       (uint16_t*)Y, N, d, k, V);
+    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, false, kDecompressDC, 1, DS, TW>),
+                       dim3((unsigned)blocks), dim3(64 * TW * DS), 0, st, Zc, ids,
+                       (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
   return hipGetLastError();
 }
 
