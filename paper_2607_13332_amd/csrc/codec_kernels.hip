@@ -30,6 +30,65 @@ namespace ssn {
 // accumulated by identical MFMA sequences into separate fp32 accumulators
 // and subtracted once at the end (compress(E[ids]) is exactly zero).
 // ===========================================================================
+// Stages one d chunk of U (KS K steps of 32 rows) into LDS in B-fragment
+// order for the "contract over d" kernels.  Fragment (K step s, column tile i)
+// for lane 16*g + n holds U[32s + 8g .. +7][n*KP + i] (column i of lane
+// position n's KP-column block).
+//   WIDE (k == 16*KP, KP in {2,4,8}): a task is an 8-row x 8-column block read
+//     with 16-byte row loads (one wave instruction covers whole 128-byte rows)
+//     that feeds 8/KP lane positions;
+//   otherwise a task is the 8-row x KP-column block of one lane position,
+//     with per-element bounds predicates when k < 16*KP.
+template <int KP, bool KFULL, int KS, int NTHREADS>
+struct UStage {
+  static constexpr bool WIDE = KFULL && (KP == 2 || KP == 4 || KP == 8);
+  static constexpr int NTASK = WIDE ? KS * 8 * KP : KS * kWave;
+  static constexpr int TPT = (NTASK + NTHREADS - 1) / NTHREADS;
+  static constexpr int UW = WIDE ? 4 : (KP + 1) / 2;
+  int srow[TPT], scol[TPT], sidx[TPT];
+  bool on[TPT];
+  uint32_t w[TPT][8][UW];
+
+  __device__ __forceinline__ void init(int tid) {
+#pragma unroll
+    for (int q = 0; q < TPT; ++q) {
+      const int t = tid + q * NTHREADS;
+      on[q] = t < NTASK;
+      if constexpr (WIDE) {
+        const int sk = t / (8 * KP), rem = t % (8 * KP);
+        srow[q] = 32 * sk + 8 * (rem / (2 * KP));
+        scol[q] = 8 * (rem % (2 * KP));
+        sidx[q] = sk * KP * kWave + 16 * (rem / (2 * KP)) + scol[q] / KP;
+      } else {
+        srow[q] = 32 * (t >> 6) + 8 * ((t >> 4) & 3);
+        scol[q] = (t & 15) * KP;
+        sidx[q] = (t >> 6) * KP * kWave + (t & 63);
+      }
+    }
+  }
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ U, int64_t row0, int k) {
+#pragma unroll
+    for (int q = 0; q < TPT; ++q)
+      if (on[q]) {
+        if constexpr (WIDE) load_block8<8, true>(U, row0 + srow[q], scol[q], k, k, w[q]);
+        else load_block8<KP, KFULL>(U, row0 + srow[q], scol[q], k, k, w[q]);
+      }
+  }
+  __device__ __forceinline__ void store(u32x4* lds) const {
+#pragma unroll
+    for (int q = 0; q < TPT; ++q)
+      if (on[q]) {
+        if constexpr (WIDE) {
+#pragma unroll
+          for (int c = 0; c < 8; ++c) lds[sidx[q] + (c % KP) * kWave + c / KP] = block8_column<8>(w[q], c);
+        } else {
+#pragma unroll
+          for (int i = 0; i < KP; ++i) lds[sidx[q] + i * kWave] = block8_column<KP>(w[q], i);
+        }
+      }
+  }
+};
+
 constexpr int kCompressKS = 4;                 // K steps (of 32) per d chunk
 constexpr int kCompressDC = 32 * kCompressKS;  // d chunk
 
@@ -40,10 +99,6 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     float* __restrict__ Z, int64_t N, int d, int k, int64_t V) {
   constexpr int DC = 32 * KS;
-  constexpr int KW = (KP + 1) / 2;
-  constexpr int TASKS = KS * kWave;            // staging tasks per chunk
-  static_assert(TASKS % (64 * WAVES) == 0 || (64 * WAVES) % TASKS == 0, "staging split");
-  constexpr int TPT = TASKS >= 64 * WAVES ? TASKS / (64 * WAVES) : 1;
   __shared__ u32x4 lds[2][KS * KP * kWave];
 
   const int tid = threadIdx.x;
@@ -55,17 +110,8 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
   const uint16_t* xrow = X + t * d + 8 * g;
   const uint16_t* erow = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * g : nullptr;
 
-  // staging tasks of this thread: task t = tid + q*64*WAVES covers K step
-  // t/64, K group (t/16)%4, column block t%16 of the chunk
-  const bool stager = tid < TASKS;
-  int srow[TPT], sidx[TPT];
-#pragma unroll
-  for (int q = 0; q < TPT; ++q) {
-    const int t = tid + q * 64 * WAVES;
-    srow[q] = 32 * (t >> 6) + 8 * ((t >> 4) & 3);
-    sidx[q] = (t >> 6) * KP * kWave + (t & 63);
-  }
-  const int scol = (tid & 15) * KP;
+  UStage<KP, KFULL, KS, 64 * WAVES> ust;
+  ust.init(tid);
   const int nch = d / DC;
   // Each block sweeps the d chunks starting at its own offset: if every wave
   // read the same column range of its rows at the same time, the requests
@@ -74,7 +120,6 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
   auto chunk = [&](int c) { const int x = c + rot; return x < nch ? x : x - nch; };
 
   u32x4 xf[NBUF][KS], ef[NBUF][KS];
-  uint32_t uw[TPT][8][KW];
 
   auto load_xe = [&](int c, u32x4(&xo)[KS], u32x4(&eo)[KS]) {
 #pragma unroll
@@ -83,21 +128,8 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
       if constexpr (HAS_E) eo[s] = ldg<NT>(erow + c * DC + 32 * s);
     }
   };
-  auto load_u = [&](int c) {
-    if (stager) {
-#pragma unroll
-      for (int q = 0; q < TPT; ++q)
-        load_block8<KP, KFULL>(U, (int64_t)c * DC + srow[q], scol, k, k, uw[q]);
-    }
-  };
-  auto store_u = [&](int buf) {
-    if (stager) {
-#pragma unroll
-      for (int q = 0; q < TPT; ++q)
-#pragma unroll
-        for (int i = 0; i < KP; ++i) lds[buf][sidx[q] + i * kWave] = block8_column<KP>(uw[q], i);
-    }
-  };
+  auto load_u = [&](int c) { ust.load(U, (int64_t)c * DC, k); };
+  auto store_u = [&](int buf) { ust.store(lds[buf]); };
 
   f32x4 accX[KP], accE[KP];
 #pragma unroll
@@ -182,8 +214,6 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     float* __restrict__ Z, int64_t N, int d, int k, int64_t V) {
   constexpr int KS = 4, DC = 128;
-  constexpr int KW = (KP + 1) / 2;
-  constexpr int TASKS = KS * kWave;              // U staging tasks per chunk (256)
   __shared__ u32x4 lds[2][KS * KP * kWave];      // U B fragments, double buffered
   __shared__ u32x4 tile[WAVES][HAS_E ? 2 : 1][16 * 16];   // [wave][X/E][row * 16 + cell ^ row]
 
@@ -223,20 +253,10 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     }
   };
 
-  const bool stager = tid < TASKS;
-  const int srow = 32 * (tid >> 6) + 8 * ((tid >> 4) & 3);
-  const int scol = (tid & 15) * KP;
-  const int sidx = (tid >> 6) * KP * kWave + (tid & 63);
-  uint32_t uw[8][KW];
-  auto load_u = [&](int c) {
-    if (stager) load_block8<KP, KFULL>(U, (int64_t)c * DC + srow, scol, k, k, uw);
-  };
-  auto store_u = [&](int buf) {
-    if (stager) {
-#pragma unroll
-      for (int i = 0; i < KP; ++i) lds[buf][sidx + i * kWave] = block8_column<KP>(uw, i);
-    }
-  };
+  UStage<KP, KFULL, KS, 64 * WAVES> ust;
+  ust.init(tid);
+  auto load_u = [&](int c) { ust.load(U, (int64_t)c * DC, k); };
+  auto store_u = [&](int buf) { ust.store(lds[buf]); };
 
   f32x4 accX[KP], accE[KP];
 #pragma unroll
@@ -316,7 +336,7 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
 constexpr int kDecompressDC = 64;
 
 template <int KS2, bool HAS_E, bool KFULL32, int DC = kDecompressDC, int PF = 1, int DSPLIT = 1,
-          int TW = 4>
+          int TW = 4, bool NTS = false>
 __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
@@ -461,8 +481,8 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
             }
           }
           if (ok[q])
-            *(u32x4*)(yrow[q] + c * DC) = u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
-                                                pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+            stg<NTS>(yrow[q] + c * DC, u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                             pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])});
         }
         store_u((i + 1) & 1);
       }
@@ -629,7 +649,9 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
   return hipGetLastError();
 }
 
-// 8 token tiles (128 tokens) x 2 halves of d per block (16 waves)
+// 8 token tiles (128 tokens) x 2 halves of d per block (16 waves); the
+// activation rows are written with non-temporal stores (streamed out instead
+// of parked dirty in the caches, where they slowed the next kernel's reads)
 template <int KS2, bool HAS_E>
 static hipError_t launch_decompress_ks(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
@@ -637,11 +659,11 @@ static hipError_t launch_decompress_ks(int64_t N, int d, int k, int64_t V, const
   constexpr int TW = 8, DS = 2;
   const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
   if (k == 32 * KS2)
-    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, true, kDecompressDC, 1, DS, TW>),
+    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, true, kDecompressDC, 1, DS, TW, true>),
                        dim3((unsigned)blocks), dim3(64 * TW * DS), 0, st, Zc, ids,
                        (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
   else
-    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, false, kDecompressDC, 1, DS, TW>),
+    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, false, kDecompressDC, 1, DS, TW, true>),
                        dim3((unsigned)blocks), dim3(64 * TW * DS), 0, st, Zc, ids,
                        (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
   return hipGetLastError();
