@@ -134,6 +134,19 @@ __device__ __forceinline__ void stg(uint16_t* p, u32x4 v) {
   else *(u32x4*)p = v;
 }
 
+// LDS transpose read of 4 bf16 per lane (ds_read_b64_tr_b16, gfx950).  Within
+// each group of 16 lanes, lane i receives element (i mod 4) of the 8-byte
+// words addressed by lanes 4j + i/4, j = 0..3.  So when lane L of a group
+// points at row r0 + L/4, columns c0 + 4 (L mod 4) .. +3 of a row-major bf16
+// tile in LDS, lane i receives rows r0 .. r0+3 of column c0 + i: the
+// row-contiguous tile yields column-contiguous MFMA fragments.
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x2 lds_read_tr16(const uint16_t* p) {
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
+}
+
 __device__ __forceinline__ int64_t clamp_id(int32_t id, int64_t V) {
   int64_t i = id;
   return i < 0 ? 0 : (i >= V ? V - 1 : i);

@@ -8,6 +8,8 @@
 #include "ssn_device.h"
 #include "ssn_launch.h"
 
+#include <type_traits>
+
 namespace ssn {
 
 struct PanelBatch {
@@ -195,6 +197,241 @@ __global__ __launch_bounds__(256) void project_weights_mfma_bf16(PanelBatch pb,
 }
 
 // ===========================================================================
+// Column-partitioned kernel, bf16 storage, MFMA, every n a multiple of 8.
+//
+// The columns of all matrices of a batch form one sequence of 16-column
+// tiles (a tile never spans two matrices).  Block b owns tiles
+// [b*tpb, (b+1)*tpb), where tpb is chosen so that the grid is one block per
+// compute unit: every block then streams the same number of bytes and the
+// launch has no partial last round.  The block has tpb/2 waves (at least 4);
+// wave w owns tiles w and w + waves for all k rows of T.
+//   pass 1  T = U^T W over chunks of 64 rows.  The block loads each chunk of
+//           W (a tile row is 32 contiguous bytes, the block's tiles of one
+//           matrix are contiguous) and of U with 16-byte loads into a
+//           row-major LDS tile; thread t moves piece t mod H of rows
+//           t/H + 16i, so one pointer per thread serves every chunk.  Two
+//           chunks are in flight in registers while one is computed.  The
+//           waves read d-contiguous MFMA fragments of both tiles with LDS
+//           transpose reads.
+//   pass 2  W = U T over the same chunks: T^T is taken straight from each
+//           wave's accumulators as bf16 hi + lo operand fragments, the U
+//           chunk comes from LDS, and each wave writes its output tiles into
+//           an LDS row tile that the whole block then stores with the same
+//           contiguous 16-byte pattern it loaded W with (non-temporal: W is
+//           not read again).
+// W is read once and written once; U comes from L2 once per pass per block.
+// ===========================================================================
+struct ColumnBatch {
+  uint16_t* W[kMaxBatch];
+  int32_t n[kMaxBatch];
+  int32_t first_tile[kMaxBatch + 1];   // prefix sums of ceil(n / 16)
+  int32_t count;
+  int32_t tiles;                       // total tiles of the batch
+  int32_t tpb;                         // tiles per block
+};
+
+constexpr int kColRows = 64;           // rows per chunk
+constexpr int kColMinWaves = 4;
+// Waves per block at most: 10 (tiles per block <= 20) while the wave's
+// registers allow three waves per SIMD, 8 for k > 64.
+constexpr int cols_max_waves(int kt) { return kt > 4 ? 8 : 10; }
+
+template <int KT, bool NTS, int DEPTH>
+__global__ __launch_bounds__(kWave * cols_max_waves(KT)) void project_weights_cols_bf16(
+    ColumnBatch cb, const uint16_t* __restrict__ U, int d, int k) {
+  static_assert(DEPTH == 1 || DEPTH == 2, "one or two chunks in flight");
+  constexpr int R = kColRows, CT = 2;
+  constexpr int RP = 16, NPW = R / RP;               // rows per pass, W pieces per thread per chunk
+  constexpr int KS2 = (KT + 1) / 2;
+  constexpr int KW = 32 * KS2;                       // U tile width (bf16), zero padded past k
+  constexpr int UPR = KW / 8;                        // U pieces (16 B) per row
+  constexpr int UP = UPR + 1;                        // U row pitch in pieces
+  constexpr int NUP = (R * UPR + kWave * kColMinWaves - 1) / (kWave * kColMinWaves);
+  constexpr int WPMAX = 4 * cols_max_waves(KT) + 1;
+  __shared__ u32x4 wt[2][R * WPMAX];                 // W (pass 1) / output (pass 2) row tiles
+  __shared__ u32x4 ut[2][R * UP];                    // U row tiles
+
+  const int tid = threadIdx.x, NT = blockDim.x, NW = NT / kWave;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int L = lane & 15, g = lane >> 4;
+  const int tpb = cb.tpb;
+  const int H = 2 * tpb, WP = H + 1;
+  const int t0 = blockIdx.x * tpb;
+  const int tcount = min(tpb, cb.tiles - t0);
+  const int nch = (d + R - 1) / R;
+
+  // W pieces of this thread: piece h of rows row0 + RP*i of every chunk
+  const bool wthr = tid < RP * H;
+  const int h = tid % H, row0 = tid / H;
+  int b = 0;
+  {
+    const int t = t0 + h / 2;
+    while (b + 1 < cb.count && t >= cb.first_tile[b + 1]) ++b;
+  }
+  const int ld = cb.n[b];
+  const int col = (t0 + h / 2 - cb.first_tile[b]) * 16 + 8 * (h & 1);
+  const bool wok = wthr && h < 2 * tcount && col < ld;
+  uint16_t* const wsrc = cb.W[b] + (int64_t)row0 * ld + col;
+  const int wofs = row0 * WP + h;
+
+  u32x4 wv[DEPTH][NPW], uv[DEPTH][NUP];
+  auto load_w = [&](int c, u32x4 (&v)[NPW]) {
+#pragma unroll
+    for (int i = 0; i < NPW; ++i) {
+      const int r = c * R + RP * i;
+      const bool ok = wok && r + row0 < d;
+      v[i] = ok ? *(const u32x4*)(wsrc + (int64_t)r * ld) : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto park_w = [&](int buf, const u32x4 (&v)[NPW]) {
+    if (wthr)
+#pragma unroll
+      for (int i = 0; i < NPW; ++i) wt[buf][wofs + RP * i * WP] = v[i];
+  };
+  auto load_u = [&](int c, u32x4 (&v)[NUP]) {
+#pragma unroll
+    for (int i = 0; i < NUP; ++i) {
+      const int q = tid + NT * i;
+      const int r = c * R + q / UPR, uc = 8 * (q % UPR);
+      const bool ok = q < R * UPR && uc < k && r < d;
+      v[i] = ok ? *(const u32x4*)(U + (int64_t)r * k + uc) : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto park_u = [&](int buf, const u32x4 (&v)[NUP]) {
+#pragma unroll
+    for (int i = 0; i < NUP; ++i) {
+      const int q = tid + NT * i;
+      if (q < R * UPR) ut[buf][(q / UPR) * UP + q % UPR] = v[i];
+    }
+  };
+
+  // ------------------------------ pass 1 ---------------------------------
+  f32x4 acc[KT][CT];
+#pragma unroll
+  for (int i = 0; i < KT; ++i)
+#pragma unroll
+    for (int c = 0; c < CT; ++c) acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute1 = [&](int c) {
+    const uint16_t* ub = (const uint16_t*)ut[c & 1];
+    const uint16_t* wb = (const uint16_t*)wt[c & 1];
+#pragma unroll
+    for (int ks = 0; ks < R / 32; ++ks) {
+      const int r = 32 * ks + 8 * g + (L >> 2);
+      u32x4 a[KT];
+#pragma unroll
+      for (int i = 0; i < KT; ++i) {
+        const uint16_t* p = ub + r * (8 * UP) + 16 * i + 4 * (L & 3);
+        const u32x2 x = lds_read_tr16(p), y = lds_read_tr16(p + 4 * 8 * UP);
+        a[i] = u32x4{x[0], x[1], y[0], y[1]};
+      }
+#pragma unroll
+      for (int cc = 0; cc < CT; ++cc) {
+        const int jl = wave + NW * cc;
+        if (jl < tcount) {
+          const uint16_t* p = wb + r * (8 * WP) + 16 * jl + 4 * (L & 3);
+          const u32x2 x = lds_read_tr16(p), y = lds_read_tr16(p + 4 * 8 * WP);
+          const u32x4 bfr = u32x4{x[0], x[1], y[0], y[1]};
+#pragma unroll
+          for (int i = 0; i < KT; ++i) acc[i][cc] = mfma16x16x32(a[i], bfr, acc[i][cc]);
+        }
+      }
+    }
+  };
+  // chunk 0 parked, chunks 1 .. DEPTH in flight; chunk j travels in set j % DEPTH
+  load_w(0, wv[0]);
+  load_u(0, uv[0]);
+  park_w(0, wv[0]);
+  park_u(0, uv[0]);
+#pragma unroll
+  for (int j = 1; j <= DEPTH; ++j)
+    if (j < nch) {
+      load_w(j, wv[j % DEPTH]);
+      load_u(j, uv[j % DEPTH]);
+    }
+  __syncthreads();
+  auto step1 = [&](int c, auto S) {
+    constexpr int s = decltype(S)::value;      // == (c + 1) % DEPTH
+    compute1(c);
+    if (c + 1 < nch) {
+      park_w((c + 1) & 1, wv[s]);
+      park_u((c + 1) & 1, uv[s]);
+    }
+    if (c + 1 + DEPTH < nch) {
+      load_w(c + 1 + DEPTH, wv[s]);
+      load_u(c + 1 + DEPTH, uv[s]);
+    }
+    __syncthreads();
+  };
+  for (int c = 0; c < nch; c += DEPTH) {
+    step1(c, std::integral_constant<int, 1 % DEPTH>{});
+    if constexpr (DEPTH == 2)
+      if (c + 1 < nch) step1(c + 1, std::integral_constant<int, 0>{});
+  }
+
+  // ------------------------------ pass 2 ---------------------------------
+  // A = T^T: row m <-> column 16*jl + m; K slot (g, r) <-> k index
+  // 32s + 4g + r (r < 4) or 32s + 16 + 4g + r - 4 (r >= 4), which is exactly
+  // what acc[2s][cc] and acc[2s+1][cc] of this lane hold.
+  u32x4 thi[CT][KS2], tlo[CT][KS2];
+#pragma unroll
+  for (int cc = 0; cc < CT; ++cc)
+#pragma unroll
+    for (int s = 0; s < KS2; ++s) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[e] = acc[2 * s][cc][e];
+        v[4 + e] = (2 * s + 1 < KT) ? acc[2 * s + 1][cc][e] : 0.f;
+      }
+      split_bf16x8(v, thi[cc][s], tlo[cc][s]);
+    }
+
+  load_u(0, uv[0]);
+  park_u(0, uv[0]);
+  if (nch > 1) load_u(1, uv[0]);
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    const uint16_t* ub = (const uint16_t*)ut[c & 1];
+    uint16_t* ob = (uint16_t*)wt[c & 1];
+#pragma unroll
+    for (int sub = 0; sub < R / 16; ++sub) {
+      const int r = 16 * sub + L;
+      u32x4 bfr[KS2];
+#pragma unroll
+      for (int s = 0; s < KS2; ++s) {
+        const uint16_t* p = ub + r * (8 * UP) + 32 * s + 4 * g;
+        const u32x2 x = *(const u32x2*)p, y = *(const u32x2*)(p + 16);
+        bfr[s] = u32x4{x[0], x[1], y[0], y[1]};
+      }
+#pragma unroll
+      for (int cc = 0; cc < CT; ++cc) {
+        const int jl = wave + NW * cc;
+        if (jl < tcount) {
+          f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < KS2; ++s) {
+            o = mfma16x16x32(thi[cc][s], bfr[s], o);
+            o = mfma16x16x32(tlo[cc][s], bfr[s], o);
+          }
+          // lane holds W[row r of the chunk][16*jl + 4g + 0..3]
+          *(u32x2*)(ob + r * (8 * WP) + 16 * jl + 4 * g) =
+              u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+        }
+      }
+    }
+    if (c + 1 < nch) park_u((c + 1) & 1, uv[0]);
+    if (c + 2 < nch) load_u(c + 2, uv[0]);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < NPW; ++i) {
+      const int r = c * R + RP * i;
+      if (wok && r + row0 < d) stg<NTS>(wsrc + (int64_t)r * ld, wt[c & 1][wofs + RP * i * WP]);
+    }
+  }
+}
+
+// ===========================================================================
 // Generic kernel: any dtype, d, k <= 1024.  One block per column (grid-
 // stride): t = U^T w by block reductions in fixed order, then w <- U t.
 // ===========================================================================
@@ -251,13 +488,64 @@ static hipError_t launch_weights_kt(const PanelBatch& pb, int blocks, const void
   return hipGetLastError();
 }
 
+static int device_cu_count() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int c = 0;
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0)
+      c = 256;
+    cus[dev] = c;
+  }
+  return cus[dev];
+}
+
+template <int KT>
+static hipError_t launch_cols(ColumnBatch cb, int cus, const void* U, int d, int k, hipStream_t st) {
+  constexpr int kMaxTpb = 2 * cols_max_waves(KT);
+  int tpb = (cb.tiles + cus - 1) / cus;
+  cb.tpb = tpb < 1 ? 1 : (tpb > kMaxTpb ? kMaxTpb : tpb);
+  int waves = (cb.tpb + 1) / 2;
+  waves = waves < kColMinWaves ? kColMinWaves : waves;
+  const unsigned grid = (unsigned)((cb.tiles + cb.tpb - 1) / cb.tpb);
+  hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, 2>), dim3(grid), dim3(kWave * waves), 0, st,
+                     cb, (const uint16_t*)U, d, k);
+  return hipGetLastError();
+}
+
 hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t* n, int64_t k,
                                   void* const* W, const void* U, hipStream_t st) {
   bool aligned = (((uintptr_t)U & 15u) == 0);
-  int64_t panels = 0;
+  bool cols8 = true;
+  int64_t panels = 0, tiles = 0;
   for (int b = 0; b < count; ++b) {
     aligned = aligned && (((uintptr_t)W[b] & 15u) == 0);
+    cols8 = cols8 && (n[b] % 8 == 0);
     panels += (n[b] + 63) / 64;
+    tiles += (n[b] + 15) / 16;
+  }
+  if (weights_use_mfma(dtype, d, k) && aligned && cols8 && tiles <= INT32_MAX / 2) {
+    ColumnBatch cb{};
+    int nb = 0;
+    int32_t acc = 0;
+    for (int b = 0; b < count; ++b) {
+      if (n[b] == 0) continue;
+      cb.W[nb] = (uint16_t*)W[b];
+      cb.n[nb] = (int32_t)n[b];
+      cb.first_tile[nb] = acc;
+      acc += (int32_t)((n[b] + 15) / 16);
+      ++nb;
+    }
+    if (nb == 0) return hipSuccess;
+    for (int b = nb; b <= kMaxBatch; ++b) cb.first_tile[b] = acc;
+    cb.count = nb;
+    cb.tiles = acc;
+    const int cus = device_cu_count();
+    const int kt = (int)((k + 15) / 16);
+    if (kt <= 2) return launch_cols<2>(cb, cus, U, (int)d, (int)k, st);
+    if (kt <= 4) return launch_cols<4>(cb, cus, U, (int)d, (int)k, st);
+    return launch_cols<8>(cb, cus, U, (int)d, (int)k, st);
   }
   if (weights_use_mfma(dtype, d, k) && aligned && panels <= INT32_MAX) {
     PanelBatch pb{};

@@ -169,6 +169,7 @@ def test_codec_shapes(N, d, k, dtype):
 WEIGHT_SHAPES = [  # (d, n, k)
     (256, 1, 64), (256, 100, 64), (512, 200, 40), (4096, 64, 128), (512, 197, 8), (96, 70, 32),
     (128, 300, 51), (64, 33, 16), (2048, 130, 96), (1024, 4096, 64),
+    (96, 72, 32), (4064, 200, 64), (160, 24, 120),
 ]
 
 
@@ -184,6 +185,37 @@ def test_weight_shapes(d, n, k, dtype):
     ssn.project_weights(W, dev(Uh, dtype))
     check("project_weights", host(W), O.project_weights(Wh, Uh), dtype,
           "bf16out" if dtype == "bf16" else "f32out")
+
+
+BATCHES = [  # (d, k, [n...]): several matrices per launch; 16-column tiles that
+    # straddle block boundaries, widths that are odd multiples of 8, every
+    # tiles-per-wave variant of the column-partitioned kernel
+    (256, 64, [40000, 8, 24, 1000]),
+    (128, 128, [36000, 16]),
+    (64, 32, [80000, 40, 8]),
+    (96, 16, [8, 8, 72, 4096]),
+]
+
+
+@pytest.mark.parametrize("d,k,ns", BATCHES, ids=lambda v: str(v) if not isinstance(v, list) else f"{len(v)}mats")
+def test_weight_batches(d, k, ns):
+    seed = d + 7 * k + sum(ns)
+    print(f"[case] weights batch d={d} k={k} n={ns}", flush=True)
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), "bf16")
+    U = dev(Uh, "bf16")
+    Whs = [I.weights_host(d, n, seed + b, "bf16") for b, n in enumerate(ns)]
+    Ws = [dev(Wh, "bf16") for Wh in Whs]
+    singles = [W.clone() for W in Ws]
+    ssn.project_weights_batched(Ws, U)
+    for W in singles:
+        ssn.project_weights(W, U)
+    torch.cuda.synchronize()
+    for b, (W, Wh) in enumerate(zip(Ws, Whs)):
+        cols = sample_rows(Wh.shape[1], 512, b)
+        got = host(W)[:, cols]
+        check(f"batched matrix {b} n={Wh.shape[1]}", got, O.project_weights(Wh[:, cols], Uh), "bf16", "bf16out")
+        # the column partition differs between the two launches; the bits do not
+        assert torch.equal(W, singles[b])
 
 
 # ---------------------------------------------------------------- exact cases
@@ -210,12 +242,13 @@ def test_exact_special_cases(d, k):
     Zs = host(ssn.compress(dev(Xh, "bf16"), ids, E, dev(Ush, "bf16")))
     ref = (O.f64(Xh) - O.f64(Eh)[ids_h])[:, cols].astype(np.float32)
     assert np.array_equal(Zs, ref)
-    Wh = I.weights_host(d, 70, 9, "bf16")
-    W = dev(Wh, "bf16")
-    ssn.project_weights(W, dev(Ush, "bf16"))
-    want = np.zeros_like(Wh)
-    want[cols] = Wh[cols]
-    assert np.array_equal(host(W), want)
+    for n in (70, 72):   # both MFMA families of the weight re-projection
+        Wh = I.weights_host(d, n, 9, "bf16")
+        W = dev(Wh, "bf16")
+        ssn.project_weights(W, dev(Ush, "bf16"))
+        want = np.zeros_like(Wh)
+        want[cols] = Wh[cols]
+        assert np.array_equal(host(W), want)
 
 
 def test_empty_batch_is_a_no_op():
