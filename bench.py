@@ -13,7 +13,10 @@ Two independent microbatch input sets alternate between steps so that
 consecutive steps gather different embedding rows.  Inputs are resident in
 HBM before the timed region starts.  The once-per-optimizer-step weight
 re-projection (4 layers x (4096x4096 + 4096x14336)) is timed separately and
-reported under "weights".
+reported under "weights".  The same step with compress against the projected
+embedding table (Z = X U - (E U)[ids], table formed once outside the timed
+region) is timed separately and reported under "variants"; the headline value
+is the step with compress as written in Eq. (2).
 
 Prints ONE JSON line (rank 0).  `--gpus` above 1 is refused: this build runs
 on one GPU.
@@ -72,6 +75,8 @@ def algorithmic_bytes(op: str, N: int, d: int, k: int, u: int, s: int = 2) -> in
         return N * k * 4 + u * d * s + N * d * s + U + 4 * N
     if op in ("project_grad", "expand_grad"):
         return N * d * s + N * k * 4 + U
+    if op == "compress_projected":
+        return N * d * s + u * k * 4 + N * k * 4 + U + 4 * N
     raise ValueError(op)
 
 
@@ -189,18 +194,25 @@ def main():
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
 
-    per_op_ms = {op: 0.0 for op in ops}
-    for i in range(args.steps):
-        for j, op in enumerate(ops):
-            per_op_ms[op] += events[i][j].elapsed_time(events[i][j + 1]) / args.steps
-    per_op = {}
-    for op in ops:
+    def op_stats(evs, names):
+        out = {}
+        for j, op in enumerate(names):
+            ts = np.array([e[j].elapsed_time(e[j + 1]) for e in evs])
+            out[op] = (float(ts.mean()), np.percentile(ts, [10, 50, 90]))
+        return out
+
+    def per_op_entry(op, mean_ms, pct):
         byts = np.mean([algorithmic_bytes(op, N, d, k, s["u"]) for s in sets])
-        per_op[op] = {"ms": round(per_op_ms[op], 5),
-                      "tokens_per_s": round(N / (per_op_ms[op] * 1e-3), 1),
-                      "algorithmic_GBps": round(byts / (per_op_ms[op] * 1e-3) / 1e9, 1),
-                      "frac_hbm_peak": round(byts / (per_op_ms[op] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                      "bytes_per_launch": int(byts)}
+        return {"ms": round(mean_ms, 5),
+                "ms_p10_p50_p90": [round(float(x), 5) for x in pct],
+                "tokens_per_s": round(N / (mean_ms * 1e-3), 1),
+                "algorithmic_GBps": round(byts / (mean_ms * 1e-3) / 1e9, 1),
+                "frac_hbm_peak": round(byts / (mean_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                "bytes_per_launch": int(byts)}
+
+    stats = op_stats(events, ops)
+    per_op = {op: per_op_entry(op, *stats[op]) for op in ops}
+    per_op_ms = {op: stats[op][0] for op in ops}
     dom = max(ops, key=lambda o: per_op_ms[o])
     achieved = per_op[dom]["algorithmic_GBps"]
     traffic = load_traffic(dom)
@@ -226,6 +238,48 @@ def main():
                      "traffic": traffic},
         "kernel_source_hash": kernel_source_hash(),
     }
+
+    # ---------------- variant: compress against the projected table ----------------
+    tev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    tev[0].record()
+    P = ssn.project_table(E, U)
+    tev[1].record()
+    torch.cuda.synchronize()
+    P = ssn.project_table(E, U)
+    ops2 = ["decompress", "project_grad", "compress_projected", "expand_grad"]
+
+    def step2(s, evs):
+        evs[0].record()
+        ssn.decompress(s["Zin"], s["ids"], E, U, out=s["Y"])
+        evs[1].record()
+        ssn.project_grad(s["G"], U, out=s["GZ"])
+        evs[2].record()
+        ssn.compress_projected(s["X"], s["ids"], P, U, out=s["Z"])
+        evs[3].record()
+        ssn.expand_grad(s["GZin"], U, out=s["GX"])
+        evs[4].record()
+
+    ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    for i in range(args.warmup):
+        step2(sets[i % 2], ev2[0])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step2(sets[i % 2], ev2[i])
+    torch.cuda.synchronize()
+    ms2 = (time.perf_counter() - t0) * 1e3 / args.steps
+    st2 = op_stats(ev2, ops2)
+    cp = per_op_entry("compress_projected", *st2["compress_projected"])
+    cp["traffic"] = load_traffic("compress_projected")
+    result["variants"] = {
+        "compress_projected": cp,
+        "table_build": {"what": f"P = E U over all V={V} rows ({V * k * 4 / 1e6:.1f} MB fp32), "
+                                "once per basis / embedding change",
+                        "ms": round(tev[0].elapsed_time(tev[1]), 5)},
+        "step_with_projected_compress": {"ms_per_step": round(ms2, 5),
+                                         "tokens_per_s": round(N / (ms2 * 1e-3), 1)},
+    }
+    del P
 
     # ---------------- weight re-projection (once per optimizer step) ----------------
     if not args.no_weights:

@@ -63,7 +63,8 @@ typedef enum {
   SSN_OP_COMPRESS = 0,
   SSN_OP_DECOMPRESS = 1,
   SSN_OP_PROJECT_GRAD = 2,
-  SSN_OP_PROJECT_WEIGHTS = 3
+  SSN_OP_PROJECT_WEIGHTS = 3,
+  SSN_OP_COMPRESS_PROJECTED = 4
 } ssn_op_t;
 
 /* Returns SSN_ABI_VERSION. */
@@ -76,10 +77,11 @@ const char *ssn_status_string(int status);
  * Name of the kernel family ("mfma" or "generic") that `op` uses for this
  * dtype and shape when every pointer is 16-byte aligned; "invalid" for an
  * unknown op.  Pure host function (no HIP call), for tests and reports.
- * The MFMA kernels cover bf16 with: compress / project_grad d % 32 == 0 and
- * k <= 128; decompress d % 64 == 0, k % 8 == 0, k <= 128; project_weights
- * d % 32 == 0, k % 8 == 0, k <= 128.  Everything else runs the generic
- * kernels (fp32 arithmetic, one wavefront per token / one block per column).
+ * The MFMA kernels cover bf16 with: compress / project_grad /
+ * compress_projected d % 128 == 0 and k <= 128; decompress d % 128 == 0,
+ * k % 8 == 0, 8 <= k <= 128; project_weights d % 32 == 0, k % 8 == 0,
+ * k <= 128.  Everything else runs the generic kernels (fp32 arithmetic, one
+ * wavefront per token / one block per column).
  */
 const char *ssn_kernel_family(ssn_op_t op, ssn_dtype_t dtype, int64_t d, int64_t k);
 
@@ -128,6 +130,37 @@ ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, 
  */
 ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k,
                               const void *G, const void *U, float *GZ, void *stream);
+
+/*
+ * ssn_project_table -- the fixed token embedding projected onto the basis,
+ * once:  P[v, :] = E[v, :] . U  for v in [0, V).
+ *   E [V, d] dtype, U [d, k] dtype, P [V, k] float32 output
+ * Section 4.1 subtracts the fixed token embedding, which both sides of the
+ * boundary hold, before projecting (Eq. (2)).  E and U stay fixed for the
+ * run, so by linearity (X - E[ids]) U = X U - (E U)[ids], and E U is a table
+ * of V x k floats that can be formed once.  The arithmetic is that of
+ * ssn_project_grad over the V rows of E (same kernel, same fp32 sequence).
+ * Same validation and error codes as ssn_project_grad with N = V.
+ */
+ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t k,
+                               const void *E, const void *U, float *P, void *stream);
+
+/*
+ * ssn_compress_projected -- Eq. (2) against the projected table:
+ *   Z[i, :] = X[i, :] . U - P[ids[i], :]          for i in [0, N)
+ *   X [N, d] dtype, ids [N] int32, P [V, k] float32 from ssn_project_table,
+ *   U [d, k] dtype, Z [N, k] float32 output
+ * Equal to ssn_compress(X, ids, E, U) up to fp32 rounding when P was made by
+ * ssn_project_table from (E, U) with the same dtype, d and k: X U is formed
+ * by the same fp32 sequence as P, so a row X[i] equal to E[ids[i]]
+ * compresses to exactly zero.  It reads X and k floats of P per token
+ * instead of X and d elements of E per token (about half the bytes of
+ * ssn_compress at d = 4096, k = 64, bf16).  Validation as ssn_compress, with
+ * P in place of E (P must be 4-byte aligned and must not overlap Z).
+ */
+ssn_status_t ssn_compress_projected(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
+                                    const void *X, const int32_t *ids, const float *P,
+                                    const void *U, float *Z, void *stream);
 
 /*
  * ssn_project_weights -- original-SSN re-projection after an optimizer step

@@ -7,6 +7,8 @@
 #include "ssn_device.h"
 #include "ssn_launch.h"
 
+#include <type_traits>
+
 namespace ssn {
 
 // ===========================================================================
@@ -92,12 +94,16 @@ struct UStage {
 constexpr int kCompressKS = 4;                 // K steps (of 32) per d chunk
 constexpr int kCompressDC = 32 * kCompressKS;  // d chunk
 
+// HAS_P (with HAS_E false): Z = X.U - P[ids], where P = E.U was produced by
+// this same kernel with HAS_P false, so that X.U of a row equal to E[id]
+// reproduces P[id] bit for bit.
 template <int KP, int NBUF, bool HAS_E, bool KFULL, bool ROT = false, bool NT = false,
-          int WAVES = 4, int KS = kCompressKS>
+          int WAVES = 4, int KS = kCompressKS, bool HAS_P = false>
 __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
-    float* __restrict__ Z, int64_t N, int d, int k, int64_t V) {
+    float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ P) {
+  static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
   constexpr int DC = 32 * KS;
   __shared__ u32x4 lds[2][KS * KP * kWave];
 
@@ -184,6 +190,20 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
       float v[KP];
 #pragma unroll
       for (int i = 0; i < KP; ++i) v[i] = HAS_E ? accX[i][j] - accE[i][j] : accX[i][j];
+      if constexpr (HAS_P) {
+        const float* pp = P + clamp_id(ids[tj], V) * k + col0;
+        if constexpr (KFULL && KP % 4 == 0) {
+#pragma unroll
+          for (int i = 0; i < KP; i += 4) {
+            const f32x4 q = *(const f32x4*)(pp + i);
+            v[i] -= q[0]; v[i + 1] -= q[1]; v[i + 2] -= q[2]; v[i + 3] -= q[3];
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < KP; ++i)
+            if (col0 + i < k) v[i] -= pp[i];
+        }
+      }
       float* zp = Z + tj * k + col0;
       if constexpr (KFULL && KP % 4 == 0) {
 #pragma unroll
@@ -208,11 +228,12 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
 // tile, and reads its A fragments from there.  The next chunk's rows are
 // loaded into registers while the current chunk computes.
 // ===========================================================================
-template <int KP, bool HAS_E, bool KFULL, int WAVES = 8>
+template <int KP, bool HAS_E, bool KFULL, int WAVES = 8, int DEPTH = 1>
 __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     float* __restrict__ Z, int64_t N, int d, int k, int64_t V) {
+  static_assert(DEPTH == 1 || DEPTH == 2, "one or two chunks of rows in flight");
   constexpr int KS = 4, DC = 128;
   __shared__ u32x4 lds[2][KS * KP * kWave];      // U B fragments, double buffered
   __shared__ u32x4 tile[WAVES][HAS_E ? 2 : 1][16 * 16];   // [wave][X/E][row * 16 + cell ^ row]
@@ -234,22 +255,23 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     xr[i] = X + t * d + 8 * lc;
     er[i] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * lc : nullptr;
   }
-  u32x4 xv[4], ev[4];
-  auto load_rows = [&](int c) {
+  // DEPTH register sets: chunk c travels in set c % DEPTH
+  u32x4 xv[DEPTH][4], ev[DEPTH][4];
+  auto load_rows = [&](int c, u32x4 (&xs)[4], u32x4 (&es)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      xv[i] = *(const u32x4*)(xr[i] + c * DC);
-      if constexpr (HAS_E) ev[i] = *(const u32x4*)(er[i] + c * DC);
+      xs[i] = *(const u32x4*)(xr[i] + c * DC);
+      if constexpr (HAS_E) es[i] = *(const u32x4*)(er[i] + c * DC);
     }
   };
   u32x4* tx = tile[wave][0];
   u32x4* te = tile[wave][HAS_E ? 1 : 0];
-  auto park_rows = [&]() {
+  auto park_rows = [&](const u32x4 (&xs)[4], const u32x4 (&es)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = 4 * i + (lane >> 4);
-      tx[r * 16 + (lc ^ r)] = xv[i];
-      if constexpr (HAS_E) te[r * 16 + (lc ^ r)] = ev[i];
+      tx[r * 16 + (lc ^ r)] = xs[i];
+      if constexpr (HAS_E) te[r * 16 + (lc ^ r)] = es[i];
     }
   };
 
@@ -266,14 +288,16 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
   }
 
   const int nch = d / DC;
-  load_rows(0);
+#pragma unroll
+  for (int j = 0; j < DEPTH; ++j)
+    if (j < nch) load_rows(j, xv[j], ev[j]);
   load_u(0);
   store_u(0);
-  for (int c = 0; c < nch; ++c) {
-    park_rows();
-    const int cn = c + 1 < nch ? c + 1 : c;
-    load_rows(cn);
-    load_u(cn);
+  auto step = [&](int c, auto S) {
+    constexpr int s0 = decltype(S)::value;       // == c % DEPTH
+    park_rows(xv[s0], ev[s0]);
+    if (c + DEPTH < nch) load_rows(c + DEPTH, xv[s0], ev[s0]);
+    load_u(c + 1 < nch ? c + 1 : c);
     __syncthreads();
     const u32x4* fr = lds[c & 1];
 #pragma unroll
@@ -292,6 +316,11 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
       }
     }
     store_u((c + 1) & 1);
+  };
+  for (int c = 0; c < nch; c += DEPTH) {
+    step(c, std::integral_constant<int, 0>{});
+    if constexpr (DEPTH == 2)
+      if (c + 1 < nch) step(c + 1, std::integral_constant<int, 1>{});
   }
 
   const int col0 = n16 * KP;
@@ -495,10 +524,11 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
 // fp32 arithmetic, wavefront reductions.  Used for fp32 storage and for shapes
 // the MFMA kernels do not tile.
 // ===========================================================================
-template <typename T, bool HAS_E>
+template <typename T, bool HAS_E, bool HAS_P = false>
 __global__ __launch_bounds__(256) void compress_generic(
     const T* __restrict__ X, const int32_t* __restrict__ ids, const T* __restrict__ E,
-    const T* __restrict__ U, float* __restrict__ Z, int64_t N, int64_t d, int64_t k, int64_t V) {
+    const T* __restrict__ U, float* __restrict__ Z, int64_t N, int64_t d, int64_t k, int64_t V,
+    const float* __restrict__ P) {
   const int lane = threadIdx.x & 63;
   const int64_t nw = (int64_t)gridDim.x * 4;
   for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < N; t += nw) {
@@ -521,7 +551,10 @@ __global__ __launch_bounds__(256) void compress_generic(
         const float s = wave_sum(acc[i]);
         if (lane == i) mine = s;
       }
-      if (lane < 16 && kc + lane < k) Z[t * k + kc + lane] = mine;
+      if (lane < 16 && kc + lane < k) {
+        if constexpr (HAS_P) mine -= P[clamp_id(ids[t], V) * k + kc + lane];
+        Z[t * k + kc + lane] = mine;
+      }
     }
   }
 }
@@ -557,14 +590,14 @@ bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) {
   return dtype == kBF16 && d % (2 * kDecompressDC) == 0 && d <= INT32_MAX && k % 8 == 0 && k >= 8 && k <= 128;
 }
 
-template <int KP, bool HAS_E, bool KFULL, int WAVES, int KS>
+template <int KP, bool HAS_E, bool KFULL, int WAVES, int KS, bool HAS_P>
 static hipError_t launch_compress_v(int64_t N, int d, int k, int64_t V, const void* X,
                                     const int32_t* ids, const void* E, const void* U, float* Z,
-                                    hipStream_t st) {
+                                    const float* P, hipStream_t st) {
   const int64_t blocks = (N + 16 * WAVES - 1) / (16 * WAVES);
-  hipLaunchKernelGGL((compress_mfma_bf16<KP, 1, HAS_E, KFULL, false, false, WAVES, KS>),
+  hipLaunchKernelGGL((compress_mfma_bf16<KP, 1, HAS_E, KFULL, false, false, WAVES, KS, HAS_P>),
                      dim3((unsigned)blocks), dim3(64 * WAVES), 0, st, (const uint16_t*)X, ids,
-                     (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V);
+                     (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P);
   return hipGetLastError();
 }
 
@@ -580,38 +613,40 @@ static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const
   return hipGetLastError();
 }
 
-// compress (with the embedding) uses the row-contiguous variant; the gradient
-// projection (one stream) the direct-fragment variant with 8 waves (128
-// tokens) per block sharing each staged slice of U, in 256-d chunks when d
-// allows, else 128.
-template <int KP, bool HAS_E>
+// compress (with the embedding rows) uses the row-contiguous variant; the
+// gradient projection and the projected-table compress (one activation
+// stream) the direct-fragment variant with 8 waves (128 tokens) per block
+// sharing each staged slice of U, in 256-d chunks when d allows, else 128.
+// The table build (P = E.U) is a gradient-projection launch, so both sides of
+// the projected-table compress take the same instantiation.
+template <int KP, bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_kp(int64_t N, int d, int k, int64_t V, const void* X,
                                      const int32_t* ids, const void* E, const void* U, float* Z,
-                                     hipStream_t st) {
+                                     const float* P, hipStream_t st) {
   const bool kfull = (k == 16 * KP);
   if constexpr (HAS_E)
     return kfull ? launch_compress_rows<KP, true>(N, d, k, V, X, ids, E, U, Z, st)
                  : launch_compress_rows<KP, false>(N, d, k, V, X, ids, E, U, Z, st);
   if (d % 256 == 0)
-    return kfull ? launch_compress_v<KP, HAS_E, true, 8, 8>(N, d, k, V, X, ids, E, U, Z, st)
-                 : launch_compress_v<KP, HAS_E, false, 8, 8>(N, d, k, V, X, ids, E, U, Z, st);
-  return kfull ? launch_compress_v<KP, HAS_E, true, 8, 4>(N, d, k, V, X, ids, E, U, Z, st)
-               : launch_compress_v<KP, HAS_E, false, 8, 4>(N, d, k, V, X, ids, E, U, Z, st);
+    return kfull ? launch_compress_v<KP, HAS_E, true, 8, 8, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st)
+                 : launch_compress_v<KP, HAS_E, false, 8, 8, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+  return kfull ? launch_compress_v<KP, HAS_E, true, 8, 4, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st)
+               : launch_compress_v<KP, HAS_E, false, 8, 4, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
 }
 
-template <bool HAS_E>
+template <bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_mfma(int64_t N, int d, int k, int64_t V, const void* X,
                                        const int32_t* ids, const void* E, const void* U, float* Z,
-                                       hipStream_t st) {
+                                       const float* P, hipStream_t st) {
   switch ((k + 15) / 16) {
-    case 1: return launch_compress_kp<1, HAS_E>(N, d, k, V, X, ids, E, U, Z, st);
-    case 2: return launch_compress_kp<2, HAS_E>(N, d, k, V, X, ids, E, U, Z, st);
-    case 3: return launch_compress_kp<3, HAS_E>(N, d, k, V, X, ids, E, U, Z, st);
-    case 4: return launch_compress_kp<4, HAS_E>(N, d, k, V, X, ids, E, U, Z, st);
-    case 5: return launch_compress_kp<5, HAS_E>(N, d, k, V, X, ids, E, U, Z, st);
-    case 6: return launch_compress_kp<6, HAS_E>(N, d, k, V, X, ids, E, U, Z, st);
-    case 7: return launch_compress_kp<7, HAS_E>(N, d, k, V, X, ids, E, U, Z, st);
-    default: return launch_compress_kp<8, HAS_E>(N, d, k, V, X, ids, E, U, Z, st);
+    case 1: return launch_compress_kp<1, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+    case 2: return launch_compress_kp<2, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+    case 3: return launch_compress_kp<3, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+    case 4: return launch_compress_kp<4, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+    case 5: return launch_compress_kp<5, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+    case 6: return launch_compress_kp<6, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+    case 7: return launch_compress_kp<7, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+    default: return launch_compress_kp<8, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
   }
 }
 
@@ -620,33 +655,34 @@ static unsigned generic_blocks(int64_t N) {
   return (unsigned)(want < 65536 ? want : 65536);
 }
 
+template <typename T, bool HAS_E, bool HAS_P>
+static hipError_t launch_compress_generic(int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
+                                          const int32_t* ids, const void* E, const void* U,
+                                          float* Z, const float* P, hipStream_t st) {
+  hipLaunchKernelGGL((compress_generic<T, HAS_E, HAS_P>), dim3(generic_blocks(N)), dim3(256), 0, st,
+                     (const T*)X, ids, (const T*)E, (const T*)U, Z, N, d, k, V, P);
+  return hipGetLastError();
+}
+
+// E non-NULL: Z = (X - E[ids]).U; P non-NULL: Z = X.U - P[ids]; neither: Z = X.U.
 hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                            const int32_t* ids, const void* E, const void* U, float* Z,
-                           hipStream_t st) {
-  const bool has_e = (E != nullptr);
-  if (compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(Z) && (!has_e || al16(E))) {
-    return has_e ? launch_compress_mfma<true>(N, (int)d, (int)k, V, X, ids, E, U, Z, st)
-                 : launch_compress_mfma<false>(N, (int)d, (int)k, V, X, ids, E, U, Z, st);
+                           const float* P, hipStream_t st) {
+  const bool has_e = (E != nullptr), has_p = (P != nullptr);
+  if (compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(Z) && (!has_e || al16(E)) &&
+      (!has_p || al16(P))) {
+    if (has_e) return launch_compress_mfma<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
+    if (has_p) return launch_compress_mfma<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
+    return launch_compress_mfma<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
   }
-  const unsigned nb = generic_blocks(N);
   if (dtype == kF32) {
-    if (has_e)
-      hipLaunchKernelGGL((compress_generic<float, true>), dim3(nb), dim3(256), 0, st,
-                         (const float*)X, ids, (const float*)E, (const float*)U, Z, N, d, k, V);
-    else
-      hipLaunchKernelGGL((compress_generic<float, false>), dim3(nb), dim3(256), 0, st,
-                         (const float*)X, ids, (const float*)E, (const float*)U, Z, N, d, k, V);
-  } else {
-    if (has_e)
-      hipLaunchKernelGGL((compress_generic<uint16_t, true>), dim3(nb), dim3(256), 0, st,
-                         (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d,
-                         k, V);
-    else
-      hipLaunchKernelGGL((compress_generic<uint16_t, false>), dim3(nb), dim3(256), 0, st,
-                         (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d,
-                         k, V);
+    if (has_e) return launch_compress_generic<float, true, false>(N, d, k, V, X, ids, E, U, Z, P, st);
+    if (has_p) return launch_compress_generic<float, false, true>(N, d, k, V, X, ids, E, U, Z, P, st);
+    return launch_compress_generic<float, false, false>(N, d, k, V, X, ids, E, U, Z, P, st);
   }
-  return hipGetLastError();
+  if (has_e) return launch_compress_generic<uint16_t, true, false>(N, d, k, V, X, ids, E, U, Z, P, st);
+  if (has_p) return launch_compress_generic<uint16_t, false, true>(N, d, k, V, X, ids, E, U, Z, P, st);
+  return launch_compress_generic<uint16_t, false, false>(N, d, k, V, X, ids, E, U, Z, P, st);
 }
 
 // 8 token tiles (128 tokens) x 2 halves of d per block (16 waves); the

@@ -56,7 +56,8 @@ const char* ssn_kernel_family(ssn_op_t op, ssn_dtype_t dtype, int64_t d, int64_t
   bool mfma = false;
   switch (op) {
     case SSN_OP_COMPRESS:
-    case SSN_OP_PROJECT_GRAD: mfma = ssn::compress_uses_mfma(dtype, d, k); break;
+    case SSN_OP_PROJECT_GRAD:
+    case SSN_OP_COMPRESS_PROJECTED: mfma = ssn::compress_uses_mfma(dtype, d, k); break;
     case SSN_OP_DECOMPRESS: mfma = ssn::decompress_uses_mfma(dtype, d, k); break;
     case SSN_OP_PROJECT_WEIGHTS: mfma = ssn::weights_use_mfma(dtype, d, k); break;
     default: return "invalid";
@@ -81,7 +82,27 @@ ssn_status_t ssn_compress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, in
       overlap(out, span(U, d * k * s)) || overlap(out, span(ids, N * 4)))
     return SSN_ERR_ALIAS;
   return launch_status(
-      ssn::launch_compress(dtype, N, d, k, V, X, ids, E, U, Z, (hipStream_t)stream));
+      ssn::launch_compress(dtype, N, d, k, V, X, ids, E, U, Z, nullptr, (hipStream_t)stream));
+}
+
+ssn_status_t ssn_compress_projected(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
+                                    const void* X, const int32_t* ids, const float* P,
+                                    const void* U, float* Z, void* stream) {
+  if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;
+  if (N < 0 || d < 1 || k < 1 || k > d || V < 1) return SSN_ERR_SHAPE;
+  if (!mul_ok(N, d) || !mul_ok(V, k) || !mul_ok(d, k) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
+  if (N == 0) return SSN_OK;
+  if (!X || !ids || !P || !U || !Z) return SSN_ERR_NULL;
+  const int64_t s = elem_size(dtype);
+  if (!aligned_to(X, s) || !aligned_to(P, 4) || !aligned_to(U, s) || !aligned_to(ids, 4) ||
+      !aligned_to(Z, 4))
+    return SSN_ERR_ALIGN;
+  const Span out = span(Z, N * k * 4);
+  if (overlap(out, span(X, N * d * s)) || overlap(out, span(P, V * k * 4)) ||
+      overlap(out, span(U, d * k * s)) || overlap(out, span(ids, N * 4)))
+    return SSN_ERR_ALIAS;
+  return launch_status(
+      ssn::launch_compress(dtype, N, d, k, V, X, ids, nullptr, U, Z, P, (hipStream_t)stream));
 }
 
 ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
@@ -119,7 +140,12 @@ ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k
   const Span out = span(GZ, N * k * 4);
   if (overlap(out, span(G, N * d * s)) || overlap(out, span(U, d * k * s))) return SSN_ERR_ALIAS;
   return launch_status(ssn::launch_compress(dtype, N, d, k, 1, G, nullptr, nullptr, U, GZ,
-                                            (hipStream_t)stream));
+                                            nullptr, (hipStream_t)stream));
+}
+
+ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t k, const void* E,
+                               const void* U, float* P, void* stream) {
+  return ssn_project_grad(dtype, V, d, k, E, U, P, stream);
 }
 
 ssn_status_t ssn_project_weights_batched(ssn_dtype_t dtype, int64_t count, int64_t d,

@@ -15,9 +15,10 @@ bool compress_uses_mfma(int dtype, int64_t d, int64_t k);
 bool decompress_uses_mfma(int dtype, int64_t d, int64_t k);
 bool weights_use_mfma(int dtype, int64_t d, int64_t k);
 
+// E non-NULL: Z = (X - E[ids]).U; P non-NULL: Z = X.U - P[ids]; neither: Z = X.U.
 hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                            const int32_t* ids, const void* E, const void* U, float* Z,
-                           hipStream_t st);
+                           const float* P, hipStream_t st);
 hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const float* Z,
                              const int32_t* ids, const void* E, const void* U, void* Y,
                              hipStream_t st);

@@ -17,7 +17,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libssn.so")
 
 SSN_F32, SSN_BF16 = 0, 1
-OPS = {"compress": 0, "decompress": 1, "project_grad": 2, "project_weights": 3}
+OPS = {"compress": 0, "decompress": 1, "project_grad": 2, "project_weights": 3,
+       "compress_projected": 4}
 MAX_BATCH = 16
 
 _c_i64 = ctypes.c_int64
@@ -45,6 +46,11 @@ def _declare(lib):
                                    _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_project_grad.restype = ctypes.c_int
     lib.ssn_project_grad.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_project_table.restype = ctypes.c_int
+    lib.ssn_project_table.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_compress_projected.restype = ctypes.c_int
+    lib.ssn_compress_projected.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
+                                           _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_project_weights.restype = ctypes.c_int
     lib.ssn_project_weights.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]
     lib.ssn_project_weights_batched.restype = ctypes.c_int
@@ -178,6 +184,42 @@ def project_grad(G: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] =
     _check("ssn_project_grad", lib().ssn_project_grad(
         _dt_code(t), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2),
         _dev(out, "out", torch.float32, 2), _stream(stream)))
+    return out
+
+
+def project_table(E: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] = None,
+                  stream=None) -> torch.Tensor:
+    """P = E U (float32 [V, k]): the fixed embedding table, projected once."""
+    V, d = E.shape
+    k = U.shape[1]
+    if U.shape[0] != d:
+        raise ValueError(f"shape mismatch E{tuple(E.shape)} U{tuple(U.shape)}")
+    if out is None:
+        out = torch.empty((V, k), dtype=torch.float32, device=E.device)
+    _same_device(E, U, out)
+    t = E.dtype
+    _check("ssn_project_table", lib().ssn_project_table(
+        _dt_code(t), V, d, k, _dev(E, "E", t, 2), _dev(U, "U", t, 2),
+        _dev(out, "out", torch.float32, 2), _stream(stream)))
+    return out
+
+
+def compress_projected(X: torch.Tensor, ids: torch.Tensor, P: torch.Tensor, U: torch.Tensor,
+                       out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Z = X U - P[ids] (float32 [N, k]), with P from project_table(E, U)."""
+    N, d = X.shape
+    V, k = P.shape
+    if U.shape != (d, k) or ids.shape != (N,):
+        raise ValueError(f"shape mismatch X{tuple(X.shape)} ids{tuple(ids.shape)} "
+                         f"P{tuple(P.shape)} U{tuple(U.shape)}")
+    if out is None:
+        out = torch.empty((N, k), dtype=torch.float32, device=X.device)
+    _same_device(X, ids, P, U, out)
+    t = X.dtype
+    _check("ssn_compress_projected", lib().ssn_compress_projected(
+        _dt_code(t), N, d, k, V, _dev(X, "X", t, 2), _dev(ids, "ids", torch.int32, 1),
+        _dev(P, "P", torch.float32, 2), _dev(U, "U", t, 2), _dev(out, "out", torch.float32, 2),
+        _stream(stream)))
     return out
 
 

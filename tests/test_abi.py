@@ -67,6 +67,9 @@ def test_kernel_family_rules(ssn):
     assert kf("decompress", "bf16", 4064, 64) == "generic"
     assert kf("project_weights", "bf16", 4096, 64) == "mfma"
     assert kf("project_weights", "f32", 4096, 64) == "generic"
+    assert kf("compress_projected", "bf16", 4096, 64) == "mfma"
+    assert kf("compress_projected", "bf16", 5120, 51) == "mfma"
+    assert kf("compress_projected", "f32", 4096, 64) == "generic"
     assert ssn.lib().ssn_kernel_family(9, 1, 4096, 64) == b"invalid"
 
 
@@ -117,6 +120,24 @@ def test_project_grad_validation(ssn):
     assert f(1, 10, 64, 8, None, D, F, None) == ERR_NULL
     assert f(1, 10, 64, 100, A, D, F, None) == ERR_SHAPE
     assert f(1, 10, 64, 8, A, D, A + 8, None) == ERR_ALIAS
+
+
+def test_projected_table_validation(ssn):
+    L = ssn.lib()
+    t = L.ssn_project_table
+    assert t(1, 0, 64, 8, None, None, None, None) == OK                # V == 0 no-op
+    assert t(1, 100, 64, 8, None, D, F, None) == ERR_NULL
+    assert t(1, 100, 64, 65, C, D, F, None) == ERR_SHAPE
+    assert t(1, 100, 64, 8, C, D, C + 64, None) == ERR_ALIAS            # P overlaps E
+    f = L.ssn_compress_projected
+    assert f(1, 0, 64, 8, 100, None, None, None, None, None, None) == OK
+    assert f(7, 10, 64, 8, 100, A, B, C, D, F, None) == ERR_DTYPE
+    assert f(1, 10, 64, 8, 0, A, B, C, D, F, None) == ERR_SHAPE          # V < 1
+    assert f(1, 10, 64, 8, 100, A, B, None, D, F, None) == ERR_NULL      # no table
+    assert f(1, 10, 64, 8, 100, A, None, C, D, F, None) == ERR_NULL      # no ids
+    assert f(1, 10, 64, 8, 100, A, B, C + 2, D, F, None) == ERR_ALIGN    # P is float32
+    assert f(1, 10, 64, 8, 100, A, B, C, D, C + 100 * 8 * 4 - 4, None) == ERR_ALIAS  # Z on P
+    assert f(1, 10, 64, 8, 100, A, B, C, D, A + 64, None) == ERR_ALIAS   # Z on X
 
 
 def test_project_weights_validation(ssn):

@@ -64,6 +64,49 @@ def test_structured_config_all_ops(cfg):
     torch.cuda.synchronize()
 
 
+# ---------------------------------------------------------------- projected-table compress
+@pytest.mark.parametrize("cfg", [I.TINY, I.MID], ids=lambda c: c.name)
+def test_compress_projected_structured(cfg):
+    t = cfg.dtype
+    h = structured_inputs(cfg)
+    X, ids, E, U = dev(h["X"], t), dev(h["ids"], t), dev(h["E"], t), dev(h["U"], t)
+    P = ssn.project_table(E, U)
+    check(f"{cfg.name} project_table", host(P), O.project_grad(h["E"], h["U"]), t, "f32out")
+    # the table is the gradient projection of the rows of E, bit for bit
+    assert torch.equal(P, ssn.project_grad(E, U))
+    Z = ssn.compress_projected(X, ids, P, U)
+    check(f"{cfg.name} compress_projected", host(Z), O.compress(h["X"], h["ids"], h["E"], h["U"]),
+          t, "f32out")
+    # rows equal to their own embedding compress to exactly zero
+    Xe = E[ids.long()].contiguous()
+    assert torch.count_nonzero(ssn.compress_projected(Xe, ids, P, U)).item() == 0
+    torch.cuda.synchronize()
+
+
+def test_compress_projected_stage8b_sampled():
+    cfg = I.STAGE8B
+    print(f"[case] {cfg.name} projected table V={cfg.V}", flush=True)
+    inp = I.codec_inputs_device(cfg, DEV, need=("U", "E", "ids", "X"))
+    X, ids, E, U = inp["X"], inp["ids"], inp["E"], inp["U"]
+    P = ssn.project_table(E, U)
+    Z = ssn.compress_projected(X, ids, P, U)
+    Zref = ssn.compress(X, ids, E, U)
+    torch.cuda.synchronize()
+    rows = sample_rows(cfg.N, 384, cfg.seed + 5)
+    r = torch.from_numpy(rows).to(DEV)
+    Es = host(E.index_select(0, ids[r].long()))
+    loc = np.arange(len(rows), dtype=np.int32)
+    check(f"{cfg.name} compress_projected", host(Z[r]), O.compress(host(X[r]), loc, Es, host(U)),
+          "bf16", "f32out")
+    vs = sample_rows(cfg.V, 256, cfg.seed + 6)
+    check(f"{cfg.name} project_table", host(P[torch.from_numpy(vs).to(DEV)]),
+          O.project_grad(host(E[torch.from_numpy(vs).to(DEV)]), host(U)), "bf16", "f32out")
+    # the two compress forms agree to fp32 rounding over every row
+    assert rel(host(Z), O.f64(host(Zref))) < 2e-6
+    del inp, X, E, P, Z, Zref
+    torch.cuda.empty_cache()
+
+
 # ---------------------------------------------------------------- full-size codec
 def _sampled_codec_check(cfg, nsample=384):
     t = cfg.dtype
@@ -160,6 +203,10 @@ def test_codec_shapes(N, d, k, dtype):
     X, E, U, ids = dev(Xh, dtype), dev(Eh, dtype), dev(Uh, dtype), dev(ids_h, dtype)
     outkind = "bf16out" if dtype == "bf16" else "f32out_dec"
     check("compress", host(ssn.compress(X, ids, E, U)), O.compress(Xh, ids_h, Eh, Uh), dtype, "f32out")
+    P = ssn.project_table(E, U)
+    check("compress_projected", host(ssn.compress_projected(X, ids, P, U)),
+          O.compress(Xh, ids_h, Eh, Uh), dtype, "f32out")
+    assert torch.count_nonzero(ssn.compress_projected(E[ids.long()].contiguous(), ids, P, U)).item() == 0
     check("project_grad", host(ssn.project_grad(X, U)), O.project_grad(Xh, Uh), dtype, "f32out")
     check("decompress", host(ssn.decompress(dev(Zin, "f32"), ids, E, U)),
           O.decompress(Zin, ids_h, Eh, Uh), dtype, outkind)
