@@ -16,7 +16,10 @@ re-projection (4 layers x (4096x4096 + 4096x14336)) is timed separately and
 reported under "weights".  The same step with compress against the projected
 embedding table (Z = X U - (E U)[ids], table formed once outside the timed
 region) is timed separately and reported under "variants"; the headline value
-is the step with compress as written in Eq. (2).
+is the step with compress as written in Eq. (2).  The same step at the
+paper's own stage shapes (Pluralis-8B d=5120, k=51, V=128,256, S=4096; the 1B
+ablation model d=2048, k=40, S=2048; b = 1 and 3 coalesced sequences) and the
+weight re-projection at those shapes are reported under "paper_shapes".
 
 Prints ONE JSON line (rank 0).  `--gpus` above 1 is refused: this build runs
 on one GPU.
@@ -56,6 +59,8 @@ def parse_args():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-weights", action="store_true")
+    p.add_argument("--no-paper-shapes", action="store_true",
+                   help="skip the timings at the paper's own stage shapes (d=5120 k=51, d=2048 k=40)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle baseline sample")
     p.add_argument("--tokens", type=int, default=0, help="override N (testing only)")
@@ -116,6 +121,106 @@ def cpu_baseline(sample, cfg, seconds: float):
     return {"value": done / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{n} of the {cfg.N} tokens of one microbatch (d={cfg.d}, k={cfg.k}), "
                       f"all four codec ops in float64, repeated {done // n}x over {el:.1f} s"}
+
+
+def time_weights(wc, steps: int, dev):
+    """W <- U (U^T W) over one stage's output projections, one batched launch."""
+    import torch
+    from paper_2607_13332_amd import inputs as I
+    from paper_2607_13332_amd import ssn
+    Ws = []
+    for layer in range(wc.layers):
+        for j, (dd, n) in enumerate(wc.shapes):
+            Ws.append(I.weights_device(dd, n, wc.seed * 100 + 10 * layer + j, dev))
+    Uw = I.to_device(I.store(I.gaussian_orthonormal_basis(wc.d, wc.k, wc.seed), "bf16"), "bf16", dev)
+    for _ in range(2):
+        ssn.project_weights_batched(Ws, Uw)
+    torch.cuda.synchronize()
+    reps = max(3, steps // 5)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record()
+    for r in range(reps):
+        ssn.project_weights_batched(Ws, Uw)
+        ev[r + 1].record()
+    torch.cuda.synchronize()
+    wms = sum(ev[r].elapsed_time(ev[r + 1]) for r in range(reps)) / reps
+    wbytes = sum(2 * W.numel() * 2 for W in Ws) + wc.d * wc.k * 2
+    wflops = sum(4.0 * wc.d * wc.k * W.shape[1] for W in Ws)
+    shapes = " + ".join(f"{a}x{b}" for a, b in wc.shapes)
+    out = {
+        "workload": f"W <- U(U^T W) for {wc.layers} layers x ({shapes}) bf16, k={wc.k}, one launch",
+        "ms": round(wms, 5),
+        "algorithmic_GBps": round(wbytes / (wms * 1e-3) / 1e9, 1),
+        "frac_hbm_peak": round(wbytes / (wms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "mfma_TFLOPs": round(wflops / (wms * 1e-3) / 1e12, 2),
+        "frac_mfma_peak": round(wflops / (wms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+    }
+    if wc.name == I.WEIGHTS.name:
+        out["traffic"] = load_traffic("project_weights")
+    del Ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def time_codec_config(cfg, steps: int, warmup: int, dev):
+    """The four codec ops of one microbatch on a workload other than the
+    headline one (two alternating input sets, HIP events per op)."""
+    import numpy as np
+    import torch
+    from paper_2607_13332_amd import inputs as I
+    from paper_2607_13332_amd import ssn
+    N, d, k = cfg.N, cfg.d, cfg.k
+    base = I.codec_inputs_device(cfg, dev, need=("U", "E"))
+    U, E = base["U"], base["E"]
+    sets = []
+    for j in range(2):
+        c = I.with_tokens(cfg, N, seed=cfg.seed + 17 * j)
+        inp = I.codec_inputs_device(c, dev, need=("ids", "X", "G"))
+        inp["Zin"] = I.coords_device(N, k, c.seed + 1, dev)
+        inp["GZin"] = I.coords_device(N, k, c.seed + 2, dev)
+        inp["Z"] = torch.empty((N, k), dtype=torch.float32, device=dev)
+        inp["GZ"] = torch.empty((N, k), dtype=torch.float32, device=dev)
+        inp["Y"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        inp["GX"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        inp["u"] = int(torch.unique(inp["ids"]).numel())
+        sets.append(inp)
+    ops = ["decompress", "project_grad", "compress", "expand_grad"]
+
+    def step(s, evs):
+        evs[0].record()
+        ssn.decompress(s["Zin"], s["ids"], E, U, out=s["Y"])
+        evs[1].record()
+        ssn.project_grad(s["G"], U, out=s["GZ"])
+        evs[2].record()
+        ssn.compress(s["X"], s["ids"], E, U, out=s["Z"])
+        evs[3].record()
+        ssn.expand_grad(s["GZin"], U, out=s["GX"])
+        evs[4].record()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    for i in range(warmup):
+        step(sets[i % 2], evs[0])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(sets[i % 2], evs[i])
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    per_op = {}
+    step_bytes = 0
+    for j, op in enumerate(ops):
+        t = float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs]))
+        byts = float(np.mean([algorithmic_bytes(op, N, d, k, s["u"]) for s in sets]))
+        step_bytes += byts
+        per_op[op] = {"ms": round(t, 5), "algorithmic_GBps": round(byts / (t * 1e-3) / 1e9, 1),
+                      "frac_hbm_peak": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    out = {"workload": f"N={N} (B={cfg.B} x S={cfg.S}), d={d}, k={k}, V={cfg.V}, bf16",
+           "ms_per_step": round(ms, 5), "tokens_per_s": round(N / (ms * 1e-3), 1),
+           "step_frac_hbm_peak": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "per_op": per_op}
+    del sets, base, U, E
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -283,35 +388,17 @@ def main():
 
     # ---------------- weight re-projection (once per optimizer step) ----------------
     if not args.no_weights:
-        wc = I.WEIGHTS
-        Ws = []
-        for layer in range(wc.layers):
-            for j, (dd, n) in enumerate(wc.shapes):
-                Ws.append(I.weights_device(dd, n, wc.seed * 100 + 10 * layer + j, dev))
-        Uw = I.to_device(I.store(I.gaussian_orthonormal_basis(wc.d, wc.k, wc.seed), "bf16"), "bf16", dev)
-        for _ in range(2):
-            ssn.project_weights_batched(Ws, Uw)
-        torch.cuda.synchronize()
-        reps = max(3, args.steps // 5)
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
-        ev[0].record()
-        for r in range(reps):
-            ssn.project_weights_batched(Ws, Uw)
-            ev[r + 1].record()
-        torch.cuda.synchronize()
-        wms = sum(ev[r].elapsed_time(ev[r + 1]) for r in range(reps)) / reps
-        wbytes = sum(2 * W.numel() * 2 for W in Ws) + wc.d * wc.k * 2
-        wflops = sum(4.0 * wc.d * wc.k * W.shape[1] for W in Ws)
-        result["weights"] = {
-            "workload": "W <- U(U^T W) for 4 layers x (W_o 4096x4096, W_down 4096x14336) bf16, k=64, one launch",
-            "ms": round(wms, 5),
-            "algorithmic_GBps": round(wbytes / (wms * 1e-3) / 1e9, 1),
-            "frac_hbm_peak": round(wbytes / (wms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-            "mfma_TFLOPs": round(wflops / (wms * 1e-3) / 1e12, 2),
-            "frac_mfma_peak": round(wflops / (wms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": load_traffic("project_weights"),
-        }
-        del Ws
+        result["weights"] = time_weights(I.WEIGHTS, args.steps, dev)
+
+    # ---------------- the paper's own shapes ----------------
+    if not args.no_paper_shapes:
+        shapes = {}
+        for cfg in I.paper_configs():
+            if cfg.B in (1, 3):
+                shapes[cfg.name] = time_codec_config(cfg, max(10, args.steps // 2), args.warmup, dev)
+        for wc in (I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B):
+            shapes[wc.name] = time_weights(wc, args.steps, dev)
+        result["paper_shapes"] = shapes
 
     # ---------------- CPU baseline: the oracle on a bounded sample ----------------
     if not args.no_cpu_baseline:

@@ -77,11 +77,11 @@ const char *ssn_status_string(int status);
  * Name of the kernel family ("mfma" or "generic") that `op` uses for this
  * dtype and shape when every pointer is 16-byte aligned; "invalid" for an
  * unknown op.  Pure host function (no HIP call), for tests and reports.
- * The MFMA kernels cover bf16 with: compress / project_grad /
- * compress_projected d % 128 == 0 and k <= 128; decompress d % 128 == 0,
- * k % 8 == 0, 8 <= k <= 128; project_weights d % 32 == 0, k % 8 == 0,
- * k <= 128.  Everything else runs the generic kernels (fp32 arithmetic, one
- * wavefront per token / one block per column).
+ * The MFMA kernels cover bf16 with k <= 128 and: compress / project_grad /
+ * compress_projected / decompress d % 128 == 0; project_weights d % 32 == 0
+ * (and, when k % 8 != 0, every n % 8 == 0).  Everything else runs the
+ * generic kernels (fp32 arithmetic, one wavefront per token / one block per
+ * column).
  */
 const char *ssn_kernel_family(ssn_op_t op, ssn_dtype_t dtype, int64_t d, int64_t k);
 
@@ -151,9 +151,10 @@ ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t 
  *   X [N, d] dtype, ids [N] int32, P [V, k] float32 from ssn_project_table,
  *   U [d, k] dtype, Z [N, k] float32 output
  * Equal to ssn_compress(X, ids, E, U) up to fp32 rounding when P was made by
- * ssn_project_table from (E, U) with the same dtype, d and k: X U is formed
- * by the same fp32 sequence as P, so a row X[i] equal to E[ids[i]]
- * compresses to exactly zero.  It reads X and k floats of P per token
+ * ssn_project_table from (E, U) with the same dtype, d and k.  A row X[i]
+ * equal to E[ids[i]] compresses to zero up to that rounding, and exactly to
+ * zero when N and V select the same kernel (both 32768 or more, or both
+ * fewer, on 16-byte aligned buffers).  It reads X and k floats of P per token
  * instead of X and d elements of E per token (about half the bytes of
  * ssn_compress at d = 4096, k = 64, bf16).  Validation as ssn_compress, with
  * P in place of E (P must be 4-byte aligned and must not overlap Z).

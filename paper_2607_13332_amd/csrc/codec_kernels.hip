@@ -345,6 +345,198 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
 }
 
 // ===========================================================================
+// compress / project_grad / projected-table compress for few tokens.
+//
+// With N/128 token tiles below the compute-unit count the kernels above leave
+// most of the chip idle.  Here a block is 16*TTW tokens x P waves and wave w
+// owns the w-th of P equal ranges of d, walked in chunks of 64 (each U
+// fragment feeds TTW token tiles).  Everything a wave
+// stages is wave-private (no block barrier until the end): its 16 X rows (and
+// 16 E[ids] rows) arrive as 8 rows x 128 contiguous bytes per load
+// instruction into an XOR-swizzled row tile, and its U rows arrive as
+// 16-byte row pieces (k % 8 == 0) or as 16-byte pieces of the chunk's
+// contiguous span scattered element-wise (any k) into a zero-padded
+// row-major tile.  A fragments are plain 16-byte LDS reads, U fragments come
+// from LDS transpose reads.  Two chunks are in flight in registers.  At the
+// end the P partial (X - E[ids]).U results meet in LDS and are summed in wave
+// order (deterministic); HAS_P subtracts the projected table rows instead of
+// accumulating E[ids].U.
+// ===========================================================================
+template <int KP, bool HAS_E, bool HAS_P, bool KV, int P, int TTW>
+__global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) void compress_split_bf16(
+    const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
+    const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
+    float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ Pt) {
+  static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
+  constexpr int DC = 64;                       // d per chunk (two K steps)
+  constexpr int KW = 16 * KP;                  // U tile width
+  constexpr int UP = KW + 8;                   // U tile pitch (bf16), rows 16-byte aligned
+  constexpr int NUL = (DC * KW / 8 + 63) / 64;  // U pieces per lane (the span of DC*k fits too)
+  constexpr int NXE = HAS_E ? 2 : 1;
+  constexpr int R = 16 * TTW;                  // token rows of a wave
+  constexpr int NXL = 2 * TTW;                 // X (and E) pieces per lane
+  // per wave: X / E row tiles [R rows x 8 cells] and the U row tile; after
+  // the main loop the same memory holds the partial results
+  constexpr int XT_BYTES = NXE * R * 8 * 16;
+  constexpr int UT_BYTES = DC * UP * 2;
+  constexpr int WAVE_BYTES = XT_BYTES + UT_BYTES;
+  constexpr int RED_BYTES = TTW * KP * 64 * 16;
+  constexpr int SMEM = (P * WAVE_BYTES > P * RED_BYTES) ? P * WAVE_BYTES : P * RED_BYTES;
+  __shared__ __align__(16) unsigned char smem[SMEM];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n16 = lane & 15, g = lane >> 4;
+  const int64_t tok0 = (int64_t)blockIdx.x * R;
+  const int nchp = d / (DC * P);               // chunks of this wave
+  const int c0 = wave * nchp;
+  u32x4* const xtw = (u32x4*)(smem + wave * WAVE_BYTES);           // [X/E][row * 8 + cell']
+  uint16_t* const utw = (uint16_t*)(smem + wave * WAVE_BYTES + XT_BYTES);
+
+  // X / E row pieces: piece q = lane + 64 j is row q/8, 16-byte cell q%8
+  const uint16_t* xr[NXL];
+  const uint16_t* er[NXL];
+#pragma unroll
+  for (int j = 0; j < NXL; ++j) {
+    const int q = lane + 64 * j;
+    int64_t t = tok0 + q / 8;
+    t = t < N ? t : N - 1;
+    xr[j] = X + t * d + 8 * (q % 8);
+    er[j] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * (q % 8) : nullptr;
+  }
+  if constexpr (!KV) {
+    // the scatter below never writes columns k .. KW
+    for (int i = lane; i < UT_BYTES / 16; i += 64) ((u32x4*)utw)[i] = u32x4{0u, 0u, 0u, 0u};
+  }
+
+  // two register sets: chunk i of this wave travels in set i % 2
+  u32x4 xs[2][NXL], es[2][NXL], us[2][NUL];
+  auto load = [&](int c, u32x4 (&x)[NXL], u32x4 (&e)[NXL], u32x4 (&u)[NUL]) __attribute__((always_inline)) {
+    const int dcol = c * DC;
+#pragma unroll
+    for (int j = 0; j < NXL; ++j) {
+      x[j] = *(const u32x4*)(xr[j] + dcol);
+      if constexpr (HAS_E) e[j] = *(const u32x4*)(er[j] + dcol);
+    }
+#pragma unroll
+    for (int i = 0; i < NUL; ++i) {
+      const int q = lane + 64 * i;
+      if constexpr (KV) {
+        const int row = q / (KW / 8), cell = q % (KW / 8);
+        const bool ok = q < DC * KW / 8 && 8 * cell < k;
+        u[i] = ok ? *(const u32x4*)(U + (int64_t)(dcol + row) * k + 8 * cell) : u32x4{0u, 0u, 0u, 0u};
+      } else {
+        const bool ok = q < DC * k / 8;
+        u[i] = ok ? *(const u32x4*)(U + (int64_t)dcol * k + 8 * q) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+  auto park = [&](const u32x4 (&x)[NXL], const u32x4 (&e)[NXL], const u32x4 (&u)[NUL]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < NXL; ++j) {
+      const int q = lane + 64 * j, row = q / 8;
+      xtw[row * 8 + ((q % 8) ^ (row & 7))] = x[j];
+      if constexpr (HAS_E) xtw[R * 8 + row * 8 + ((q % 8) ^ (row & 7))] = e[j];
+    }
+#pragma clang loop unroll(full)
+    for (int i = 0; i < NUL; ++i) {
+      const int q = lane + 64 * i;
+      if constexpr (KV) {
+        if (q < DC * KW / 8) {
+          const int row = q / (KW / 8), cell = q % (KW / 8);
+          *(u32x4*)(utw + row * UP + 8 * cell) = u[i];
+        }
+      } else if (q < DC * k / 8) {
+        const uint32_t w[4] = {u[i][0], u[i][1], u[i][2], u[i][3]};
+        int row = (8 * q) / k, col = 8 * q - row * k;
+#pragma clang loop unroll(full)
+        for (int e2 = 0; e2 < 8; ++e2) {
+          utw[row * UP + col] = (uint16_t)((e2 & 1) ? (w[e2 >> 1] >> 16) : (w[e2 >> 1] & 0xFFFFu));
+          const bool wrap = (col + 1 == k);
+          col = wrap ? 0 : col + 1;
+          row = wrap ? row + 1 : row;
+        }
+      }
+    }
+  };
+
+  f32x4 accX[TTW][KP], accE[TTW][KP];
+#pragma unroll
+  for (int tt = 0; tt < TTW; ++tt)
+#pragma unroll
+    for (int i = 0; i < KP; ++i) {
+      accX[tt][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      accE[tt][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  auto compute = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < DC / 32; ++s) {
+      const int cell = (4 * s + g) ^ (n16 & 7);
+      u32x4 xa[TTW], ea[TTW];
+#pragma unroll
+      for (int tt = 0; tt < TTW; ++tt) {
+        xa[tt] = xtw[(16 * tt + n16) * 8 + cell];
+        if constexpr (HAS_E) ea[tt] = xtw[R * 8 + (16 * tt + n16) * 8 + cell];
+      }
+      const int r = 32 * s + 8 * g + (n16 >> 2);
+#pragma unroll
+      for (int i = 0; i < KP; ++i) {
+        const uint16_t* p = utw + r * UP + 16 * i + 4 * (n16 & 3);
+        const u32x2 a = lds_read_tr16(p), b = lds_read_tr16(p + 4 * UP);
+        const u32x4 bfr = u32x4{a[0], a[1], b[0], b[1]};
+#pragma unroll
+        for (int tt = 0; tt < TTW; ++tt) {
+          accX[tt][i] = mfma16x16x32(xa[tt], bfr, accX[tt][i]);
+          if constexpr (HAS_E) accE[tt][i] = mfma16x16x32(ea[tt], bfr, accE[tt][i]);
+        }
+      }
+    }
+  };
+  auto step = [&](int i, auto S) __attribute__((always_inline)) {
+    constexpr int sl = decltype(S)::value;       // register set of chunk i + 1
+    compute();
+    if (i + 1 < nchp) park(xs[sl], es[sl], us[sl]);
+    if (i + 3 < nchp) load(c0 + i + 3, xs[sl], es[sl], us[sl]);
+  };
+  load(c0, xs[0], es[0], us[0]);
+  park(xs[0], es[0], us[0]);
+  if (nchp > 1) load(c0 + 1, xs[1], es[1], us[1]);
+  if (nchp > 2) load(c0 + 2, xs[0], es[0], us[0]);
+  for (int i = 0; i < nchp; i += 2) {
+    step(i, std::integral_constant<int, 1>{});
+    if (i + 1 < nchp) step(i + 1, std::integral_constant<int, 0>{});
+  }
+
+  // ---- partial results of the P ranges of d, summed in wave order ----
+  __syncthreads();                             // the staging tiles become the reduction buffer
+  f32x4* const red = (f32x4*)smem;             // [wave][tt][i][lane]
+#pragma unroll
+  for (int tt = 0; tt < TTW; ++tt)
+#pragma unroll
+    for (int i = 0; i < KP; ++i)
+      red[((wave * TTW + tt) * KP + i) * 64 + lane] = HAS_E ? accX[tt][i] - accE[tt][i] : accX[tt][i];
+  __syncthreads();
+  for (int idx = tid; idx < TTW * KP * 64; idx += 64 * P) {
+    const int l = idx % 64, ti = idx / 64, i = ti % KP, tt = ti / KP;
+    f32x4 sum = red[ti * 64 + l];
+#pragma unroll
+    for (int w = 1; w < P; ++w) sum += red[(w * TTW * KP + ti) * 64 + l];
+    // lane l of tile (tt, i) holds Z[tok0 + 16 tt + 4 (l/16) + e][16 i + l % 16]
+    const int col = 16 * i + (l & 15);
+    if (col < k) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t t = tok0 + 16 * tt + 4 * (l >> 4) + e;
+        if (t < N) {
+          float v = sum[e];
+          if constexpr (HAS_P) v -= Pt[clamp_id(ids[t], V) * k + col];
+          Z[t * k + col] = v;
+        }
+      }
+    }
+  }
+}
+
+// ===========================================================================
 // decompress / gradient expansion, bf16 storage, MFMA.
 //
 // Computes Y^T tiles [16 d x 16 tokens] = U_rows [16 d x k] . Z^T [k x 16 tok]
@@ -364,13 +556,20 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
 // ===========================================================================
 constexpr int kDecompressDC = 64;
 
-template <int KS2, bool HAS_E, bool KFULL32, int DC = kDecompressDC, int PF = 1, int DSPLIT = 1,
+// KM: 0 when k == 32*KS2; 1 when k % 8 == 0 (16-byte rows of U and Z, zero
+// groups past k); 2 for any other k: Z is read element by element, and each
+// chunk of U (DC whole rows, one contiguous span of DC*k bf16 that starts
+// 16-byte aligned) is read with 16-byte loads and scattered element by
+// element into the zero-padded fragment layout.
+template <int KS2, bool HAS_E, int KM, int DC = kDecompressDC, int PF = 1, int DSPLIT = 1,
           int TW = 4, bool NTS = false>
 __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     uint16_t* __restrict__ Y, int64_t N, int d, int k, int64_t V) {
   static_assert(DC == 64 || DC == 128, "chunk of 64 or 128 d");
+  static_assert(KM >= 0 && KM <= 2, "k layout mode");
+  constexpr bool KFULL32 = (KM == 0);
   constexpr int NT = DC / 16;                     // MFMA tiles per chunk
   constexpr int FR = NT * KS2 * kWave;            // A fragments per chunk
   constexpr int PT = 64 * TW;                      // stager threads per part
@@ -395,14 +594,17 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     for (int s = 0; s < KS2; ++s) {
       const int c0 = 32 * s + 8 * g;
       float v[8];
-      if (KFULL32 || c0 + 8 <= k) {
+      if constexpr (KM == 2) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = (c0 + e < k) ? zp[c0 + e] : 0.f;
+      } else if (KFULL32 || c0 + 8 <= k) {
         const f32x4 a = *(const f32x4*)(zp + c0);
         const f32x4 b = *(const f32x4*)(zp + c0 + 4);
         v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
         v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
       } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = 0.f;   // k % 8 == 0 on this path
+        for (int e = 0; e < 8; ++e) v[e] = 0.f;   // the whole group lies past k
       }
       split_bf16x8(v, zhi[s], zlo[s]);
     }
@@ -438,18 +640,56 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
   }
   u32x4 ust[FPT];
   auto load_u = [&](int c) {
+    if constexpr (KM == 2) {
+      // pieces of 8 consecutive elements of the chunk's span of DC*k
+      const uint16_t* span = U + (int64_t)c * DC * k;
 #pragma unroll
-    for (int q = 0; q < FPT; ++q)
-      if (stid + PT * q < FR)
-        ust[q] = (KFULL32 || scol[q] < k)
-                     ? *(const u32x4*)(U + (int64_t)(c * DC + srow[q]) * k + scol[q])
-                     : u32x4{0u, 0u, 0u, 0u};
+      for (int q = 0; q < FPT; ++q)
+        if (stid + PT * q < DC * k / 8) ust[q] = *(const u32x4*)(span + 8 * (stid + PT * q));
+    } else {
+#pragma unroll
+      for (int q = 0; q < FPT; ++q)
+        if (stid + PT * q < FR)
+          ust[q] = (KFULL32 || scol[q] < k)
+                       ? *(const u32x4*)(U + (int64_t)(c * DC + srow[q]) * k + scol[q])
+                       : u32x4{0u, 0u, 0u, 0u};
+    }
   };
   auto store_u = [&](int buf) {
+    if constexpr (KM == 2) {
+      // element (r, col) of the chunk -> fragment (r/16)*KS2 + col/32, lane
+      // position 16*((col%32)/8) + r%16, element col%8
+      uint16_t* dst = (uint16_t*)(ufr[buf] + spart * FR);
 #pragma unroll
-    for (int q = 0; q < FPT; ++q)
-      if (stid + PT * q < FR) ufr[buf][spart * FR + stid + PT * q] = ust[q];
+      for (int q = 0; q < FPT; ++q) {
+        const int p = stid + PT * q;
+        if (p < DC * k / 8) {
+          int r = (8 * p) / k, col = 8 * p - r * k;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int f = ((r >> 4) * KS2 + (col >> 5)) * kWave + 16 * ((col & 31) >> 3) + (r & 15);
+            const uint32_t w = ust[q][e >> 1];
+            dst[8 * f + (col & 7)] = (uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu));
+            if (++col == k) {
+              col = 0;
+              ++r;
+            }
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < FPT; ++q)
+        if (stid + PT * q < FR) ufr[buf][spart * FR + stid + PT * q] = ust[q];
+    }
   };
+  if constexpr (KM == 2) {
+    // the padding (columns k .. 32*KS2) is never written by the scatter: zero
+    // both buffers once
+    for (int i = tid; i < 2 * DSPLIT * FR; i += 64 * TW * DSPLIT)
+      (&ufr[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+  }
   u32x4 ering[PF + 1][NQ];
   auto load_e = [&](int c, u32x4(&eo)[NQ]) {
     if constexpr (HAS_E) {
@@ -458,10 +698,16 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     }
   };
 
-  // part p walks chunks [p*nch, (p+1)*nch) of d (nch per part), rotated
-  const int nch = d / (DC * DSPLIT);
+  // blockIdx.y selects one of gridDim.y equal ranges of d (more blocks when
+  // there are few tokens); part p of the block walks chunks
+  // [(y*DSPLIT + p)*nch, +nch) of that range, rotated per block
+  const int nch = d / (DC * DSPLIT * (int)gridDim.y);
   const int rot = (int)(blockIdx.x % (unsigned)nch);
-  auto chunk_of = [&](int p, int i) { const int x = i + rot; return p * nch + (x < nch ? x : x - nch); };
+  const int pbase = (int)blockIdx.y * DSPLIT;
+  auto chunk_of = [&](int p, int i) {
+    const int x = i + rot;
+    return (pbase + p) * nch + (x < nch ? x : x - nch);
+  };
   auto chunk = [&](int i) { return chunk_of(part, i); };
   f32x4* st = stage[wave];
 
@@ -587,7 +833,7 @@ bool compress_uses_mfma(int dtype, int64_t d, int64_t k) {
 }
 
 bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) {
-  return dtype == kBF16 && d % (2 * kDecompressDC) == 0 && d <= INT32_MAX && k % 8 == 0 && k >= 8 && k <= 128;
+  return dtype == kBF16 && d % (2 * kDecompressDC) == 0 && d <= INT32_MAX && k >= 1 && k <= 128;
 }
 
 template <int KP, bool HAS_E, bool KFULL, int WAVES, int KS, bool HAS_P>
@@ -655,6 +901,63 @@ static unsigned generic_blocks(int64_t N) {
   return (unsigned)(want < 65536 ? want : 65536);
 }
 
+// Few tokens: 16-token blocks of P waves that split d (P = 2, 4, 8; P <= 4
+// when k > 64, where eight waves' tiles would not fit in LDS).
+template <int KP, bool HAS_E, bool HAS_P, int P, int TTW>
+static hipError_t launch_split_t(int64_t N, int d, int k, int64_t V, const void* X,
+                                 const int32_t* ids, const void* E, const void* U, float* Z,
+                                 const float* Pt, hipStream_t st) {
+  const dim3 grid((unsigned)((N + 16 * TTW - 1) / (16 * TTW)));
+  if (k % 8 == 0)
+    hipLaunchKernelGGL((compress_split_bf16<KP, HAS_E, HAS_P, true, P, TTW>), grid, dim3(64 * P), 0,
+                       st, (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k,
+                       V, Pt);
+  else
+    hipLaunchKernelGGL((compress_split_bf16<KP, HAS_E, HAS_P, false, P, TTW>), grid, dim3(64 * P), 0,
+                       st, (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k,
+                       V, Pt);
+  return hipGetLastError();
+}
+
+template <int KP, bool HAS_E, bool HAS_P>
+static hipError_t launch_split_kp(int P, int TTW, int64_t N, int d, int k, int64_t V, const void* X,
+                                  const int32_t* ids, const void* E, const void* U, float* Z,
+                                  const float* Pt, hipStream_t st) {
+  if constexpr (KP <= 4) {
+    if (P == 8) return launch_split_t<KP, HAS_E, HAS_P, 8, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st);
+    if (P == 4 && TTW == 2)
+      return launch_split_t<KP, HAS_E, HAS_P, 4, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st);
+  }
+  if (P >= 4) return launch_split_t<KP, HAS_E, HAS_P, 4, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st);
+  return launch_split_t<KP, HAS_E, HAS_P, 2, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st);
+}
+
+// When the d-split kernel runs (measured on MI355X at d = 4096 and 5120):
+// with k % 8 == 0 the token-parallel kernels win once N/64 (compress) or
+// N/128 (projection) blocks fill the chip, above 8192 and 16384 tokens; for
+// other k those kernels stage U element by element and the d-split kernel
+// wins at every N.
+static bool compress_uses_split(int64_t N, int64_t d, int64_t k, bool has_e) {
+  if (d % 128 != 0) return false;
+  if (k % 8 != 0) return true;
+  return N <= (has_e ? 8192 : 16384);
+}
+
+template <bool HAS_E, bool HAS_P>
+static hipError_t launch_split(int64_t N, int d, int k, int64_t V, const void* X, const int32_t* ids,
+                               const void* E, const void* U, float* Z, const float* Pt,
+                               hipStream_t st) {
+  // eight waves over d while that gives about eight waves per compute unit,
+  // else four; two token tiles per wave for the projections (with one stream
+  // of rows the registers allow it)
+  int P = N <= 6144 ? 8 : 4;
+  const int TTW = (P == 4 && !HAS_E) ? 2 : 1;
+  while (P > 2 && d % (64 * P) != 0) P /= 2;
+  if (k <= 32) return launch_split_kp<2, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st);
+  if (k <= 64) return launch_split_kp<4, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st);
+  return launch_split_kp<8, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st);
+}
+
 template <typename T, bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_generic(int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                                           const int32_t* ids, const void* E, const void* U,
@@ -671,6 +974,11 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
   const bool has_e = (E != nullptr), has_p = (P != nullptr);
   if (compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(Z) && (!has_e || al16(E)) &&
       (!has_p || al16(P))) {
+    if (compress_uses_split(N, d, k, has_e)) {
+      if (has_e) return launch_split<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
+      if (has_p) return launch_split<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
+      return launch_split<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
+    }
     if (has_e) return launch_compress_mfma<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
     if (has_p) return launch_compress_mfma<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
     return launch_compress_mfma<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
@@ -688,21 +996,34 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
 // 8 token tiles (128 tokens) x 2 halves of d per block (16 waves); the
 // activation rows are written with non-temporal stores (streamed out instead
 // of parked dirty in the caches, where they slowed the next kernel's reads)
-template <int KS2, bool HAS_E>
-static hipError_t launch_decompress_ks(int64_t N, int d, int k, int64_t V, const float* Zc,
+template <int KS2, bool HAS_E, int KM>
+static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
                                        hipStream_t st) {
   constexpr int TW = 8, DS = 2;
   const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
-  if (k == 32 * KS2)
-    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, true, kDecompressDC, 1, DS, TW, true>),
-                       dim3((unsigned)blocks), dim3(64 * TW * DS), 0, st, Zc, ids,
-                       (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
-  else
-    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, false, kDecompressDC, 1, DS, TW, true>),
-                       dim3((unsigned)blocks), dim3(64 * TW * DS), 0, st, Zc, ids,
-                       (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
+  // with few token tiles, also split d over the grid: the smallest divisor gy
+  // of the chunk-pair count that gives one block per compute unit
+  const int pairs = d / (kDecompressDC * DS);
+  const int64_t cus = device_cu_count();
+  int gy = 1;
+  while (gy < pairs && blocks * gy < cus) {
+    ++gy;
+    while (pairs % gy != 0) ++gy;
+  }
+  hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, DS, TW, true>),
+                     dim3((unsigned)blocks, (unsigned)gy), dim3(64 * TW * DS), 0, st, Zc, ids,
+                     (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
   return hipGetLastError();
+}
+
+template <int KS2, bool HAS_E>
+static hipError_t launch_decompress_ks(int64_t N, int d, int k, int64_t V, const float* Zc,
+                                       const int32_t* ids, const void* E, const void* U, void* Y,
+                                       hipStream_t st) {
+  if (k == 32 * KS2) return launch_decompress_km<KS2, HAS_E, 0>(N, d, k, V, Zc, ids, E, U, Y, st);
+  if (k % 8 == 0) return launch_decompress_km<KS2, HAS_E, 1>(N, d, k, V, Zc, ids, E, U, Y, st);
+  return launch_decompress_km<KS2, HAS_E, 2>(N, d, k, V, Zc, ids, E, U, Y, st);
 }
 
 template <bool HAS_E>

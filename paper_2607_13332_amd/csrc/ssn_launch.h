@@ -11,6 +11,9 @@ constexpr int kF32 = 0;
 constexpr int kBF16 = 1;
 constexpr int kMaxBatch = 16;
 
+// Compute units of the current device (cached per device).
+int device_cu_count();
+
 bool compress_uses_mfma(int dtype, int64_t d, int64_t k);
 bool decompress_uses_mfma(int dtype, int64_t d, int64_t k);
 bool weights_use_mfma(int dtype, int64_t d, int64_t k);

@@ -233,11 +233,15 @@ struct ColumnBatch {
 constexpr int kColRows = 64;           // rows per chunk
 constexpr int kColMinWaves = 4;
 // Waves per block at most: 10 (tiles per block <= 20) while the wave's
-// registers allow three waves per SIMD, 8 for k > 64.
-constexpr int cols_max_waves(int kt) { return kt > 4 ? 8 : 10; }
+// registers allow three waves per SIMD; 8 for k > 64 or k % 8 != 0.
+constexpr int cols_max_waves(int kt, bool kv) { return (kt > 4 || !kv) ? 8 : 10; }
 
-template <int KT, bool NTS, int DEPTH>
-__global__ __launch_bounds__(kWave * cols_max_waves(KT)) void project_weights_cols_bf16(
+// KV: k % 8 == 0, so U rows are whole 16-byte pieces.  Otherwise a chunk of
+// U (64 whole rows, one contiguous span of 64*k bf16 that starts 16-byte
+// aligned) is read with 16-byte loads and scattered element by element into
+// the zero-padded row tile.
+template <int KT, bool NTS, int DEPTH, bool KV>
+__global__ __launch_bounds__(kWave * cols_max_waves(KT, KV)) void project_weights_cols_bf16(
     ColumnBatch cb, const uint16_t* __restrict__ U, int d, int k) {
   static_assert(DEPTH == 1 || DEPTH == 2, "one or two chunks in flight");
   constexpr int R = kColRows, CT = 2;
@@ -247,7 +251,7 @@ __global__ __launch_bounds__(kWave * cols_max_waves(KT)) void project_weights_co
   constexpr int UPR = KW / 8;                        // U pieces (16 B) per row
   constexpr int UP = UPR + 1;                        // U row pitch in pieces
   constexpr int NUP = (R * UPR + kWave * kColMinWaves - 1) / (kWave * kColMinWaves);
-  constexpr int WPMAX = 4 * cols_max_waves(KT) + 1;
+  constexpr int WPMAX = 4 * cols_max_waves(KT, KV) + 1;
   __shared__ u32x4 wt[2][R * WPMAX];                 // W (pass 1) / output (pass 2) row tiles
   __shared__ u32x4 ut[2][R * UP];                    // U row tiles
 
@@ -292,18 +296,45 @@ __global__ __launch_bounds__(kWave * cols_max_waves(KT)) void project_weights_co
 #pragma unroll
     for (int i = 0; i < NUP; ++i) {
       const int q = tid + NT * i;
-      const int r = c * R + q / UPR, uc = 8 * (q % UPR);
-      const bool ok = q < R * UPR && uc < k && r < d;
-      v[i] = ok ? *(const u32x4*)(U + (int64_t)r * k + uc) : u32x4{0u, 0u, 0u, 0u};
+      if constexpr (KV) {
+        const int r = c * R + q / UPR, uc = 8 * (q % UPR);
+        const bool ok = q < R * UPR && uc < k && r < d;
+        v[i] = ok ? *(const u32x4*)(U + (int64_t)r * k + uc) : u32x4{0u, 0u, 0u, 0u};
+      } else {
+        // piece q of the chunk's span; d % 32 == 0 makes the end of U fall on
+        // a piece boundary
+        const int64_t e0 = (int64_t)c * R * k + 8 * q;
+        const bool ok = q < R * k / 8 && e0 + 8 <= (int64_t)d * k;
+        v[i] = ok ? *(const u32x4*)(U + e0) : u32x4{0u, 0u, 0u, 0u};
+      }
     }
   };
   auto park_u = [&](int buf, const u32x4 (&v)[NUP]) {
 #pragma unroll
     for (int i = 0; i < NUP; ++i) {
       const int q = tid + NT * i;
-      if (q < R * UPR) ut[buf][(q / UPR) * UP + q % UPR] = v[i];
+      if constexpr (KV) {
+        if (q < R * UPR) ut[buf][(q / UPR) * UP + q % UPR] = v[i];
+      } else if (q < R * k / 8) {
+        uint16_t* t = (uint16_t*)ut[buf];
+        int r = (8 * q) / k, col = 8 * q - r * k;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t w = v[i][e >> 1];
+          t[r * (8 * UP) + col] = (uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu));
+          if (++col == k) {
+            col = 0;
+            ++r;
+          }
+        }
+      }
     }
   };
+  if constexpr (!KV) {
+    // columns k .. KW of the U tiles are never written by the scatter
+    for (int i = tid; i < 2 * R * UP; i += NT) (&ut[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+  }
 
   // ------------------------------ pass 1 ---------------------------------
   f32x4 acc[KT][CT];
@@ -477,7 +508,7 @@ __global__ __launch_bounds__(256) void project_weights_generic(T* __restrict__ W
 }
 
 bool weights_use_mfma(int dtype, int64_t d, int64_t k) {
-  return dtype == kBF16 && d % 32 == 0 && d <= INT32_MAX && k % 8 == 0 && k >= 8 && k <= 128;
+  return dtype == kBF16 && d % 32 == 0 && d <= INT32_MAX && k >= 1 && k <= 128;
 }
 
 template <int KT>
@@ -488,7 +519,7 @@ static hipError_t launch_weights_kt(const PanelBatch& pb, int blocks, const void
   return hipGetLastError();
 }
 
-static int device_cu_count() {
+int device_cu_count() {
   static int cus[64] = {0};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
@@ -501,17 +532,25 @@ static int device_cu_count() {
   return cus[dev];
 }
 
-template <int KT>
-static hipError_t launch_cols(ColumnBatch cb, int cus, const void* U, int d, int k, hipStream_t st) {
-  constexpr int kMaxTpb = 2 * cols_max_waves(KT);
+template <int KT, bool KV>
+static hipError_t launch_cols_kv(ColumnBatch cb, int cus, const void* U, int d, int k, hipStream_t st) {
+  constexpr int kMaxTpb = 2 * cols_max_waves(KT, KV);
+  // one chunk in flight where two would spill registers (k > 64, k % 8 != 0)
+  constexpr int DEPTH = (KT > 4 && !KV) ? 1 : 2;
   int tpb = (cb.tiles + cus - 1) / cus;
   cb.tpb = tpb < 1 ? 1 : (tpb > kMaxTpb ? kMaxTpb : tpb);
   int waves = (cb.tpb + 1) / 2;
   waves = waves < kColMinWaves ? kColMinWaves : waves;
   const unsigned grid = (unsigned)((cb.tiles + cb.tpb - 1) / cb.tpb);
-  hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, 2>), dim3(grid), dim3(kWave * waves), 0, st,
-                     cb, (const uint16_t*)U, d, k);
+  hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, DEPTH, KV>), dim3(grid), dim3(kWave * waves),
+                     0, st, cb, (const uint16_t*)U, d, k);
   return hipGetLastError();
+}
+
+template <int KT>
+static hipError_t launch_cols(const ColumnBatch& cb, int cus, const void* U, int d, int k, hipStream_t st) {
+  return k % 8 == 0 ? launch_cols_kv<KT, true>(cb, cus, U, d, k, st)
+                    : launch_cols_kv<KT, false>(cb, cus, U, d, k, st);
 }
 
 hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t* n, int64_t k,
@@ -547,7 +586,8 @@ hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t
     if (kt <= 4) return launch_cols<4>(cb, cus, U, (int)d, (int)k, st);
     return launch_cols<8>(cb, cus, U, (int)d, (int)k, st);
   }
-  if (weights_use_mfma(dtype, d, k) && aligned && panels <= INT32_MAX) {
+  // the 64-column panel kernel reads U rows as 16-byte pieces: k % 8 == 0
+  if (weights_use_mfma(dtype, d, k) && k % 8 == 0 && aligned && panels <= INT32_MAX) {
     PanelBatch pb{};
     int nb = 0;
     int32_t acc = 0;

@@ -176,7 +176,30 @@ def sweep_configs():
     return out
 
 
-CONFIGS = {c.name: c for c in [TINY, MID, STAGE8B] + sweep_configs()}
+def paper_configs():
+    """The paper's own stage-boundary shapes (section 4.2 model card and the
+    1B ablation card of section 6): Pluralis-8B d=5120 at rank ~51 (100x),
+    S=4096; the 1B model d=2048 at rank 40, S=2048; vocabulary 128,256; a
+    microbatch of b coalesced sequences, b in {1, 2, 3}."""
+    out = []
+    for b in (1, 2, 3):
+        out.append(CodecConfig(f"paper8b_b{b}", B=b, S=4096, d=5120, k=51, V=128256,
+                               dtype="bf16", seed=1020 + b, structured=False))
+    for b in (1, 2, 3):
+        out.append(CodecConfig(f"paper1b_b{b}", B=b, S=2048, d=2048, k=40, V=128256,
+                               dtype="bf16", seed=1024 + b, structured=False))
+    return out
+
+
+# Output projections of one body stage (4 layers) at the paper's shapes:
+# W_o [d, d] and W_down [d, ffn] with ffn = d * 8/3 * 1.3 rounded up to a
+# multiple of 1024 (18,432 at d=5120, 7,168 at d=2048).
+WEIGHTS_PAPER8B = WeightsConfig("weights_paper8b", d=5120, k=51, layers=4,
+                                shapes=((5120, 5120), (5120, 18432)), dtype="bf16", seed=1030)
+WEIGHTS_PAPER1B = WeightsConfig("weights_paper1b", d=2048, k=40, layers=4,
+                                shapes=((2048, 2048), (2048, 7168)), dtype="bf16", seed=1031)
+
+CONFIGS = {c.name: c for c in [TINY, MID, STAGE8B] + sweep_configs() + paper_configs()}
 
 
 def with_tokens(cfg: CodecConfig, N: int, seed: Optional[int] = None) -> CodecConfig:

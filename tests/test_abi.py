@@ -63,7 +63,10 @@ def test_kernel_family_rules(ssn):
     assert kf("compress", "f32", 256, 8) == "generic"
     assert kf("project_grad", "bf16", 2048, 32) == "mfma"
     assert kf("decompress", "bf16", 4096, 64) == "mfma"
-    assert kf("decompress", "bf16", 4096, 51) == "generic"
+    assert kf("decompress", "bf16", 4096, 51) == "mfma"
+    assert kf("decompress", "bf16", 5120, 1) == "mfma"
+    assert kf("decompress", "bf16", 4096, 129) == "generic"
+    assert kf("project_weights", "bf16", 5120, 51) == "mfma"
     assert kf("decompress", "bf16", 4064, 64) == "generic"
     assert kf("project_weights", "bf16", 4096, 64) == "mfma"
     assert kf("project_weights", "f32", 4096, 64) == "generic"

@@ -72,3 +72,30 @@ def test_config_table():
     sw = I.sweep_configs()
     assert len(sw) == 12 and {c.k for c in sw} == {32, 64, 128}
     assert {c.N for c in sw} == {4096, 16384, 65536, 131072}
+
+
+def test_paper_configs_follow_the_model_cards():
+    """The paper-shaped workloads are the shapes the paper prints (fixtures
+    in tests/golden cite the passages)."""
+    import json
+    import math
+    import os
+    fig = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_figures.json")))
+    m8, r8, m1 = fig["model_8b"], fig["rank_8b"], fig["model_1b"]
+    p8 = [c for c in I.paper_configs() if c.name.startswith("paper8b")]
+    p1 = [c for c in I.paper_configs() if c.name.startswith("paper1b")]
+    assert {c.B for c in p8} == {1, 2, 3} and {c.B for c in p1} == {1, 2, 3}
+    for c in p8:
+        assert (c.d, c.k, c.V, c.S) == (m8["d"], r8["rank"], m8["vocab"], m8["seq_len"])
+    for c in p1:
+        assert (c.d, c.k, c.V, c.S) == (m1["d"], m1["rank"], m1["vocab"], m1["seq_len"])
+    # Llama-style FFN width: 8/3 d times the multiplier, rounded up to 1024
+    ffn8 = math.ceil(m8["d"] * 8 / 3 * m8["ffn_multiplier"] / m8["ffn_round"]) * m8["ffn_round"]
+    ffn1 = math.ceil(m1["d"] * 8 / 3 * m8["ffn_multiplier"] / m8["ffn_round"]) * m8["ffn_round"]
+    assert ffn1 == m1["ffn_inner"]              # the rule reproduces the printed 1B width
+    w8, w1 = I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B
+    assert (w8.d, w8.k, w8.layers) == (m8["d"], r8["rank"], m8["body_layers"])
+    assert tuple(w8.shapes) == ((m8["d"], m8["d"]), (m8["d"], ffn8))
+    assert (w1.d, w1.k, w1.layers) == (m1["d"], m1["rank"], m1["body_layers"])
+    assert tuple(w1.shapes) == ((m1["d"], m1["d"]), (m1["d"], m1["ffn_inner"]))
+
