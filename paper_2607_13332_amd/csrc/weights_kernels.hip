@@ -233,25 +233,29 @@ struct ColumnBatch {
 constexpr int kColRows = 64;           // rows per chunk
 constexpr int kColMinWaves = 4;
 // Waves per block at most: 10 (tiles per block <= 20) while the wave's
-// registers allow three waves per SIMD; 8 for k > 64 or k % 8 != 0.
-constexpr int cols_max_waves(int kt, bool kv) { return (kt > 4 || !kv) ? 8 : 10; }
+// registers allow three waves per SIMD; 8 for k > 64 or k % 8 != 0, and for
+// three tiles per wave.
+constexpr int cols_max_waves(int kt, bool kv, int ct) { return (kt > 4 || !kv || ct > 2) ? 8 : 10; }
 
 // KV: k % 8 == 0, so U rows are whole 16-byte pieces.  Otherwise a chunk of
 // U (64 whole rows, one contiguous span of 64*k bf16 that starts 16-byte
 // aligned) is read with 16-byte loads and scattered element by element into
 // the zero-padded row tile.
-template <int KT, bool NTS, int DEPTH, bool KV>
-__global__ __launch_bounds__(kWave * cols_max_waves(KT, KV)) void project_weights_cols_bf16(
+template <int KT, bool NTS, int DEPTH, bool KV, int CT = 2>
+__global__ __launch_bounds__(kWave * cols_max_waves(KT, KV, CT)) void project_weights_cols_bf16(
     ColumnBatch cb, const uint16_t* __restrict__ U, int d, int k) {
   static_assert(DEPTH == 1 || DEPTH == 2, "one or two chunks in flight");
-  constexpr int R = kColRows, CT = 2;
-  constexpr int RP = 16, NPW = R / RP;               // rows per pass, W pieces per thread per chunk
+  static_assert(CT == 2 || CT == 3, "two or three tiles per wave");
+  constexpr int R = kColRows;
+  // rows per pass (threads t < RP*H each move one 16-byte piece per pass) and
+  // W pieces per thread per chunk
+  constexpr int RP = CT == 2 ? 16 : 8, NPW = R / RP;
   constexpr int KS2 = (KT + 1) / 2;
   constexpr int KW = 32 * KS2;                       // U tile width (bf16), zero padded past k
   constexpr int UPR = KW / 8;                        // U pieces (16 B) per row
   constexpr int UP = UPR + 1;                        // U row pitch in pieces
   constexpr int NUP = (R * UPR + kWave * kColMinWaves - 1) / (kWave * kColMinWaves);
-  constexpr int WPMAX = 4 * cols_max_waves(KT, KV) + 1;
+  constexpr int WPMAX = 2 * CT * cols_max_waves(KT, KV, CT) + 1;
   __shared__ u32x4 wt[2][R * WPMAX];                 // W (pass 1) / output (pass 2) row tiles
   __shared__ u32x4 ut[2][R * UP];                    // U row tiles
 
@@ -534,16 +538,24 @@ int device_cu_count() {
 
 template <int KT, bool KV>
 static hipError_t launch_cols_kv(ColumnBatch cb, int cus, const void* U, int d, int k, hipStream_t st) {
-  constexpr int kMaxTpb = 2 * cols_max_waves(KT, KV);
   // one chunk in flight where two would spill registers (k > 64, k % 8 != 0)
   constexpr int DEPTH = (KT > 4 && !KV) ? 1 : 2;
+  constexpr int W2 = cols_max_waves(KT, KV, 2), W3 = cols_max_waves(KT, KV, 3);
+  // three tiles per wave only for k <= 64, where its registers fit
+  constexpr int kMaxTpb = KT <= 4 ? 3 * W3 : 2 * W2;
   int tpb = (cb.tiles + cus - 1) / cus;
   cb.tpb = tpb < 1 ? 1 : (tpb > kMaxTpb ? kMaxTpb : tpb);
-  int waves = (cb.tpb + 1) / 2;
-  waves = waves < kColMinWaves ? kColMinWaves : waves;
   const unsigned grid = (unsigned)((cb.tiles + cb.tpb - 1) / cb.tpb);
-  hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, DEPTH, KV>), dim3(grid), dim3(kWave * waves),
-                     0, st, cb, (const uint16_t*)U, d, k);
+  if (cb.tpb <= 2 * W2) {
+    int waves = (cb.tpb + 1) / 2;
+    waves = waves < kColMinWaves ? kColMinWaves : waves;
+    hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, DEPTH, KV, 2>), dim3(grid),
+                       dim3(kWave * waves), 0, st, cb, (const uint16_t*)U, d, k);
+  } else if constexpr (KT <= 4) {
+    const int waves = (cb.tpb + 2) / 3;
+    hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, DEPTH, KV, 3>), dim3(grid),
+                       dim3(kWave * waves), 0, st, cb, (const uint16_t*)U, d, k);
+  }
   return hipGetLastError();
 }
 

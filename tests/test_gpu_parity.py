@@ -287,6 +287,8 @@ BATCHES = [  # (d, k, [n...]): several matrices per launch; 16-column tiles that
     (160, 51, [30000, 24, 520]),
     (96, 115, [33000, 8]),
     (64, 13, [70000, 16]),
+    (64, 64, [96000, 8]),          # 21-24 tiles per block: three tiles per wave
+    (96, 51, [100000]),
 ]
 
 
