@@ -19,7 +19,9 @@ region) is timed separately and reported under "variants"; the headline value
 is the step with compress as written in Eq. (2).  The same step at the
 paper's own stage shapes (Pluralis-8B d=5120, k=51, V=128,256, S=4096; the 1B
 ablation model d=2048, k=40, S=2048; b = 1 and 3 coalesced sequences) and the
-weight re-projection at those shapes are reported under "paper_shapes".
+weight re-projection at those shapes are reported under "paper_shapes", and
+the k=64 points of the sweep (d=4096, N=4096..131072, Zipf(1.1) ids) under
+"sweep_k64".
 
 Prints ONE JSON line (rank 0).  `--gpus` above 1 is refused: this build runs
 on one GPU.
@@ -59,6 +61,8 @@ def parse_args():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-weights", action="store_true")
+    p.add_argument("--no-sweep", action="store_true",
+                   help="skip the k=64 sweep points (d=4096, N=4096..131072, Zipf ids)")
     p.add_argument("--no-paper-shapes", action="store_true",
                    help="skip the timings at the paper's own stage shapes (d=5120 k=51, d=2048 k=40)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -214,7 +218,8 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         step_bytes += byts
         per_op[op] = {"ms": round(t, 5), "algorithmic_GBps": round(byts / (t * 1e-3) / 1e9, 1),
                       "frac_hbm_peak": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-    out = {"workload": f"N={N} (B={cfg.B} x S={cfg.S}), d={d}, k={k}, V={cfg.V}, bf16",
+    out = {"workload": f"N={N} (B={cfg.B} x S={cfg.S}), d={d}, k={k}, V={cfg.V}, bf16, "
+                       f"{cfg.ids_dist} ids",
            "ms_per_step": round(ms, 5), "tokens_per_s": round(N / (ms * 1e-3), 1),
            "step_frac_hbm_peak": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "per_op": per_op}
@@ -389,6 +394,11 @@ def main():
     # ---------------- weight re-projection (once per optimizer step) ----------------
     if not args.no_weights:
         result["weights"] = time_weights(I.WEIGHTS, args.steps, dev)
+
+    # ---------------- sweep points at k = 64 (Zipf ids) ----------------
+    if not args.no_sweep:
+        result["sweep_k64"] = {c.name: time_codec_config(c, max(10, args.steps // 2), args.warmup, dev)
+                               for c in I.sweep_configs() if c.k == 64}
 
     # ---------------- the paper's own shapes ----------------
     if not args.no_paper_shapes:
