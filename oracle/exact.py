@@ -84,5 +84,34 @@ def project_weights(W, U):
     return out
 
 
+def _matmul(A, B):
+    """Exact product of two Fraction matrices (nested loops)."""
+    n, m = A.shape
+    p = B.shape[1]
+    out = np.empty((n, p), dtype=object)
+    for i in range(n):
+        for j in range(p):
+            acc = Fraction(0)
+            for t in range(m):
+                acc += A[i, t] * B[t, j]
+            out[i, j] = acc
+    return out
+
+
+def reparam_forward(H, Zp, U):
+    """Y = H W with the weight formed explicitly, W = Zp U^T (the function the
+    factorization must reproduce)."""
+    W = _matmul(_frac(Zp), _frac(U).T)
+    return _matmul(_frac(H), W)
+
+
+def bilinear(G, Y):
+    """<G, Y> = sum of elementwise products (a loss that is linear in Y)."""
+    acc = Fraction(0)
+    for g, y in zip(np.asarray(G, dtype=object).ravel(), np.asarray(Y, dtype=object).ravel()):
+        acc += g * y
+    return acc
+
+
 def to_float(a) -> np.ndarray:
     return np.vectorize(float, otypes=[np.float64])(a)

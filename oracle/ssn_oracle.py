@@ -108,6 +108,57 @@ def project_weights(W, U) -> np.ndarray:
     return U64 @ T
 
 
+# --------------------------------------------------------------------------
+# Reparameterized SSN (section 4.1, Eq. (3)).  An output projection W [din, d]
+# (row-vector convention of Eq. (1): a layer adds H W to the residual stream,
+# H [N, din]) is stored as its factor Zp [din, k] with W = Zp U^T, so every
+# row of W lies in span(U).  The layer never forms W:
+#   forward            Y = (H Zp) U^T                          [N, d]
+#   input gradient     dL/dH = dL/dY W^T = (dL/dY U) Zp^T       [N, din]
+#   factor gradient    dL/dZp = (dL/dW) U = H^T (dL/dY U)       [din, k]
+# and the trainable embedding is factored the same way, T_S = E U^T, looked up
+# by token id: X0 = E[ids] U^T with E [V, k].
+# --------------------------------------------------------------------------
+def reparam_forward(H, Zp, U) -> np.ndarray:
+    """Y = (H Zp) U^T, row blocks of H."""
+    H = np.asarray(H)
+    Zp64, U64 = f64(Zp), f64(U)
+    N = H.shape[0]
+    out = np.empty((N, U64.shape[0]), dtype=np.float64)
+    for r0 in range(0, N, ROW_BLOCK):
+        r1 = min(N, r0 + ROW_BLOCK)
+        out[r0:r1] = (f64(H[r0:r1]) @ Zp64) @ U64.T
+    return out
+
+
+def reparam_grad_input(G, Zp, U) -> np.ndarray:
+    """dL/dH = (G U) Zp^T for G = dL/dY [N, d]."""
+    G = np.asarray(G)
+    Zp64, U64 = f64(Zp), f64(U)
+    N = G.shape[0]
+    out = np.empty((N, Zp64.shape[0]), dtype=np.float64)
+    for r0 in range(0, N, ROW_BLOCK):
+        r1 = min(N, r0 + ROW_BLOCK)
+        out[r0:r1] = (f64(G[r0:r1]) @ U64) @ Zp64.T
+    return out
+
+
+def reparam_grad_factor(H, G, U) -> np.ndarray:
+    """dL/dZp = H^T (G U) [din, k], summed over row blocks of the tokens."""
+    H, G = np.asarray(H), np.asarray(G)
+    U64 = f64(U)
+    out = np.zeros((H.shape[1], U64.shape[1]), dtype=np.float64)
+    for r0 in range(0, H.shape[0], ROW_BLOCK):
+        r1 = min(H.shape[0], r0 + ROW_BLOCK)
+        out += f64(H[r0:r1]).T @ (f64(G[r0:r1]) @ U64)
+    return out
+
+
+def factored_embedding(E, ids, U) -> np.ndarray:
+    """X0 = E[ids] U^T for the factored embedding table E [V, k]."""
+    return decompress(np.asarray(E)[np.asarray(ids)], None, None, U)
+
+
 def rel_frobenius(got, ref) -> float:
     """||got - ref||_F / ||ref||_F in float64 (the parity metric)."""
     g = f64(got) if np.asarray(got).dtype == np.uint16 else np.asarray(got, dtype=np.float64)

@@ -215,3 +215,69 @@ def test_paper_wire_figures():
     assert round(c1["d"] / c1["rank"]) == c1["rate"]
     # the codec message is 1/rate of the uncompressed one (activations in FP32)
     assert O.boundary_bits(b["tokens"], c8["wire_width"], 32) == pytest.approx(bits / c8["rate"])
+
+
+# ---------------------------------------------------------------- reparameterized SSN
+def test_reparam_forward_equals_the_formed_weight():
+    """Eq. (3): the factorized layer computes the same function as H W with
+    W = Zp U^T formed explicitly (exact rational brute force)."""
+    r = np.random.default_rng(3)
+    N, din, d, k = 4, 6, 5, 2
+    H = I.store(r.standard_normal((N, din)), "bf16")
+    Zp = I.store(r.standard_normal((din, k)), "bf16")
+    U = I.store(I.gaussian_orthonormal_basis(d, k, 3), "bf16")
+    ref = exact.to_float(exact.reparam_forward(H, Zp, U))
+    assert _rel(O.reparam_forward(H, Zp, U), ref) < 1e-14
+
+
+def test_reparam_gradients_by_exact_perturbation():
+    """L = <G, Y> is linear in H and in Zp, so a perturbation by t in one
+    entry changes L by exactly t times that entry of the gradient (exact
+    rational arithmetic, forward function only)."""
+    from fractions import Fraction
+    r = np.random.default_rng(11)
+    N, din, d, k = 3, 5, 4, 2
+    H = r.standard_normal((N, din)).astype(np.float32)
+    Zp = r.standard_normal((din, k)).astype(np.float32)
+    U = I.gaussian_orthonormal_basis(d, k, 11).astype(np.float32)
+    G = r.standard_normal((N, d)).astype(np.float32)
+    Gf = exact._frac(G)
+    L0 = exact.bilinear(Gf, exact.reparam_forward(H, Zp, U))
+    gZ = O.reparam_grad_factor(H, G, U)
+    gH = O.reparam_grad_input(G, Zp, U)
+    t = 0.5
+    for (i, j) in [(0, 0), (din - 1, k - 1), (2, 1)]:
+        Zq = Zp.copy()
+        Zq[i, j] += np.float32(t)
+        dL = exact.bilinear(Gf, exact.reparam_forward(H, Zq, U)) - L0
+        step = Fraction(float(Zq[i, j])) - Fraction(float(Zp[i, j]))
+        assert abs(float(dL / step) - gZ[i, j]) <= 1e-12 * max(1.0, abs(gZ[i, j]))
+    for (i, j) in [(0, 0), (N - 1, din - 1), (1, 3)]:
+        Hq = H.copy()
+        Hq[i, j] += np.float32(t)
+        dL = exact.bilinear(Gf, exact.reparam_forward(Hq, Zp, U)) - L0
+        step = Fraction(float(Hq[i, j])) - Fraction(float(H[i, j]))
+        assert abs(float(dL / step) - gH[i, j]) <= 1e-12 * max(1.0, abs(gH[i, j]))
+
+
+def test_reparam_rows_stay_in_the_subspace_and_embedding_round_trips():
+    """Every row of the layer output lies in span(U): compressing it (E = 0)
+    recovers H Zp exactly in exact arithmetic; the factored embedding looked
+    up by id and compressed returns the factor rows E[ids]."""
+    r = np.random.default_rng(5)
+    N, din, d, k, V = 6, 7, 16, 3, 9
+    U = I.hadamard_basis(d, k, 5)                     # exactly orthonormal
+    H = r.standard_normal((N, din))
+    Zp = r.standard_normal((din, k))
+    Y = O.reparam_forward(H, Zp, U)
+    zeros = np.zeros((1, d))
+    ids0 = np.zeros(N, dtype=np.int32)
+    assert _rel(O.compress(Y, ids0, zeros, U), H @ Zp) < 1e-13
+    Ef = r.standard_normal((V, k))
+    ids = r.integers(0, V, size=N).astype(np.int32)
+    X0 = O.factored_embedding(Ef, ids, U)
+    assert _rel(O.compress(X0, ids0, zeros, U), Ef[ids]) < 1e-13
+    # the factor gradient is the weight gradient projected onto U
+    G = r.standard_normal((N, d))
+    assert _rel(O.reparam_grad_factor(H, G, U), (H.T @ G) @ U) < 1e-13
+
