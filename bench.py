@@ -43,6 +43,7 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_2607_13332_amd/csrc/codec_kernels.hip",
                   "paper_2607_13332_amd/csrc/weights_kernels.hip",
+                  "paper_2607_13332_amd/csrc/reparam_kernels.hip",
                   "paper_2607_13332_amd/csrc/ssn_device.h"]
 
 
@@ -63,6 +64,8 @@ def parse_args():
     p.add_argument("--no-weights", action="store_true")
     p.add_argument("--no-sweep", action="store_true",
                    help="skip the k=64 sweep points (d=4096, N=4096..131072, Zipf ids)")
+    p.add_argument("--no-reparam", action="store_true",
+                   help="skip the reparameterized-SSN projection timings")
     p.add_argument("--no-paper-shapes", action="store_true",
                    help="skip the timings at the paper's own stage shapes (d=5120 k=51, d=2048 k=40)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -162,6 +165,52 @@ def time_weights(wc, steps: int, dev):
     if wc.name == I.WEIGHTS.name:
         out["traffic"] = load_traffic("project_weights")
     del Ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def time_reparam(N: int, din: int, d: int, k: int, steps: int, dev, seed: int = 1040):
+    """Reparameterized-SSN projection of one layer: forward (H Zp) U^T and the
+    backward (G U, (G U) Zp^T, H^T (G U)), bf16 storage."""
+    import numpy as np
+    import torch
+    from paper_2607_13332_amd import inputs as I
+    from paper_2607_13332_amd import ssn
+    g = torch.Generator(device=dev).manual_seed(seed)
+    H = torch.randn((N, din), generator=g, device=dev).to(torch.bfloat16)
+    G = torch.randn((N, d), generator=g, device=dev).to(torch.bfloat16)
+    Zp = (0.02 * torch.randn((din, k), generator=g, device=dev)).to(torch.bfloat16)
+    U = I.to_device(I.store(I.gaussian_orthonormal_basis(d, k, seed), "bf16"), "bf16", dev)
+    T = torch.empty((N, k), dtype=torch.float32, device=dev)
+    Y = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+    GT = torch.empty((N, k), dtype=torch.float32, device=dev)
+    GH = torch.empty((N, din), dtype=torch.bfloat16, device=dev)
+    GZ = torch.empty((din, k), dtype=torch.float32, device=dev)
+    ws = torch.empty((max(4, ssn.reparam_workspace_bytes("bf16", N, din, k)) + 3) // 4,
+                     dtype=torch.float32, device=dev)
+    for _ in range(3):
+        ssn.reparam_forward(H, Zp, U, T, Y)
+        ssn.reparam_backward(H, Zp, U, G, GT, GH, GZ, ws)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    for i in range(steps):
+        ev[i][0].record()
+        ssn.reparam_forward(H, Zp, U, T, Y)
+        ev[i][1].record()
+        ssn.reparam_backward(H, Zp, U, G, GT, GH, GZ, ws)
+        ev[i][2].record()
+    torch.cuda.synchronize()
+    fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    bwd = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    fb = 2.0 * N * din + 2.0 * N * d + 8.0 * N * k + 2.0 * (din + d) * k
+    bb = 2.0 * N * d + 4.0 * N * din + 12.0 * N * k + 2.0 * (din + d) * k + 4.0 * din * k
+    out = {"workload": f"one projection layer: H [{N}, {din}], Zp [{din}, {k}], U [{d}, {k}], bf16",
+           "forward_ms": round(fwd, 5),
+           "forward_frac_hbm_peak": round(fb / (fwd * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "backward_ms": round(bwd, 5),
+           "backward_frac_hbm_peak": round(bb / (bwd * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "tokens_per_s_fwd_bwd": round(N / ((fwd + bwd) * 1e-3), 1)}
+    del H, G, Zp, U, T, Y, GT, GH, GZ, ws
     torch.cuda.empty_cache()
     return out
 
@@ -409,6 +458,13 @@ def main():
         for wc in (I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B):
             shapes[wc.name] = time_weights(wc, args.steps, dev)
         result["paper_shapes"] = shapes
+
+    # ---------------- reparameterized-SSN projections (section 4.1, Eq. (3)) ----------------
+    if not args.no_reparam:
+        result["reparam"] = {
+            "paper8b_mlp_out": time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2), dev),
+            "stage8b_mlp_out": time_reparam(32768, 14336, 4096, 64, max(10, args.steps // 2), dev),
+        }
 
     # ---------------- CPU baseline: the oracle on a bounded sample ----------------
     if not args.no_cpu_baseline:

@@ -187,6 +187,64 @@ ssn_status_t ssn_project_weights_batched(ssn_dtype_t dtype, int64_t count, int64
                                          const int64_t *n, int64_t k, void *const *W,
                                          const void *U, void *stream);
 
+/*
+ * Reparameterized SSN (section 4.1, Eq. (3)).  An output projection
+ * W [din, d] (Eq. (1)'s row-vector convention: a layer adds H W to the
+ * residual stream) is trained as its factor Zp [din, k] with W = Zp U^T, so
+ * every row of W lies in span(U) by construction and W is never formed.
+ *   H  [N, din] dtype   layer input (attention concat or MLP hidden)
+ *   Zp [din, k] dtype   trainable factor
+ *   U  [d, k]   dtype   the shared basis
+ * Shape rules: 1 <= k <= d, k <= din; N == 0 is a no-op (backward: GZp = 0).
+ * All intermediate products accumulate in fp32; bf16 outputs are rounded once.
+ */
+
+/*
+ * ssn_reparam_forward -- the layer's contribution Y = (H Zp) U^T.
+ *   T [N, k] float32   output: the projected input H Zp (the backward needs
+ *                      only G, H and Zp, but T is what crosses to U^T)
+ *   Y [N, d] dtype     output
+ * Two launches on `stream` (the projection of H by Zp, then the expansion
+ * by U^T).  Outputs must not overlap inputs or each other.
+ */
+ssn_status_t ssn_reparam_forward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,
+                                 const void *H, const void *Zp, const void *U, float *T, void *Y,
+                                 void *stream);
+
+/*
+ * Bytes of device workspace ssn_reparam_backward needs for these sizes
+ * (partial factor gradients of the token splits; 0 when none is needed).
+ * Depends on (dtype, N, din, k) only.
+ */
+size_t ssn_reparam_workspace_bytes(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t k);
+
+/*
+ * ssn_reparam_backward -- gradients of the layer for G = dL/dY [N, d]:
+ *   GT  [N, k]   float32  output: G U
+ *   GH  [N, din] dtype    output: dL/dH = (G U) Zp^T
+ *   GZp [din, k] float32  output: dL/dZp = (dL/dW) U = H^T (G U)
+ * `workspace` (device, 4-byte aligned, caller-owned) holds at least
+ * ssn_reparam_workspace_bytes(dtype, N, din, k) bytes, else SSN_ERR_SHAPE.
+ * The factor gradient is summed over token splits in a fixed order
+ * (deterministic).  Three or four launches on `stream`.
+ */
+ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,
+                                  const void *H, const void *Zp, const void *U, const void *G,
+                                  float *GT, void *GH, float *GZp, void *workspace,
+                                  size_t workspace_bytes, void *stream);
+
+/*
+ * ssn_factored_embedding -- the trainable embedding factored through the
+ * basis, T_S = E U^T (section 4.1), looked up by token id:
+ *   X0[i, :] = E[ids[i], :] . U^T
+ *   ids [N] int32, E [V, k] float32, U [d, k] dtype, X0 [N, d] dtype output.
+ * Same kernel as ssn_decompress (expansion form) with the coordinate rows
+ * gathered by id.
+ */
+ssn_status_t ssn_factored_embedding(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
+                                    const int32_t *ids, const float *E, const void *U, void *X0,
+                                    void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libssn.so")
-SOURCES = ["ssn_api.hip", "codec_kernels.hip", "weights_kernels.hip"]
+SOURCES = ["ssn_api.hip", "codec_kernels.hip", "weights_kernels.hip", "reparam_kernels.hip"]
 ARCH = "gfx950"
 
 

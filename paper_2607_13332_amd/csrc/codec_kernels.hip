@@ -561,14 +561,18 @@ constexpr int kDecompressDC = 64;
 // chunk of U (DC whole rows, one contiguous span of DC*k bf16 that starts
 // 16-byte aligned) is read with 16-byte loads and scattered element by
 // element into the zero-padded fragment layout.
+// GZ: the coordinate row of token t is Z[ids[t]] (a gathered table of
+// coordinates, e.g. the factored embedding E U^T of section 4.1) instead of
+// Z[t]; used without the additive embedding.
 template <int KS2, bool HAS_E, int KM, int DC = kDecompressDC, int PF = 1, int DSPLIT = 1,
-          int TW = 4, bool NTS = false>
+          int TW = 4, bool NTS = false, bool GZ = false>
 __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     uint16_t* __restrict__ Y, int64_t N, int d, int k, int64_t V) {
   static_assert(DC == 64 || DC == 128, "chunk of 64 or 128 d");
   static_assert(KM >= 0 && KM <= 2, "k layout mode");
+  static_assert(!(HAS_E && GZ), "gathered coordinates carry no additive embedding");
   constexpr bool KFULL32 = (KM == 0);
   constexpr int NT = DC / 16;                     // MFMA tiles per chunk
   constexpr int FR = NT * KS2 * kWave;            // A fragments per chunk
@@ -589,7 +593,7 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
   {
     int64_t t = tok0 + n16;
     t = t < N ? t : N - 1;
-    const float* zp = Zc + t * k;
+    const float* zp = Zc + (GZ ? clamp_id(ids[t], V) : t) * k;
 #pragma unroll
     for (int s = 0; s < KS2; ++s) {
       const int c0 = 32 * s + 8 * g;
@@ -805,14 +809,14 @@ __global__ __launch_bounds__(256) void compress_generic(
   }
 }
 
-template <typename T, bool HAS_E>
+template <typename T, bool HAS_E, bool GZ = false>
 __global__ __launch_bounds__(256) void decompress_generic(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids, const T* __restrict__ E,
     const T* __restrict__ U, T* __restrict__ Y, int64_t N, int64_t d, int64_t k, int64_t V) {
   const int lane = threadIdx.x & 63;
   const int64_t nw = (int64_t)gridDim.x * 4;
   for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < N; t += nw) {
-    const float* zr = Zc + t * k;
+    const float* zr = Zc + (GZ ? clamp_id(ids[t], V) : t) * k;
     const T* er = HAS_E ? E + clamp_id(ids[t], V) * d : nullptr;
     for (int64_t j = lane; j < d; j += 64) {
       float acc = HAS_E ? load_as_f32(er + j) : 0.f;
@@ -996,7 +1000,7 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
 // 8 token tiles (128 tokens) x 2 halves of d per block (16 waves); the
 // activation rows are written with non-temporal stores (streamed out instead
 // of parked dirty in the caches, where they slowed the next kernel's reads)
-template <int KS2, bool HAS_E, int KM>
+template <int KS2, bool HAS_E, int KM, bool GZ>
 static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
                                        hipStream_t st) {
@@ -1011,58 +1015,59 @@ static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const
     ++gy;
     while (pairs % gy != 0) ++gy;
   }
-  hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, DS, TW, true>),
+  hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, DS, TW, true, GZ>),
                      dim3((unsigned)blocks, (unsigned)gy), dim3(64 * TW * DS), 0, st, Zc, ids,
                      (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
   return hipGetLastError();
 }
 
-template <int KS2, bool HAS_E>
+template <int KS2, bool HAS_E, bool GZ>
 static hipError_t launch_decompress_ks(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
                                        hipStream_t st) {
-  if (k == 32 * KS2) return launch_decompress_km<KS2, HAS_E, 0>(N, d, k, V, Zc, ids, E, U, Y, st);
-  if (k % 8 == 0) return launch_decompress_km<KS2, HAS_E, 1>(N, d, k, V, Zc, ids, E, U, Y, st);
-  return launch_decompress_km<KS2, HAS_E, 2>(N, d, k, V, Zc, ids, E, U, Y, st);
+  if (k == 32 * KS2) return launch_decompress_km<KS2, HAS_E, 0, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
+  if (k % 8 == 0) return launch_decompress_km<KS2, HAS_E, 1, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
+  return launch_decompress_km<KS2, HAS_E, 2, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
 }
 
-template <bool HAS_E>
+template <bool HAS_E, bool GZ>
 static hipError_t launch_decompress_mfma(int64_t N, int d, int k, int64_t V, const float* Zc,
                                          const int32_t* ids, const void* E, const void* U, void* Y,
                                          hipStream_t st) {
   switch ((k + 31) / 32) {
-    case 1: return launch_decompress_ks<1, HAS_E>(N, d, k, V, Zc, ids, E, U, Y, st);
-    case 2: return launch_decompress_ks<2, HAS_E>(N, d, k, V, Zc, ids, E, U, Y, st);
-    case 3: return launch_decompress_ks<3, HAS_E>(N, d, k, V, Zc, ids, E, U, Y, st);
-    default: return launch_decompress_ks<4, HAS_E>(N, d, k, V, Zc, ids, E, U, Y, st);
+    case 1: return launch_decompress_ks<1, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
+    case 2: return launch_decompress_ks<2, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
+    case 3: return launch_decompress_ks<3, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
+    default: return launch_decompress_ks<4, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
   }
+}
+
+template <typename T, bool HAS_E, bool GZ>
+static hipError_t launch_decompress_generic(int64_t N, int64_t d, int64_t k, int64_t V,
+                                            const float* Zc, const int32_t* ids, const void* E,
+                                            const void* U, void* Y, hipStream_t st) {
+  hipLaunchKernelGGL((decompress_generic<T, HAS_E, GZ>), dim3(generic_blocks(N)), dim3(256), 0, st, Zc,
+                     ids, (const T*)E, (const T*)U, (T*)Y, N, d, k, V);
+  return hipGetLastError();
 }
 
 hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const float* Zc,
                              const int32_t* ids, const void* E, const void* U, void* Y,
-                             hipStream_t st) {
+                             bool gather_z, hipStream_t st) {
   const bool has_e = (E != nullptr);
   if (decompress_uses_mfma(dtype, d, k) && al16(Zc) && al16(U) && al16(Y) && (!has_e || al16(E))) {
-    return has_e ? launch_decompress_mfma<true>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st)
-                 : launch_decompress_mfma<false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st);
+    if (has_e) return launch_decompress_mfma<true, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st);
+    if (gather_z) return launch_decompress_mfma<false, true>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st);
+    return launch_decompress_mfma<false, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st);
   }
-  const unsigned nb = generic_blocks(N);
   if (dtype == kF32) {
-    if (has_e)
-      hipLaunchKernelGGL((decompress_generic<float, true>), dim3(nb), dim3(256), 0, st, Zc, ids,
-                         (const float*)E, (const float*)U, (float*)Y, N, d, k, V);
-    else
-      hipLaunchKernelGGL((decompress_generic<float, false>), dim3(nb), dim3(256), 0, st, Zc, ids,
-                         (const float*)E, (const float*)U, (float*)Y, N, d, k, V);
-  } else {
-    if (has_e)
-      hipLaunchKernelGGL((decompress_generic<uint16_t, true>), dim3(nb), dim3(256), 0, st, Zc, ids,
-                         (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
-    else
-      hipLaunchKernelGGL((decompress_generic<uint16_t, false>), dim3(nb), dim3(256), 0, st, Zc, ids,
-                         (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
+    if (has_e) return launch_decompress_generic<float, true, false>(N, d, k, V, Zc, ids, E, U, Y, st);
+    if (gather_z) return launch_decompress_generic<float, false, true>(N, d, k, V, Zc, ids, E, U, Y, st);
+    return launch_decompress_generic<float, false, false>(N, d, k, V, Zc, ids, E, U, Y, st);
   }
-  return hipGetLastError();
+  if (has_e) return launch_decompress_generic<uint16_t, true, false>(N, d, k, V, Zc, ids, E, U, Y, st);
+  if (gather_z) return launch_decompress_generic<uint16_t, false, true>(N, d, k, V, Zc, ids, E, U, Y, st);
+  return launch_decompress_generic<uint16_t, false, false>(N, d, k, V, Zc, ids, E, U, Y, st);
 }
 
 }  // namespace ssn

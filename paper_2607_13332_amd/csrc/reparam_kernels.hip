@@ -1,0 +1,269 @@
+// Reparameterized-SSN factor gradient (section 4.1, Eq. (3)).
+//
+// An output projection W [din, d] is stored as its factor Zp [din, k] with
+// W = Zp U^T; the optimizer needs dL/dZp = (dL/dW) U = H^T (G U).  The
+// gradient projection GT = G U [N, k] is formed by the codec's projection
+// kernel; this file contracts it with the layer input H [N, din] over the
+// tokens:
+//     dZp[i, c] = sum_t H[t, i] GT[t, c]            (float32 result)
+#include "ssn_device.h"
+#include "ssn_launch.h"
+
+namespace ssn {
+
+constexpr int kFgRows = 64;      // tokens per chunk
+constexpr int kFgTiles = 8;      // 16-column tiles of din per block (128 columns)
+constexpr int kFgThreads = 256;  // 4 waves, two tiles each
+constexpr int kFgTargetBlocks = 512;
+
+// ===========================================================================
+// MFMA kernel, bf16 H.  Block (column block x, token split y) owns din
+// columns [128x, 128x + 128) and tokens [y*tps, (y+1)*tps).  Per chunk of 64
+// tokens the block loads H rows (16-byte pieces; thread t moves piece t mod
+// 16 of rows t/16 + 16i) into a row-major LDS tile, and GT rows split into
+// bf16 hi + lo parts into two row-major LDS tiles (zero past k).  Both MFMA
+// operands are token-contiguous fragments read with LDS transpose reads:
+// A = H^T (16 din x 32 tokens), B = GT (32 tokens x 16 of k), two MFMAs per
+// pair (hi, lo) so GT keeps ~fp32 accuracy.  Wave w owns tiles w and w + 4
+// for all of k.  The block writes its partial sums for its token split; a
+// second kernel adds the splits in order (deterministic).
+// ===========================================================================
+template <int KT, bool K4>
+__global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* __restrict__ H,
+                                                               const float* __restrict__ GT,
+                                                               float* __restrict__ out, int64_t N,
+                                                               int din, int k, int64_t tps) {
+  constexpr int R = kFgRows, NT = kFgThreads, NW = NT / kWave;
+  constexpr int HP = 2 * kFgTiles, WP = HP + 1;      // H pieces per row, pitch in pieces
+  constexpr int KS2 = (KT + 1) / 2, KW = 32 * KS2;   // GT tile width (bf16)
+  constexpr int GPI = KW + 8;                          // GT tile pitch (bf16)
+  constexpr int NHP = R * HP / NT;                     // H pieces per thread per chunk (4)
+  constexpr int NGQ = K4 ? (R * KW / 4 + NT - 1) / NT : (R * KW + NT - 1) / NT;
+  __shared__ u32x4 ht[2][R * WP];
+  __shared__ __align__(16) uint16_t gtl[2][2][R * GPI];   // [buffer][hi / lo][row * GPI + col]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int L = lane & 15, g = lane >> 4;
+  const int col0 = (int)blockIdx.x * 16 * kFgTiles;
+  const int tcount = min(kFgTiles, din / 16 - (int)blockIdx.x * kFgTiles);
+  const int64_t t_begin = (int64_t)blockIdx.y * tps;
+  const int64_t t_end = min(N, t_begin + tps);
+  const int nch = (int)((t_end - t_begin + R - 1) / R);
+
+  // GT padding columns k .. KW are never written below
+  for (int i = tid; i < 2 * 2 * R * GPI / 8; i += NT) ((u32x4*)&gtl[0][0][0])[i] = u32x4{0u, 0u, 0u, 0u};
+
+  const int h = tid % HP, row0 = tid / HP;
+  const bool hok = h < 2 * tcount;
+  const uint16_t* hsrc = H + (t_begin + row0) * din + col0 + 8 * h;
+
+  u32x4 hv[NHP];
+  float gv[NGQ][K4 ? 4 : 1];
+  auto load = [&](int c) __attribute__((always_inline)) {
+    const int64_t r0 = (int64_t)c * R;
+#pragma unroll
+    for (int i = 0; i < NHP; ++i) {
+      const int64_t t = t_begin + r0 + row0 + 16 * i;
+      hv[i] = (hok && t < t_end) ? *(const u32x4*)(hsrc + (r0 + 16 * i) * din) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < NGQ; ++j) {
+      const int q = tid + NT * j;
+      if constexpr (K4) {
+        const int row = q / (k / 4), c4 = q - (q / (k / 4)) * (k / 4);
+        const int64_t t = t_begin + r0 + row;
+        const bool ok = q < R * (k / 4) && t < t_end;
+        const f32x4 v = ok ? *(const f32x4*)(GT + t * k + 4 * c4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        gv[j][0] = v[0]; gv[j][1] = v[1]; gv[j][2] = v[2]; gv[j][3] = v[3];
+      } else {
+        const int row = q / k;
+        const int64_t t = t_begin + r0 + row;
+        gv[j][0] = (q < R * k && t < t_end) ? GT[t * k + (q - row * k)] : 0.f;
+      }
+    }
+  };
+  auto park = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NHP; ++i) ht[buf][(row0 + 16 * i) * WP + h] = hv[i];
+#pragma unroll
+    for (int j = 0; j < NGQ; ++j) {
+      const int q = tid + NT * j;
+      if constexpr (K4) {
+        if (q < R * (k / 4)) {
+          const int row = q / (k / 4), c4 = q - (q / (k / 4)) * (k / 4);
+          uint32_t hi[2], lo[2];
+#pragma unroll
+          for (int m = 0; m < 2; ++m) {
+            const uint32_t h0 = f32_to_bf16(gv[j][2 * m]), h1 = f32_to_bf16(gv[j][2 * m + 1]);
+            hi[m] = h0 | (h1 << 16);
+            lo[m] = pack_bf16x2(gv[j][2 * m] - bf16_to_f32(h0), gv[j][2 * m + 1] - bf16_to_f32(h1));
+          }
+          *(u32x2*)&gtl[buf][0][row * GPI + 4 * c4] = u32x2{hi[0], hi[1]};
+          *(u32x2*)&gtl[buf][1][row * GPI + 4 * c4] = u32x2{lo[0], lo[1]};
+        }
+      } else if (q < R * k) {
+        const int row = q / k, col = q - row * k;
+        const uint32_t h0 = f32_to_bf16(gv[j][0]);
+        gtl[buf][0][row * GPI + col] = (uint16_t)h0;
+        gtl[buf][1][row * GPI + col] = (uint16_t)f32_to_bf16(gv[j][0] - bf16_to_f32(h0));
+      }
+    }
+  };
+
+  f32x4 acc[2][KT];
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+    for (int i = 0; i < KT; ++i) acc[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  __syncthreads();   // padding zeroed before the first park
+  if (nch > 0) {
+    load(0);
+    park(0);
+    if (nch > 1) load(1);
+  }
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    const uint16_t* hb = (const uint16_t*)ht[c & 1];
+#pragma unroll
+    for (int ks = 0; ks < R / 32; ++ks) {
+      const int r = 32 * ks + 8 * g + (L >> 2);
+      u32x4 bhi[KT], blo[KT];
+#pragma unroll
+      for (int i = 0; i < KT; ++i) {
+        const uint16_t* ph = &gtl[c & 1][0][r * GPI + 16 * i + 4 * (L & 3)];
+        const uint16_t* pl = &gtl[c & 1][1][r * GPI + 16 * i + 4 * (L & 3)];
+        const u32x2 a = lds_read_tr16(ph), b = lds_read_tr16(ph + 4 * GPI);
+        const u32x2 x = lds_read_tr16(pl), y = lds_read_tr16(pl + 4 * GPI);
+        bhi[i] = u32x4{a[0], a[1], b[0], b[1]};
+        blo[i] = u32x4{x[0], x[1], y[0], y[1]};
+      }
+#pragma unroll
+      for (int ct = 0; ct < 2; ++ct) {
+        const int jl = wave + NW * ct;
+        if (jl < tcount) {
+          const uint16_t* p = hb + r * (8 * WP) + 16 * jl + 4 * (L & 3);
+          const u32x2 a = lds_read_tr16(p), b = lds_read_tr16(p + 4 * 8 * WP);
+          const u32x4 af = u32x4{a[0], a[1], b[0], b[1]};
+#pragma unroll
+          for (int i = 0; i < KT; ++i) {
+            acc[ct][i] = mfma16x16x32(af, bhi[i], acc[ct][i]);
+            acc[ct][i] = mfma16x16x32(af, blo[i], acc[ct][i]);
+          }
+        }
+      }
+    }
+    if (c + 1 < nch) park((c + 1) & 1);
+    if (c + 2 < nch) load(c + 2);
+    __syncthreads();
+  }
+
+  // lane (L, g) of tile (jl, i) holds dZp[col0 + 16 jl + 4g + e][16 i + L]
+  float* dst = out + (int64_t)blockIdx.y * din * k;
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct) {
+    const int jl = wave + NW * ct;
+    if (jl < tcount) {
+#pragma unroll
+      for (int i = 0; i < KT; ++i) {
+        const int c = 16 * i + L;
+        if (c < k) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dst[(int64_t)(col0 + 16 * jl + 4 * g + e) * k + c] = acc[ct][i][e];
+        }
+      }
+    }
+  }
+}
+
+// Sum of the S partial results, in split order.
+__global__ __launch_bounds__(256) void factor_grad_reduce(const float* __restrict__ ws,
+                                                          float* __restrict__ out, int64_t n, int S) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    float s = ws[i];
+    for (int j = 1; j < S; ++j) s += ws[(int64_t)j * n + i];
+    out[i] = s;
+  }
+}
+
+// Generic kernel (fp32 H, or din not a multiple of 16): one thread per
+// output element, fp32 FMA over the tokens in order.
+template <typename T>
+__global__ __launch_bounds__(256) void factor_grad_generic(const T* __restrict__ H,
+                                                           const float* __restrict__ GT,
+                                                           float* __restrict__ out, int64_t N,
+                                                           int64_t din, int64_t k) {
+  for (int64_t o = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; o < din * k;
+       o += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = o / k, c = o % k;
+    float s = 0.f;
+    for (int64_t t = 0; t < N; ++t) s = fmaf(load_as_f32(H + t * din + i), GT[t * k + c], s);
+    out[o] = s;
+  }
+}
+
+static bool factor_grad_uses_mfma(int dtype, int64_t din, int64_t k) {
+  return dtype == kBF16 && din % 16 == 0 && din <= INT32_MAX / 2 && k >= 1 && k <= 128;
+}
+
+// Token splits: enough blocks for about two per compute unit, at least one
+// chunk of tokens per split.  Depends on (N, din) only, so results are the
+// same on every device.
+static int64_t factor_grad_splits(int64_t N, int64_t din) {
+  const int64_t cb = (din / 16 + kFgTiles - 1) / kFgTiles;
+  int64_t S = (kFgTargetBlocks + cb - 1) / cb;
+  const int64_t chunks = (N + kFgRows - 1) / kFgRows;
+  S = S > chunks ? chunks : S;
+  return S < 1 ? 1 : S;
+}
+
+size_t factor_grad_workspace_bytes(int dtype, int64_t N, int64_t din, int64_t k) {
+  if (!factor_grad_uses_mfma(dtype, din, k)) return 0;
+  const int64_t S = factor_grad_splits(N, din);
+  return S > 1 ? (size_t)S * (size_t)din * (size_t)k * sizeof(float) : 0;
+}
+
+template <int KT>
+static hipError_t launch_factor_grad_kt(int64_t N, int din, int k, const void* H, const float* GT,
+                                        float* dst, int64_t S, int64_t tps, hipStream_t st) {
+  const dim3 grid((unsigned)((din / 16 + kFgTiles - 1) / kFgTiles), (unsigned)S);
+  if (k % 4 == 0 && ((uintptr_t)GT & 15u) == 0)
+    hipLaunchKernelGGL((factor_grad_bf16<KT, true>), grid, dim3(kFgThreads), 0, st,
+                       (const uint16_t*)H, GT, dst, N, din, k, tps);
+  else
+    hipLaunchKernelGGL((factor_grad_bf16<KT, false>), grid, dim3(kFgThreads), 0, st,
+                       (const uint16_t*)H, GT, dst, N, din, k, tps);
+  return hipGetLastError();
+}
+
+hipError_t launch_factor_grad(int dtype, int64_t N, int64_t din, int64_t k, const void* H,
+                              const float* GT, float* dZp, float* ws, hipStream_t st) {
+  if (factor_grad_uses_mfma(dtype, din, k) && ((uintptr_t)H & 15u) == 0) {
+    const int64_t S = factor_grad_splits(N, din);
+    const int64_t chunks = (N + kFgRows - 1) / kFgRows;
+    const int64_t tps = ((chunks + S - 1) / S) * kFgRows;
+    float* dst = S > 1 ? ws : dZp;
+    hipError_t e;
+    const int kt = (int)((k + 15) / 16);
+    if (kt <= 2) e = launch_factor_grad_kt<2>(N, (int)din, (int)k, H, GT, dst, S, tps, st);
+    else if (kt <= 4) e = launch_factor_grad_kt<4>(N, (int)din, (int)k, H, GT, dst, S, tps, st);
+    else e = launch_factor_grad_kt<8>(N, (int)din, (int)k, H, GT, dst, S, tps, st);
+    if (e != hipSuccess || S == 1) return e;
+    const int64_t n = din * k;
+    const unsigned blocks = (unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+    hipLaunchKernelGGL(factor_grad_reduce, dim3(blocks), dim3(256), 0, st, ws, dZp, n, (int)S);
+    return hipGetLastError();
+  }
+  const int64_t n = din * k;
+  const unsigned blocks = (unsigned)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
+  if (dtype == kF32)
+    hipLaunchKernelGGL((factor_grad_generic<float>), dim3(blocks), dim3(256), 0, st,
+                       (const float*)H, GT, dZp, N, din, k);
+  else
+    hipLaunchKernelGGL((factor_grad_generic<uint16_t>), dim3(blocks), dim3(256), 0, st,
+                       (const uint16_t*)H, GT, dZp, N, din, k);
+  return hipGetLastError();
+}
+
+}  // namespace ssn

@@ -125,7 +125,7 @@ ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, 
       (has_e && (overlap(out, span(E, V * d * s)) || overlap(out, span(ids, N * 4)))))
     return SSN_ERR_ALIAS;
   return launch_status(ssn::launch_decompress(dtype, N, d, k, has_e ? V : 1, Z, ids, E, U, Xout,
-                                              (hipStream_t)stream));
+                                              false, (hipStream_t)stream));
 }
 
 ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, const void* G,
@@ -146,6 +146,100 @@ ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k
 ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t k, const void* E,
                                const void* U, float* P, void* stream) {
   return ssn_project_grad(dtype, V, d, k, E, U, P, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Reparameterized SSN (section 4.1, Eq. (3))
+// ---------------------------------------------------------------------------
+static ssn_status_t reparam_shape(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k) {
+  if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;
+  if (N < 0 || din < 1 || d < 1 || k < 1 || k > d || k > din) return SSN_ERR_SHAPE;
+  if (!mul_ok(N, din) || !mul_ok(N, d) || !mul_ok(N, k) || !mul_ok(din, k) || !mul_ok(d, k))
+    return SSN_ERR_SHAPE;
+  return SSN_OK;
+}
+
+ssn_status_t ssn_reparam_forward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,
+                                 const void* H, const void* Zp, const void* U, float* T, void* Y,
+                                 void* stream) {
+  const ssn_status_t sh = reparam_shape(dtype, N, din, d, k);
+  if (sh != SSN_OK || N == 0) return sh;
+  if (!H || !Zp || !U || !T || !Y) return SSN_ERR_NULL;
+  const int64_t s = elem_size(dtype);
+  if (!aligned_to(H, s) || !aligned_to(Zp, s) || !aligned_to(U, s) || !aligned_to(T, 4) ||
+      !aligned_to(Y, s))
+    return SSN_ERR_ALIGN;
+  const Span ts = span(T, N * k * 4), ys = span(Y, N * d * s);
+  const Span ins[3] = {span(H, N * din * s), span(Zp, din * k * s), span(U, d * k * s)};
+  for (const Span& in : ins)
+    if (overlap(ts, in) || overlap(ys, in)) return SSN_ERR_ALIAS;
+  if (overlap(ts, ys)) return SSN_ERR_ALIAS;
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = ssn::launch_compress(dtype, N, din, k, 1, H, nullptr, nullptr, Zp, T, nullptr, st);
+  if (e != hipSuccess) return SSN_ERR_LAUNCH;
+  return launch_status(ssn::launch_decompress(dtype, N, d, k, 1, T, nullptr, nullptr, U, Y, false, st));
+}
+
+size_t ssn_reparam_workspace_bytes(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t k) {
+  if (!valid_dtype(dtype) || N < 0 || din < 1 || k < 1 || !mul_ok(din, k)) return 0;
+  return ssn::factor_grad_workspace_bytes(dtype, N, din, k);
+}
+
+ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,
+                                  const void* H, const void* Zp, const void* U, const void* G,
+                                  float* GT, void* GH, float* GZp, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  const ssn_status_t sh = reparam_shape(dtype, N, din, d, k);
+  if (sh != SSN_OK) return sh;
+  if (!GZp) return SSN_ERR_NULL;
+  const int64_t s = elem_size(dtype);
+  if (!aligned_to(GZp, 4)) return SSN_ERR_ALIGN;
+  const size_t need = ssn::factor_grad_workspace_bytes(dtype, N, din, k);
+  if (N > 0) {
+    if (!H || !Zp || !U || !G || !GT || !GH) return SSN_ERR_NULL;
+    if (!aligned_to(H, s) || !aligned_to(Zp, s) || !aligned_to(U, s) || !aligned_to(G, s) ||
+        !aligned_to(GT, 4) || !aligned_to(GH, s))
+      return SSN_ERR_ALIGN;
+    if (workspace_bytes < need || (need > 0 && !workspace)) return SSN_ERR_SHAPE;
+    if (need > 0 && !aligned_to(workspace, 4)) return SSN_ERR_ALIGN;
+    const Span outs[4] = {span(GT, N * k * 4), span(GH, N * din * s), span(GZp, din * k * 4),
+                          span(workspace, (int64_t)need)};
+    const Span ins[4] = {span(H, N * din * s), span(Zp, din * k * s), span(U, d * k * s),
+                         span(G, N * d * s)};
+    for (int a = 0; a < 4; ++a) {
+      for (const Span& in : ins)
+        if (overlap(outs[a], in)) return SSN_ERR_ALIAS;
+      for (int b = 0; b < a; ++b)
+        if (overlap(outs[a], outs[b])) return SSN_ERR_ALIAS;
+    }
+  }
+  hipStream_t st = (hipStream_t)stream;
+  if (N == 0)   // no tokens: the factor-gradient kernel writes zeros (no memset, capture-safe)
+    return launch_status(ssn::launch_factor_grad(dtype, 0, din, k, H, GT, GZp, (float*)workspace, st));
+  hipError_t e = ssn::launch_compress(dtype, N, d, k, 1, G, nullptr, nullptr, U, GT, nullptr, st);
+  if (e != hipSuccess) return SSN_ERR_LAUNCH;
+  e = ssn::launch_decompress(dtype, N, din, k, 1, GT, nullptr, nullptr, Zp, GH, false, st);
+  if (e != hipSuccess) return SSN_ERR_LAUNCH;
+  return launch_status(ssn::launch_factor_grad(dtype, N, din, k, H, GT, GZp, (float*)workspace, st));
+}
+
+ssn_status_t ssn_factored_embedding(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
+                                    const int32_t* ids, const float* E, const void* U, void* X0,
+                                    void* stream) {
+  if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;
+  if (N < 0 || d < 1 || k < 1 || k > d || V < 1) return SSN_ERR_SHAPE;
+  if (!mul_ok(N, d) || !mul_ok(V, k) || !mul_ok(d, k)) return SSN_ERR_SHAPE;
+  if (N == 0) return SSN_OK;
+  if (!ids || !E || !U || !X0) return SSN_ERR_NULL;
+  const int64_t s = elem_size(dtype);
+  if (!aligned_to(ids, 4) || !aligned_to(E, 4) || !aligned_to(U, s) || !aligned_to(X0, s))
+    return SSN_ERR_ALIGN;
+  const Span out = span(X0, N * d * s);
+  if (overlap(out, span(ids, N * 4)) || overlap(out, span(E, V * k * 4)) ||
+      overlap(out, span(U, d * k * s)))
+    return SSN_ERR_ALIAS;
+  return launch_status(ssn::launch_decompress(dtype, N, d, k, V, E, ids, nullptr, U, X0, true,
+                                              (hipStream_t)stream));
 }
 
 ssn_status_t ssn_project_weights_batched(ssn_dtype_t dtype, int64_t count, int64_t d,

@@ -22,9 +22,15 @@ bool weights_use_mfma(int dtype, int64_t d, int64_t k);
 hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                            const int32_t* ids, const void* E, const void* U, float* Z,
                            const float* P, hipStream_t st);
+// E non-NULL: Y = E[ids] + Z U^T; gather_z: Y = Z[ids] U^T; else Y = Z U^T.
 hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const float* Z,
                              const int32_t* ids, const void* E, const void* U, void* Y,
-                             hipStream_t st);
+                             bool gather_z, hipStream_t st);
+// dZp[din, k] = H[N, din]^T . GT[N, k] (float32 GT and dZp); `ws` holds the
+// partial sums of the token splits (factor_grad_workspace_bytes).
+size_t factor_grad_workspace_bytes(int dtype, int64_t N, int64_t din, int64_t k);
+hipError_t launch_factor_grad(int dtype, int64_t N, int64_t din, int64_t k, const void* H,
+                              const float* GT, float* dZp, float* ws, hipStream_t st);
 // count matrices W[b] [d, n[b]] sharing U [d, k], re-projected in place.
 hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t* n, int64_t k,
                                   void* const* W, const void* U, hipStream_t st);

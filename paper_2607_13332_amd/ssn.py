@@ -51,6 +51,18 @@ def _declare(lib):
     lib.ssn_compress_projected.restype = ctypes.c_int
     lib.ssn_compress_projected.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
                                            _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_reparam_forward.restype = ctypes.c_int
+    lib.ssn_reparam_forward.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
+                                        _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_reparam_workspace_bytes.restype = ctypes.c_size_t
+    lib.ssn_reparam_workspace_bytes.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64]
+    lib.ssn_reparam_backward.restype = ctypes.c_int
+    lib.ssn_reparam_backward.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
+                                         _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
+                                         ctypes.c_size_t, _c_p]
+    lib.ssn_factored_embedding.restype = ctypes.c_int
+    lib.ssn_factored_embedding.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
+                                           _c_p, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_project_weights.restype = ctypes.c_int
     lib.ssn_project_weights.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]
     lib.ssn_project_weights_batched.restype = ctypes.c_int
@@ -220,6 +232,77 @@ def compress_projected(X: torch.Tensor, ids: torch.Tensor, P: torch.Tensor, U: t
         _dt_code(t), N, d, k, V, _dev(X, "X", t, 2), _dev(ids, "ids", torch.int32, 1),
         _dev(P, "P", torch.float32, 2), _dev(U, "U", t, 2), _dev(out, "out", torch.float32, 2),
         _stream(stream)))
+    return out
+
+
+def reparam_forward(H: torch.Tensor, Zp: torch.Tensor, U: torch.Tensor, T=None, Y=None,
+                    stream=None):
+    """Reparameterized projection: T = H Zp (float32 [N, k]), Y = T U^T
+    (storage dtype [N, d]).  Returns (T, Y)."""
+    N, din = H.shape
+    d, k = U.shape
+    if Zp.shape != (din, k):
+        raise ValueError(f"shape mismatch H{tuple(H.shape)} Zp{tuple(Zp.shape)} U{tuple(U.shape)}")
+    t = H.dtype
+    if T is None:
+        T = torch.empty((N, k), dtype=torch.float32, device=H.device)
+    if Y is None:
+        Y = torch.empty((N, d), dtype=t, device=H.device)
+    _same_device(H, Zp, U, T, Y)
+    _check("ssn_reparam_forward", lib().ssn_reparam_forward(
+        _dt_code(t), N, din, d, k, _dev(H, "H", t, 2), _dev(Zp, "Zp", t, 2), _dev(U, "U", t, 2),
+        _dev(T, "T", torch.float32, 2), _dev(Y, "Y", t, 2), _stream(stream)))
+    return T, Y
+
+
+def reparam_workspace_bytes(dtype, N: int, din: int, k: int) -> int:
+    return int(lib().ssn_reparam_workspace_bytes(_dt_code(dtype), N, din, k))
+
+
+def reparam_backward(H: torch.Tensor, Zp: torch.Tensor, U: torch.Tensor, G: torch.Tensor,
+                     GT=None, GH=None, GZp=None, workspace=None, stream=None):
+    """Gradients for G = dL/dY: GT = G U, GH = (G U) Zp^T, GZp = H^T (G U).
+    Returns (GT, GH, GZp)."""
+    N, din = H.shape
+    d, k = U.shape
+    if Zp.shape != (din, k) or G.shape != (N, d):
+        raise ValueError(f"shape mismatch H{tuple(H.shape)} Zp{tuple(Zp.shape)} U{tuple(U.shape)} "
+                         f"G{tuple(G.shape)}")
+    t = H.dtype
+    dev = H.device
+    if GT is None:
+        GT = torch.empty((N, k), dtype=torch.float32, device=dev)
+    if GH is None:
+        GH = torch.empty((N, din), dtype=t, device=dev)
+    if GZp is None:
+        GZp = torch.empty((din, k), dtype=torch.float32, device=dev)
+    need = reparam_workspace_bytes(t, N, din, k)
+    if workspace is None:
+        workspace = torch.empty((max(need, 4) + 3) // 4, dtype=torch.float32, device=dev)
+    _same_device(H, Zp, U, G, GT, GH, GZp, workspace)
+    _check("ssn_reparam_backward", lib().ssn_reparam_backward(
+        _dt_code(t), N, din, d, k, _dev(H, "H", t, 2), _dev(Zp, "Zp", t, 2), _dev(U, "U", t, 2),
+        _dev(G, "G", t, 2), _dev(GT, "GT", torch.float32, 2), _dev(GH, "GH", t, 2),
+        _dev(GZp, "GZp", torch.float32, 2), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+    return GT, GH, GZp
+
+
+def factored_embedding(ids: torch.Tensor, E: torch.Tensor, U: torch.Tensor,
+                       out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """X0 = E[ids] U^T for the factored embedding E [V, k] (float32)."""
+    (N,) = ids.shape
+    V, k = E.shape
+    d = U.shape[0]
+    if U.shape[1] != k:
+        raise ValueError(f"shape mismatch E{tuple(E.shape)} U{tuple(U.shape)}")
+    t = U.dtype
+    if out is None:
+        out = torch.empty((N, d), dtype=t, device=U.device)
+    _same_device(ids, E, U, out)
+    _check("ssn_factored_embedding", lib().ssn_factored_embedding(
+        _dt_code(t), N, d, k, V, _dev(ids, "ids", torch.int32, 1), _dev(E, "E", torch.float32, 2),
+        _dev(U, "U", t, 2), _dev(out, "out", t, 2), _stream(stream)))
     return out
 
 

@@ -143,6 +143,35 @@ def test_projected_table_validation(ssn):
     assert f(1, 10, 64, 8, 100, A, B, C, D, A + 64, None) == ERR_ALIAS   # Z on X
 
 
+def test_reparam_validation(ssn):
+    L = ssn.lib()
+    f = L.ssn_reparam_forward
+    assert f(1, 0, 256, 128, 16, None, None, None, None, None, None) == OK
+    assert f(1, 10, 256, 128, 200, A, B, C, D, F, None) == ERR_SHAPE        # k > d
+    assert f(1, 10, 8, 128, 16, A, B, C, D, F, None) == ERR_SHAPE          # k > din
+    assert f(1, 10, 256, 128, 16, A, None, C, D, F, None) == ERR_NULL
+    assert f(1, 10, 256, 128, 16, A, B, C, D + 2, F, None) == ERR_ALIGN    # T is float32
+    assert f(1, 10, 256, 128, 16, A, B, C, A + 64, F, None) == ERR_ALIAS   # T on H
+    assert f(1, 10, 256, 128, 16, A, B, C, D, D + 64, None) == ERR_ALIAS   # Y on T
+    w = L.ssn_reparam_workspace_bytes
+    assert w(1, 32768, 14336, 64) == w(1, 32768, 14336, 64) > 0
+    assert w(0, 32768, 14336, 64) == 0                                    # generic path: none
+    b = L.ssn_reparam_backward
+    E6 = 0x7F5000000000
+    need = w(1, 1000, 256, 16)                  # 16 token splits of 64 tokens
+    assert need == 16 * 256 * 16 * 4
+    assert b(1, 1000, 256, 128, 16, A, B, C, D, F, E6, 0x7F6000000000, 0x7F7000000000,
+             need - 4, None) == ERR_SHAPE                                  # workspace too small
+    assert b(1, 10, 256, 128, 16, A, B, C, D, F, E6, None, None, 0, None) == ERR_NULL
+    assert b(1, 10, 256, 128, 16, A, B, C, D, F, F + 8, 0x7F7000000000, None, 0, None) == ERR_ALIAS
+    e = L.ssn_factored_embedding
+    assert e(1, 0, 128, 16, 100, None, None, None, None, None) == OK
+    assert e(1, 10, 128, 16, 0, A, B, C, D, None) == ERR_SHAPE
+    assert e(1, 10, 128, 16, 100, A, None, C, D, None) == ERR_NULL
+    assert e(1, 10, 128, 16, 100, A, B + 2, C, D, None) == ERR_ALIGN      # E is float32
+    assert e(1, 10, 128, 16, 100, A, B, C, B + 64, None) == ERR_ALIAS
+
+
 def test_project_weights_validation(ssn):
     L = ssn.lib()
     f = L.ssn_project_weights

@@ -313,6 +313,76 @@ def test_weight_batches(d, k, ns):
         assert torch.equal(W, singles[b])
 
 
+# ---------------------------------------------------------------- reparameterized SSN
+REPARAM_SHAPES = [  # (N, din, d, k, dtype): every kernel family and tail
+    (64, 256, 128, 16, "f32"), (300, 512, 256, 40, "bf16"), (1000, 2048, 1024, 51, "bf16"),
+    (777, 1024, 512, 64, "bf16"), (130, 4096, 2048, 128, "bf16"), (33, 100, 96, 10, "bf16"),
+    (5000, 384, 256, 8, "bf16"),
+]
+
+
+@pytest.mark.parametrize("N,din,d,k,dtype", REPARAM_SHAPES)
+def test_reparam_shapes(N, din, d, k, dtype):
+    seed = N + 3 * din + 5 * d + k
+    print(f"[case] reparam N={N} din={din} d={d} k={k} {dtype}", flush=True)
+    r = np.random.default_rng(seed)
+    Hh = I.store(r.standard_normal((N, din)), dtype)
+    Zh = I.store(0.05 * r.standard_normal((din, k)), dtype)
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), dtype)
+    Gh = I.store(r.standard_normal((N, d)), dtype)
+    H, Zp, U, G = dev(Hh, dtype), dev(Zh, dtype), dev(Uh, dtype), dev(Gh, dtype)
+    outk = "bf16out" if dtype == "bf16" else "f32out_dec"
+    T, Y = ssn.reparam_forward(H, Zp, U)
+    check("T = H Zp", host(T), O.project_grad(Hh, Zh), dtype, "f32out")
+    check("Y = (H Zp) U^T", host(Y), O.reparam_forward(Hh, Zh, Uh), dtype, outk)
+    GT, GH, GZ = ssn.reparam_backward(H, Zp, U, G)
+    check("GT = G U", host(GT), O.project_grad(Gh, Uh), dtype, "f32out")
+    check("dL/dH", host(GH), O.reparam_grad_input(Gh, Zh, Uh), dtype, outk)
+    check("dL/dZp", host(GZ), O.reparam_grad_factor(Hh, Gh, Uh), dtype, "f32out")
+    # the split reduction is deterministic
+    _, _, GZ2 = ssn.reparam_backward(H, Zp, U, G)
+    assert torch.equal(GZ, GZ2)
+
+
+def test_reparam_paper_shape_sampled():
+    """Pluralis-8B MLP output projection: din = 18432, d = 5120, k = 51,
+    one 4096-token sequence; checked on sampled rows / factor rows."""
+    N, din, d, k = 4096, 18432, 5120, 51
+    print(f"[case] reparam paper shape N={N} din={din} d={d} k={k}", flush=True)
+    g = torch.Generator(device=DEV).manual_seed(2024)
+    H = torch.randn((N, din), generator=g, device=DEV).to(torch.bfloat16)
+    G = torch.randn((N, d), generator=g, device=DEV).to(torch.bfloat16)
+    Zp = (0.02 * torch.randn((din, k), generator=g, device=DEV)).to(torch.bfloat16)
+    U = dev(I.store(I.gaussian_orthonormal_basis(d, k, 2024), "bf16"), "bf16")
+    T, Y = ssn.reparam_forward(H, Zp, U)
+    GT, GH, GZ = ssn.reparam_backward(H, Zp, U, G)
+    torch.cuda.synchronize()
+    rows = torch.from_numpy(sample_rows(N, 128, 1)).to(DEV)
+    cols = torch.from_numpy(sample_rows(din, 128, 2)).to(DEV)
+    Hs, Gs, Zh, Uh = host(H[rows]), host(G[rows]), host(Zp), host(U)
+    check("paper Y", host(Y[rows]), O.reparam_forward(Hs, Zh, Uh), "bf16", "bf16out")
+    check("paper dL/dH", host(GH[rows]), O.reparam_grad_input(Gs, Zh, Uh), "bf16", "bf16out")
+    # factor gradient rows need every token: the oracle takes H's sampled columns
+    check("paper dL/dZp", host(GZ[cols]), O.reparam_grad_factor(host(H[:, cols].contiguous()), host(G), Uh),
+          "bf16", "f32out")
+    del H, G, T, Y, GT, GH, GZ
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("N,d,k,V,dtype", [(300, 256, 16, 50, "bf16"), (4096, 5120, 51, 128256, "bf16"),
+                                          (100, 96, 7, 10, "f32")])
+def test_factored_embedding(N, d, k, V, dtype):
+    seed = N + d + k
+    r = np.random.default_rng(seed)
+    Ef = (0.1 * r.standard_normal((V, k))).astype(np.float32)
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), dtype)
+    ids_h = r.integers(0, V, size=N).astype(np.int32)
+    ids_h[0], ids_h[-1] = 0, V - 1
+    X0 = ssn.factored_embedding(dev(ids_h, dtype), dev(Ef, "f32"), dev(Uh, dtype))
+    check("factored embedding", host(X0), O.factored_embedding(Ef, ids_h, Uh), dtype,
+          "bf16out" if dtype == "bf16" else "f32out_dec")
+
+
 # ---------------------------------------------------------------- exact cases
 @pytest.mark.parametrize("d,k", [(4096, 64), (256, 8), (100, 10)])
 def test_exact_special_cases(d, k):
