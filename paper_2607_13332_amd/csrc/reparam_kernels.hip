@@ -9,24 +9,28 @@
 #include "ssn_device.h"
 #include "ssn_launch.h"
 
+#include <type_traits>
+
 namespace ssn {
 
-constexpr int kFgRows = 64;      // tokens per chunk
-constexpr int kFgTiles = 8;      // 16-column tiles of din per block (128 columns)
-constexpr int kFgThreads = 256;  // 4 waves, two tiles each
-constexpr int kFgTargetBlocks = 512;
+constexpr int kFgRows = 32;      // tokens per chunk (one K step)
+constexpr int kFgTiles = 32;     // 16-column tiles of din per block (512 columns)
+constexpr int kFgThreads = 512;  // 8 waves, four tiles each
+constexpr int kFgTargetBlocks = 256;
 
 // ===========================================================================
 // MFMA kernel, bf16 H.  Block (column block x, token split y) owns din
-// columns [128x, 128x + 128) and tokens [y*tps, (y+1)*tps).  Per chunk of 64
+// columns [512x, 512x + 512) and tokens [y*tps, (y+1)*tps).  Per chunk of 32
 // tokens the block loads H rows (16-byte pieces; thread t moves piece t mod
-// 16 of rows t/16 + 16i) into a row-major LDS tile, and GT rows split into
+// 64 of rows t/64 + 8i) into a row-major LDS tile, and GT rows split into
 // bf16 hi + lo parts into two row-major LDS tiles (zero past k).  Both MFMA
 // operands are token-contiguous fragments read with LDS transpose reads:
 // A = H^T (16 din x 32 tokens), B = GT (32 tokens x 16 of k), two MFMAs per
-// pair (hi, lo) so GT keeps ~fp32 accuracy.  Wave w owns tiles w and w + 4
-// for all of k.  The block writes its partial sums for its token split; a
-// second kernel adds the splits in order (deterministic).
+// pair (hi, lo) so GT keeps ~fp32 accuracy.  Wave w owns tiles w + 8j for
+// all of k.  The wide column block makes each block's GT rows serve 512
+// columns (GT comes from L2 once per 512 columns).  The block writes its
+// partial sums for its token split; a second kernel adds the splits in order
+// (deterministic).
 // ===========================================================================
 template <int KT, bool K4>
 __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* __restrict__ H,
@@ -34,10 +38,13 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
                                                                float* __restrict__ out, int64_t N,
                                                                int din, int k, int64_t tps) {
   constexpr int R = kFgRows, NT = kFgThreads, NW = NT / kWave;
+  constexpr int CT = kFgTiles / NW;                    // tiles per wave
   constexpr int HP = 2 * kFgTiles, WP = HP + 1;      // H pieces per row, pitch in pieces
+  constexpr int RP = NT / HP;                          // H rows per pass
   constexpr int KS2 = (KT + 1) / 2, KW = 32 * KS2;   // GT tile width (bf16)
   constexpr int GPI = KW + 8;                          // GT tile pitch (bf16)
-  constexpr int NHP = R * HP / NT;                     // H pieces per thread per chunk (4)
+  constexpr int NHP = R / RP;                          // H pieces per thread per chunk
+  static_assert(NT % HP == 0 && R % RP == 0 && R % 32 == 0, "piece mapping");
   constexpr int NGQ = K4 ? (R * KW / 4 + NT - 1) / NT : (R * KW + NT - 1) / NT;
   __shared__ u32x4 ht[2][R * WP];
   __shared__ __align__(16) uint16_t gtl[2][2][R * GPI];   // [buffer][hi / lo][row * GPI + col]
@@ -53,18 +60,19 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
   // GT padding columns k .. KW are never written below
   for (int i = tid; i < 2 * 2 * R * GPI / 8; i += NT) ((u32x4*)&gtl[0][0][0])[i] = u32x4{0u, 0u, 0u, 0u};
 
-  const int h = tid % HP, row0 = tid / HP;
+  const int h = tid % HP, row0 = tid / HP;          // row0 < RP
   const bool hok = h < 2 * tcount;
   const uint16_t* hsrc = H + (t_begin + row0) * din + col0 + 8 * h;
 
-  u32x4 hv[NHP];
-  float gv[NGQ][K4 ? 4 : 1];
-  auto load = [&](int c) __attribute__((always_inline)) {
+  // two register sets: chunk c travels in set c % 2
+  u32x4 hv[2][NHP];
+  float gv[2][NGQ][K4 ? 4 : 1];
+  auto load = [&](int c, u32x4 (&hr)[NHP], float (&gr)[NGQ][K4 ? 4 : 1]) __attribute__((always_inline)) {
     const int64_t r0 = (int64_t)c * R;
 #pragma unroll
     for (int i = 0; i < NHP; ++i) {
-      const int64_t t = t_begin + r0 + row0 + 16 * i;
-      hv[i] = (hok && t < t_end) ? *(const u32x4*)(hsrc + (r0 + 16 * i) * din) : u32x4{0u, 0u, 0u, 0u};
+      const int64_t t = t_begin + r0 + row0 + RP * i;
+      hr[i] = (hok && t < t_end) ? *(const u32x4*)(hsrc + (r0 + RP * i) * din) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int j = 0; j < NGQ; ++j) {
@@ -74,17 +82,17 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
         const int64_t t = t_begin + r0 + row;
         const bool ok = q < R * (k / 4) && t < t_end;
         const f32x4 v = ok ? *(const f32x4*)(GT + t * k + 4 * c4) : f32x4{0.f, 0.f, 0.f, 0.f};
-        gv[j][0] = v[0]; gv[j][1] = v[1]; gv[j][2] = v[2]; gv[j][3] = v[3];
+        gr[j][0] = v[0]; gr[j][1] = v[1]; gr[j][2] = v[2]; gr[j][3] = v[3];
       } else {
         const int row = q / k;
         const int64_t t = t_begin + r0 + row;
-        gv[j][0] = (q < R * k && t < t_end) ? GT[t * k + (q - row * k)] : 0.f;
+        gr[j][0] = (q < R * k && t < t_end) ? GT[t * k + (q - row * k)] : 0.f;
       }
     }
   };
-  auto park = [&](int buf) __attribute__((always_inline)) {
+  auto park = [&](int buf, const u32x4 (&hr)[NHP], const float (&gr)[NGQ][K4 ? 4 : 1]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < NHP; ++i) ht[buf][(row0 + 16 * i) * WP + h] = hv[i];
+    for (int i = 0; i < NHP; ++i) ht[buf][(row0 + RP * i) * WP + h] = hr[i];
 #pragma unroll
     for (int j = 0; j < NGQ; ++j) {
       const int q = tid + NT * j;
@@ -94,52 +102,45 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
           uint32_t hi[2], lo[2];
 #pragma unroll
           for (int m = 0; m < 2; ++m) {
-            const uint32_t h0 = f32_to_bf16(gv[j][2 * m]), h1 = f32_to_bf16(gv[j][2 * m + 1]);
+            const uint32_t h0 = f32_to_bf16(gr[j][2 * m]), h1 = f32_to_bf16(gr[j][2 * m + 1]);
             hi[m] = h0 | (h1 << 16);
-            lo[m] = pack_bf16x2(gv[j][2 * m] - bf16_to_f32(h0), gv[j][2 * m + 1] - bf16_to_f32(h1));
+            lo[m] = pack_bf16x2(gr[j][2 * m] - bf16_to_f32(h0), gr[j][2 * m + 1] - bf16_to_f32(h1));
           }
           *(u32x2*)&gtl[buf][0][row * GPI + 4 * c4] = u32x2{hi[0], hi[1]};
           *(u32x2*)&gtl[buf][1][row * GPI + 4 * c4] = u32x2{lo[0], lo[1]};
         }
       } else if (q < R * k) {
         const int row = q / k, col = q - row * k;
-        const uint32_t h0 = f32_to_bf16(gv[j][0]);
+        const uint32_t h0 = f32_to_bf16(gr[j][0]);
         gtl[buf][0][row * GPI + col] = (uint16_t)h0;
-        gtl[buf][1][row * GPI + col] = (uint16_t)f32_to_bf16(gv[j][0] - bf16_to_f32(h0));
+        gtl[buf][1][row * GPI + col] = (uint16_t)f32_to_bf16(gr[j][0] - bf16_to_f32(h0));
       }
     }
   };
 
-  f32x4 acc[2][KT];
+  f32x4 acc[CT][KT];
 #pragma unroll
-  for (int ct = 0; ct < 2; ++ct)
+  for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
     for (int i = 0; i < KT; ++i) acc[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  __syncthreads();   // padding zeroed before the first park
-  if (nch > 0) {
-    load(0);
-    park(0);
-    if (nch > 1) load(1);
-  }
-  __syncthreads();
-  for (int c = 0; c < nch; ++c) {
-    const uint16_t* hb = (const uint16_t*)ht[c & 1];
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const uint16_t* hb = (const uint16_t*)ht[buf];
 #pragma unroll
     for (int ks = 0; ks < R / 32; ++ks) {
       const int r = 32 * ks + 8 * g + (L >> 2);
       u32x4 bhi[KT], blo[KT];
 #pragma unroll
       for (int i = 0; i < KT; ++i) {
-        const uint16_t* ph = &gtl[c & 1][0][r * GPI + 16 * i + 4 * (L & 3)];
-        const uint16_t* pl = &gtl[c & 1][1][r * GPI + 16 * i + 4 * (L & 3)];
+        const uint16_t* ph = &gtl[buf][0][r * GPI + 16 * i + 4 * (L & 3)];
+        const uint16_t* pl = &gtl[buf][1][r * GPI + 16 * i + 4 * (L & 3)];
         const u32x2 a = lds_read_tr16(ph), b = lds_read_tr16(ph + 4 * GPI);
         const u32x2 x = lds_read_tr16(pl), y = lds_read_tr16(pl + 4 * GPI);
         bhi[i] = u32x4{a[0], a[1], b[0], b[1]};
         blo[i] = u32x4{x[0], x[1], y[0], y[1]};
       }
 #pragma unroll
-      for (int ct = 0; ct < 2; ++ct) {
+      for (int ct = 0; ct < CT; ++ct) {
         const int jl = wave + NW * ct;
         if (jl < tcount) {
           const uint16_t* p = hb + r * (8 * WP) + 16 * jl + 4 * (L & 3);
@@ -153,15 +154,33 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
         }
       }
     }
-    if (c + 1 < nch) park((c + 1) & 1);
-    if (c + 2 < nch) load(c + 2);
+  };
+
+  __syncthreads();   // padding zeroed before the first park
+  // chunk 0 parked, chunks 1 and 2 in flight
+  if (nch > 0) {
+    load(0, hv[0], gv[0]);
+    park(0, hv[0], gv[0]);
+    if (nch > 1) load(1, hv[1], gv[1]);
+    if (nch > 2) load(2, hv[0], gv[0]);
+  }
+  __syncthreads();
+  auto step = [&](int c, auto S) __attribute__((always_inline)) {
+    constexpr int sl = decltype(S)::value;      // register set of chunk c + 1
+    compute(c & 1);
+    if (c + 1 < nch) park((c + 1) & 1, hv[sl], gv[sl]);
+    if (c + 3 < nch) load(c + 3, hv[sl], gv[sl]);
     __syncthreads();
+  };
+  for (int c = 0; c < nch; c += 2) {
+    step(c, std::integral_constant<int, 1>{});
+    if (c + 1 < nch) step(c + 1, std::integral_constant<int, 0>{});
   }
 
   // lane (L, g) of tile (jl, i) holds dZp[col0 + 16 jl + 4g + e][16 i + L]
   float* dst = out + (int64_t)blockIdx.y * din * k;
 #pragma unroll
-  for (int ct = 0; ct < 2; ++ct) {
+  for (int ct = 0; ct < CT; ++ct) {
     const int jl = wave + NW * ct;
     if (jl < tcount) {
 #pragma unroll
@@ -207,12 +226,12 @@ static bool factor_grad_uses_mfma(int dtype, int64_t din, int64_t k) {
   return dtype == kBF16 && din % 16 == 0 && din <= INT32_MAX / 2 && k >= 1 && k <= 128;
 }
 
-// Token splits: enough blocks for about two per compute unit, at least one
-// chunk of tokens per split.  Depends on (N, din) only, so results are the
-// same on every device.
+// Token splits: as many as keep the grid within one round of one block per
+// compute unit of an MI355X (256), at least one chunk of tokens per split.
+// Depends on (N, din) only, so results are the same on every device.
 static int64_t factor_grad_splits(int64_t N, int64_t din) {
   const int64_t cb = (din / 16 + kFgTiles - 1) / kFgTiles;
-  int64_t S = (kFgTargetBlocks + cb - 1) / cb;
+  int64_t S = kFgTargetBlocks / cb;
   const int64_t chunks = (N + kFgRows - 1) / kFgRows;
   S = S > chunks ? chunks : S;
   return S < 1 ? 1 : S;

@@ -158,8 +158,8 @@ def test_reparam_validation(ssn):
     assert w(0, 32768, 14336, 64) == 0                                    # generic path: none
     b = L.ssn_reparam_backward
     E6 = 0x7F5000000000
-    need = w(1, 1000, 256, 16)                  # 16 token splits of 64 tokens
-    assert need == 16 * 256 * 16 * 4
+    need = w(1, 1000, 256, 16)                  # 32 token splits of 32 tokens (one chunk each)
+    assert need == 32 * 256 * 16 * 4
     assert b(1, 1000, 256, 128, 16, A, B, C, D, F, E6, 0x7F6000000000, 0x7F7000000000,
              need - 4, None) == ERR_SHAPE                                  # workspace too small
     assert b(1, 10, 256, 128, 16, A, B, C, D, F, E6, None, None, 0, None) == ERR_NULL
