@@ -159,6 +159,46 @@ def factored_embedding(E, ids, U) -> np.ndarray:
     return decompress(np.asarray(E)[np.asarray(ids)], None, None, U)
 
 
+# --------------------------------------------------------------------------
+# Sparse weight averaging with the delta rule (section 4.2, Eq. (sparta) and
+# Eq. (delta_rule); the asynchronous sparse weight-averaging algorithm of
+# section 3.3.1).  Each round
+# selects an index set P of the float32 master weights theta (a rotating
+# segment, or any shared index set); every replica snapshots theta[P]; a
+# reducer averages the replicas' snapshots with weights w_i and returns each
+# sender the difference average - snapshot; the replica, whose weights have
+# moved on meanwhile, adds lambda times (average - snapshot) to them
+# (lambda = 1 in the paper).
+# --------------------------------------------------------------------------
+def sparta_indices(n: int, m: int, I=None, first: int = 0) -> np.ndarray:
+    """The round's index set: the list I, or the segment [first, first + m)."""
+    if I is not None:
+        return np.asarray(I, dtype=np.int64)
+    return np.arange(first, first + m, dtype=np.int64)
+
+
+def sparta_snapshot(theta, idx) -> np.ndarray:
+    """snap = theta[P]."""
+    return f64(theta)[np.asarray(idx, dtype=np.int64)]
+
+
+def sparta_average(chunks, weights):
+    """acc = sum_i w_i c_i / sum_i w_i; delta_i = acc - c_i (what the reducer
+    returns to sender i)."""
+    C = np.stack([f64(c) for c in chunks])
+    w = np.asarray(weights, dtype=np.float64)
+    acc = (w[:, None] * C).sum(axis=0) / w.sum()
+    return acc, [acc - C[i] for i in range(C.shape[0])]
+
+
+def delta_rule(theta, idx, avg, snap, lam: float = 1.0) -> np.ndarray:
+    """theta[P] <- theta[P] + lam (avg - snap); other entries unchanged."""
+    out = f64(theta).copy()
+    idx = np.asarray(idx, dtype=np.int64)
+    out[idx] = out[idx] + lam * (f64(avg) - f64(snap))
+    return out
+
+
 def rel_frobenius(got, ref) -> float:
     """||got - ref||_F / ||ref||_F in float64 (the parity metric)."""
     g = f64(got) if np.asarray(got).dtype == np.uint16 else np.asarray(got, dtype=np.float64)

@@ -281,3 +281,46 @@ def test_reparam_rows_stay_in_the_subspace_and_embedding_round_trips():
     G = r.standard_normal((N, d))
     assert _rel(O.reparam_grad_factor(H, G, U), (H.T @ G) @ U) < 1e-13
 
+
+# ---------------------------------------------------------------- sparse averaging, delta rule
+def test_delta_rule_consensus_and_retained_progress():
+    """Eq. (sparta) / Eq. (delta_rule): replicas that did not move during the
+    round end on the average; replicas that moved keep their local update on
+    top of the consensus shift; coordinates outside P never change."""
+    r = np.random.default_rng(9)
+    n, R = 200, 4
+    P = O.sparta_indices(n, 10, I=r.choice(n, 10, replace=False))
+    thetas = [r.standard_normal(n) for _ in range(R)]
+    snaps = [O.sparta_snapshot(t, P) for t in thetas]
+    avg, deltas = O.sparta_average(snaps, [1.0] * R)
+    assert np.allclose(avg, np.mean([t[P] for t in thetas], axis=0), rtol=0, atol=1e-15)
+    for j in range(R):
+        # no local progress: the replica lands on the average exactly (up to rounding)
+        out = O.delta_rule(thetas[j], P, avg, snaps[j])
+        assert np.allclose(out[P], avg, atol=1e-15)
+        mask = np.ones(n, bool)
+        mask[P] = False
+        assert np.array_equal(out[mask], thetas[j][mask])
+        # local progress made during the round is kept
+        moved = thetas[j] + 0.25
+        out2 = O.delta_rule(moved, P, avg, snaps[j])
+        assert np.allclose(out2[P] - avg, moved[P] - snaps[j], atol=1e-14)
+        # the reducer's return is the same correction
+        assert np.allclose(snaps[j] + deltas[j], avg, atol=1e-15)
+    # lam scales the correction (AsyncMesh form); lam = 0 leaves theta alone
+    assert np.array_equal(O.delta_rule(thetas[0], P, avg, snaps[0], 0.0), thetas[0])
+
+
+def test_sparta_weighted_average_and_segments():
+    """Weighted mean by hand, zero-weight senders add nothing (the averaging
+    algorithm lets a sender with weight 0 absorb the average), the weighted
+    deltas sum to zero, and 20 rotating segments tile the vector."""
+    c = [np.array([1.0, 2.0]), np.array([3.0, 6.0]), np.array([100.0, -7.0])]
+    acc, deltas = O.sparta_average(c, [1.0, 3.0, 0.0])
+    assert np.allclose(acc, [(1 + 9) / 4, (2 + 18) / 4])
+    assert np.allclose(deltas[2], acc - c[2])
+    assert np.allclose(sum(w * dl for w, dl in zip([1.0, 3.0, 0.0], deltas)), 0.0)
+    n, segs = 1000, 20
+    cover = np.concatenate([O.sparta_indices(n, n // segs, first=j * (n // segs)) for j in range(segs)])
+    assert np.array_equal(np.sort(cover), np.arange(n))
+
