@@ -44,6 +44,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_2607_13332_amd/csrc/codec_kernels.hip",
                   "paper_2607_13332_amd/csrc/weights_kernels.hip",
                   "paper_2607_13332_amd/csrc/reparam_kernels.hip",
+                  "paper_2607_13332_amd/csrc/sparta_kernels.hip",
                   "paper_2607_13332_amd/csrc/ssn_device.h"]
 
 
@@ -66,6 +67,8 @@ def parse_args():
                    help="skip the k=64 sweep points (d=4096, N=4096..131072, Zipf ids)")
     p.add_argument("--no-reparam", action="store_true",
                    help="skip the reparameterized-SSN projection timings")
+    p.add_argument("--no-sparta", action="store_true",
+                   help="skip the sparse-averaging round (320M-parameter block)")
     p.add_argument("--no-paper-shapes", action="store_true",
                    help="skip the timings at the paper's own stage shapes (d=5120 k=51, d=2048 k=40)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -211,6 +214,60 @@ def time_reparam(N: int, din: int, d: int, k: int, steps: int, dev, seed: int = 
            "backward_frac_hbm_peak": round(bb / (bwd * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "tokens_per_s_fwd_bwd": round(N / ((fwd + bwd) * 1e-3), 1)}
     del H, G, Zp, U, T, Y, GT, GH, GZ, ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def time_sparta(cfg, steps: int, dev):
+    """One sparse-averaging round over a block of float32 master weights
+    (section 4.2): snapshot, the reducer's average with per-sender deltas,
+    the receive step (buffer += delta) and the delta rule, for a rotating
+    segment and for a sorted random index set of the same size."""
+    import torch
+    from paper_2607_13332_amd import inputs as I
+    from paper_2607_13332_amd import ssn
+    m, R = cfg.m, cfg.R
+    theta = I.sparta_replica_device(cfg.n, cfg.seed, dev)
+    first, _ = ssn.sparta_segment(cfg.n, 7)
+    Ilist = I.sparta_positions_device(cfg.n, m, cfg.seed, dev)
+    snap = torch.empty(m, dtype=torch.float32, device=dev)
+    ssn.sparta_snapshot(theta, first=first, m=m, out=snap)
+    chunks = I.sparta_chunks_device(snap, R, cfg.seed)
+    acc = torch.empty(m, dtype=torch.float32, device=dev)
+    deltas = [torch.empty(m, dtype=torch.float32, device=dev) for _ in range(R)]
+    w = [1.0] * R
+    ops = {
+        "snapshot_segment": (lambda: ssn.sparta_snapshot(theta, first=first, m=m, out=snap), 8 * m),
+        "snapshot_list": (lambda: ssn.sparta_snapshot(theta, I=Ilist, out=snap), 16 * m),
+        "average": (lambda: ssn.sparta_average(chunks, w, acc=acc, deltas=deltas), 4 * m * (2 * R + 1)),
+        "receive_segment": (lambda: ssn.delta_rule(theta, deltas[0], None, first=first), 12 * m),
+        "apply_segment": (lambda: ssn.delta_rule(theta, acc, snap, first=first), 16 * m),
+        "apply_list": (lambda: ssn.delta_rule(theta, acc, snap, I=Ilist), 24 * m),
+    }
+    reps = max(10, steps)
+    out = {"workload": f"{cfg.n / 1e6:.0f}M float32 parameters, p = 1/{cfg.segments} "
+                       f"({m / 1e6:.0f}M per round), {R} senders",
+           "per_op": {}}
+    total = 0.0
+    for name, (fn, nbytes) in ops.items():
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out["per_op"][name] = {"ms": round(ms, 5), "algorithmic_bytes": nbytes,
+                               "algorithmic_GBps": round(gbs, 1),
+                               "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+        if name in ("snapshot_segment", "average", "receive_segment", "apply_segment"):
+            total += ms
+    out["round_segment_ms"] = round(total, 5)
+    del theta, Ilist, snap, chunks, acc, deltas
     torch.cuda.empty_cache()
     return out
 
@@ -465,6 +522,10 @@ def main():
             "paper8b_mlp_out": time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2), dev),
             "stage8b_mlp_out": time_reparam(32768, 14336, 4096, 64, max(10, args.steps // 2), dev),
         }
+
+    # ---------------- sparse averaging with the delta rule (section 4.2) ----------------
+    if not args.no_sparta:
+        result["sparta"] = time_sparta(I.SPARTA_BLOCK8B, args.steps, dev)
 
     # ---------------- CPU baseline: the oracle on a bounded sample ----------------
     if not args.no_cpu_baseline:

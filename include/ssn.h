@@ -8,7 +8,8 @@
  * E[ids] that both sides of the boundary hold (Eq. (2)); the receiver rebuilds
  * the activation with U^T; gradients travel back through the same compression;
  * and the original SSN re-projects its full-width output projections into
- * span(U) after every optimizer step.
+ * span(U) after every optimizer step.  The data-parallel side (section 4.2)
+ * adds the per-GPU steps of sparse weight averaging with the delta rule.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -45,6 +46,8 @@ extern "C" {
 #define SSN_ABI_VERSION 1
 /* Largest matrix count accepted by ssn_project_weights_batched. */
 #define SSN_MAX_BATCH 16
+/* Largest sender count accepted by ssn_sparta_average. */
+#define SSN_SPARTA_MAX_SENDERS 64
 
 typedef enum { SSN_F32 = 0, SSN_BF16 = 1 } ssn_dtype_t;
 
@@ -244,6 +247,60 @@ ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int
 ssn_status_t ssn_factored_embedding(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
                                     const int32_t *ids, const float *E, const void *U, void *X0,
                                     void *stream);
+
+/*
+ * Sparse weight averaging with the delta rule (section 4.2, Eq. (sparta) and
+ * Eq. (delta_rule); the averaging round of the worker in section 3.3.1): the
+ * one-GPU steps of a round over the float32 master weights theta [n].  A round
+ * selects m positions P (p = 5% of the parameters in the paper):
+ *   I != NULL   P_i = I[i], I an int64 DEVICE array of m DISTINCT positions
+ *               in [0, n).  Entries outside [0, n) are a contract violation:
+ *               they are clamped into range (memory stays in bounds) and the
+ *               affected values are unspecified; repeated positions race.
+ *   I == NULL   the segment P_i = first + i, with 0 <= first and
+ *               first + m <= n (else SSN_ERR_SHAPE).  The paper tiles theta
+ *               with 20 such segments and rotates through them.
+ * All arithmetic is float32; m == 0 is a no-op.  Segment calls whose pointers
+ * are 16-byte aligned (and m % 4 == 0) use 16-byte accesses.
+ */
+
+/*
+ * ssn_sparta_snapshot -- snap[i] = theta[P_i], the copy each replica takes at
+ * the start of a round.  theta [n] float32, snap [m] float32 output; snap
+ * must not overlap theta or I.  One launch.
+ */
+ssn_status_t ssn_sparta_snapshot(int64_t n, int64_t m, const int64_t *I, int64_t first,
+                                 const float *theta, float *snap, void *stream);
+
+/*
+ * ssn_sparta_average -- the reducer's step for one slice of m values from R
+ * senders:
+ *   acc[i]      = sum_r w_r chunks[r][i] / sum_r w_r   (senders summed in order)
+ *   deltas[r][i] = acc[i] - chunks[r][i]                (what sender r receives)
+ * chunks and deltas are HOST arrays of R device pointers ([m] float32 each);
+ * weights is a HOST array of R floats, or NULL for all ones.  Weights must be
+ * finite and >= 0 with a positive sum (else SSN_ERR_SHAPE); a sender with
+ * weight 0 adds nothing to acc and still gets its delta.  deltas may be NULL,
+ * and so may any entry (that delta is not written).  1 <= R <=
+ * SSN_SPARTA_MAX_SENDERS.  Outputs must not overlap the chunks or each other.
+ * One launch.
+ */
+ssn_status_t ssn_sparta_average(int64_t R, int64_t m, const float *const *chunks,
+                                const float *weights, float *acc, float *const *deltas,
+                                void *stream);
+
+/*
+ * ssn_delta_rule -- apply a finished round to the weights, in place:
+ *   theta[P_i] += lambda * (avg[i] - snap[i])
+ * avg [m] float32 is the group average, snap [m] float32 the snapshot taken
+ * at the start of the round, so progress made meanwhile is kept (the paper
+ * uses lambda = 1).  snap may be NULL: theta[P_i] += lambda * avg[i], which
+ * is also how a replica adds the delta a reducer returned to its buffer.
+ * lambda must be finite (else SSN_ERR_SHAPE).  theta must not overlap avg,
+ * snap or I.  One launch.
+ */
+ssn_status_t ssn_delta_rule(int64_t n, int64_t m, const int64_t *I, int64_t first, float *theta,
+                            const float *avg, const float *snap, float lambda, void *stream);
 
 #ifdef __cplusplus
 }

@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <math.h>
 #include <stdint.h>
 
 #include "ssn_launch.h"
@@ -281,6 +282,83 @@ ssn_status_t ssn_project_weights(ssn_dtype_t dtype, int64_t d, int64_t n, int64_
   if (n == 0 && d >= 1 && k >= 1 && k <= d) return SSN_OK;
   if (n > 0 && !W) return SSN_ERR_NULL;
   return ssn_project_weights_batched(dtype, 1, d, nn, k, w, U, stream);
+}
+
+// Index set of a sparse-averaging round: the list form needs n >= 1, the
+// segment form first + m <= n.
+static ssn_status_t sparta_shape(int64_t n, int64_t m, const int64_t* I, int64_t first) {
+  if (n < 0 || m < 0 || n > kMaxElems / 4 || m > kMaxElems / 8) return SSN_ERR_SHAPE;
+  if (m == 0) return SSN_OK;
+  if (I) return n >= 1 ? SSN_OK : SSN_ERR_SHAPE;
+  if (first < 0 || first > n || m > n - first) return SSN_ERR_SHAPE;
+  return SSN_OK;
+}
+
+ssn_status_t ssn_sparta_snapshot(int64_t n, int64_t m, const int64_t* I, int64_t first,
+                                 const float* theta, float* snap, void* stream) {
+  const ssn_status_t sh = sparta_shape(n, m, I, first);
+  if (sh != SSN_OK || m == 0) return sh;
+  if (!theta || !snap) return SSN_ERR_NULL;
+  if (!aligned_to(theta, 4) || !aligned_to(snap, 4) || (I && !aligned_to(I, 8))) return SSN_ERR_ALIGN;
+  const Span out = span(snap, m * 4);
+  if (overlap(out, span(theta, n * 4)) || (I && overlap(out, span(I, m * 8)))) return SSN_ERR_ALIAS;
+  return launch_status(ssn::launch_sparta_snapshot(n, m, I, first, theta, snap, (hipStream_t)stream));
+}
+
+ssn_status_t ssn_sparta_average(int64_t R, int64_t m, const float* const* chunks,
+                                const float* weights, float* acc, float* const* deltas,
+                                void* stream) {
+  if (R < 1 || R > SSN_SPARTA_MAX_SENDERS || m < 0 || m > kMaxElems / 8) return SSN_ERR_SHAPE;
+  if (weights) {
+    double wsum = 0.0;
+    for (int64_t r = 0; r < R; ++r) {
+      if (!isfinite(weights[r]) || weights[r] < 0.f) return SSN_ERR_SHAPE;
+      wsum += weights[r];
+    }
+    if (!(wsum > 0.0) || !isfinite((float)(1.0 / wsum))) return SSN_ERR_SHAPE;
+  }
+  if (m == 0) return SSN_OK;
+  if (!chunks || !acc) return SSN_ERR_NULL;
+  if (!aligned_to(acc, 4)) return SSN_ERR_ALIGN;
+  for (int64_t r = 0; r < R; ++r) {
+    if (!chunks[r]) return SSN_ERR_NULL;
+    if (!aligned_to(chunks[r], 4)) return SSN_ERR_ALIGN;
+    if (deltas && deltas[r] && !aligned_to(deltas[r], 4)) return SSN_ERR_ALIGN;
+  }
+  const int64_t bytes = m * 4;
+  const Span a = span(acc, bytes);
+  for (int64_t r = 0; r < R; ++r) {
+    const Span c = span(chunks[r], bytes);
+    if (overlap(a, c)) return SSN_ERR_ALIAS;
+    if (!deltas) continue;
+    for (int64_t q = 0; q < R; ++q)
+      if (deltas[q] && overlap(span(deltas[q], bytes), c)) return SSN_ERR_ALIAS;
+    if (!deltas[r]) continue;
+    const Span dr = span(deltas[r], bytes);
+    if (overlap(dr, a)) return SSN_ERR_ALIAS;
+    for (int64_t q = 0; q < r; ++q)
+      if (deltas[q] && overlap(dr, span(deltas[q], bytes))) return SSN_ERR_ALIAS;
+  }
+  return launch_status(ssn::launch_sparta_average((int)R, m, chunks, weights, acc, deltas,
+                                                  (hipStream_t)stream));
+}
+
+ssn_status_t ssn_delta_rule(int64_t n, int64_t m, const int64_t* I, int64_t first, float* theta,
+                            const float* avg, const float* snap, float lambda, void* stream) {
+  const ssn_status_t sh = sparta_shape(n, m, I, first);
+  if (sh != SSN_OK) return sh;
+  if (!isfinite(lambda)) return SSN_ERR_SHAPE;
+  if (m == 0) return SSN_OK;
+  if (!theta || !avg) return SSN_ERR_NULL;
+  if (!aligned_to(theta, 4) || !aligned_to(avg, 4) || (snap && !aligned_to(snap, 4)) ||
+      (I && !aligned_to(I, 8)))
+    return SSN_ERR_ALIGN;
+  const Span t = span(theta, n * 4);
+  if (overlap(t, span(avg, m * 4)) || (snap && overlap(t, span(snap, m * 4))) ||
+      (I && overlap(t, span(I, m * 8))))
+    return SSN_ERR_ALIAS;
+  return launch_status(ssn::launch_delta_rule(n, m, I, first, theta, avg, snap, lambda,
+                                              (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -10,6 +10,7 @@ namespace ssn {
 constexpr int kF32 = 0;
 constexpr int kBF16 = 1;
 constexpr int kMaxBatch = 16;
+constexpr int kSpartaMaxSenders = 64;
 
 // Compute units of the current device (cached per device).
 int device_cu_count();
@@ -34,5 +35,17 @@ hipError_t launch_factor_grad(int dtype, int64_t N, int64_t din, int64_t k, cons
 // count matrices W[b] [d, n[b]] sharing U [d, k], re-projected in place.
 hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t* n, int64_t k,
                                   void* const* W, const void* U, hipStream_t st);
+
+// Sparse averaging round (float32): snap = theta[P]; acc and per-sender
+// deltas from R chunks (host arrays; weights NULL = all 1, deltas NULL or a
+// NULL entry = not written); theta[P] += lambda (avg - snap), or
+// += lambda avg when snap is NULL.  P = I[0..m) when I is non-NULL, else
+// [first, first + m).
+hipError_t launch_sparta_snapshot(int64_t n, int64_t m, const int64_t* I, int64_t first,
+                                  const float* theta, float* snap, hipStream_t st);
+hipError_t launch_sparta_average(int R, int64_t m, const float* const* chunks, const float* weights,
+                                 float* acc, float* const* deltas, hipStream_t st);
+hipError_t launch_delta_rule(int64_t n, int64_t m, const int64_t* I, int64_t first, float* theta,
+                             const float* avg, const float* snap, float lambda, hipStream_t st);
 
 }  // namespace ssn

@@ -29,7 +29,8 @@ import numpy as np
 # Independent random streams per input kind, so that e.g. changing the noise
 # level never changes the basis or the ids.
 STREAM = {"U": 0, "E": 1, "ids": 2, "Z0": 3, "noise": 4, "X": 5, "G": 6, "W": 7,
-          "perm": 8, "sel": 9, "uZipf": 10}
+          "perm": 8, "sel": 9, "uZipf": 10, "theta": 11, "drift": 12, "P": 13,
+          "progress": 14}
 
 
 def rng(seed: int, stream: str) -> np.random.Generator:
@@ -177,7 +178,7 @@ def sweep_configs():
 
 
 def paper_configs():
-    """The paper's own stage-boundary shapes (section 4.2 model card and the
+    """The paper's own stage-boundary shapes (section 5.2 model card and the
     1B ablation card of section 6): Pluralis-8B d=5120 at rank ~51 (100x),
     S=4096; the 1B model d=2048 at rank 40, S=2048; vocabulary 128,256; a
     microbatch of b coalesced sequences, b in {1, 2, 3}."""
@@ -200,6 +201,75 @@ WEIGHTS_PAPER1B = WeightsConfig("weights_paper1b", d=2048, k=40, layers=4,
                                 shapes=((2048, 2048), (2048, 7168)), dtype="bf16", seed=1031)
 
 CONFIGS = {c.name: c for c in [TINY, MID, STAGE8B] + sweep_configs() + paper_configs()}
+
+
+@dataclasses.dataclass(frozen=True)
+class SpartaConfig:
+    """One sparse-averaging round over a block of float32 master weights."""
+    name: str
+    n: int                 # parameters of the block
+    R: int                 # replicas contributing to the round
+    seed: int
+    segments: int = 20     # p = 1 / segments of the block per round
+    std: float = 0.02      # weight scale
+    drift: float = 1e-3    # spread between replicas, and local progress per round
+
+    @property
+    def m(self) -> int:
+        return self.n // self.segments
+
+
+# The paper's per-block estimate (section 4.2): p = 5% of a block is about 16M
+# parameters, 0.5 Gbit per round against 10 Gbit for the whole block, so a
+# block holds about 320M float32 parameters; four senders as in the averaging
+# round pictured in section 3.3.1.
+SPARTA_BLOCK8B = SpartaConfig("sparta_block8b", n=320_000_000, R=4, seed=1040)
+SPARTA_TINY = SpartaConfig("sparta_tiny", n=100_003, R=3, seed=1041)
+
+
+def sparta_replicas_host(n: int, R: int, seed: int, std: float = 0.02,
+                         drift: float = 1e-3) -> np.ndarray:
+    """[R, n] float32 replicas: a shared N(0, std^2) vector plus per-replica
+    N(0, drift^2) divergence."""
+    base = std * rng(seed, "theta").standard_normal(n)
+    spread = drift * rng(seed, "drift").standard_normal((R, n))
+    return (base[None, :] + spread).astype(np.float32)
+
+
+def sparta_progress_host(n: int, seed: int, drift: float = 1e-3) -> np.ndarray:
+    """[n] float32 local progress a replica makes while a round is in flight."""
+    return (drift * rng(seed, "progress").standard_normal(n)).astype(np.float32)
+
+
+def sparta_positions_host(n: int, m: int, seed: int, order: str = "sorted") -> np.ndarray:
+    """m distinct int64 positions in [0, n): a shared random index set, sorted
+    or in random order."""
+    pos = rng(seed, "P").choice(n, size=m, replace=False).astype(np.int64)
+    return np.sort(pos) if order == "sorted" else pos
+
+
+def sparta_replica_device(n: int, seed: int, device, std: float = 0.02):
+    """[n] float32 weights of one replica drawn on the device."""
+    import torch
+    return std * torch.randn(n, generator=_gen(device, seed, "theta"), device=device)
+
+
+def sparta_chunks_device(snap, R: int, seed: int, drift: float = 1e-3):
+    """R senders' chunks around a snapshot: chunk 0 is the snapshot itself,
+    the others add N(0, drift^2) divergence (device draws)."""
+    import torch
+    g = _gen(snap.device, seed, "drift")
+    out = [snap.clone()]
+    for _ in range(R - 1):
+        out.append(snap + drift * torch.randn(snap.shape, generator=g, device=snap.device))
+    return out
+
+
+def sparta_positions_device(n: int, m: int, seed: int, device):
+    """m distinct sorted int64 positions in [0, n) drawn on the device."""
+    import torch
+    perm = torch.randperm(n, generator=_gen(device, seed, "P"), device=device)
+    return torch.sort(perm[:m]).values.contiguous()
 
 
 def with_tokens(cfg: CodecConfig, N: int, seed: Optional[int] = None) -> CodecConfig:

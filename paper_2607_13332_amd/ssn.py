@@ -20,6 +20,7 @@ SSN_F32, SSN_BF16 = 0, 1
 OPS = {"compress": 0, "decompress": 1, "project_grad": 2, "project_weights": 3,
        "compress_projected": 4}
 MAX_BATCH = 16
+SPARTA_MAX_SENDERS = 64
 
 _c_i64 = ctypes.c_int64
 _c_p = ctypes.c_void_p
@@ -65,6 +66,15 @@ def _declare(lib):
                                            _c_p, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_project_weights.restype = ctypes.c_int
     lib.ssn_project_weights.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]
+    lib.ssn_sparta_snapshot.restype = ctypes.c_int
+    lib.ssn_sparta_snapshot.argtypes = [_c_i64, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_p]
+    lib.ssn_sparta_average.restype = ctypes.c_int
+    lib.ssn_sparta_average.argtypes = [_c_i64, _c_i64, ctypes.POINTER(_c_p),
+                                       ctypes.POINTER(ctypes.c_float), _c_p,
+                                       ctypes.POINTER(_c_p), _c_p]
+    lib.ssn_delta_rule.restype = ctypes.c_int
+    lib.ssn_delta_rule.argtypes = [_c_i64, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_p,
+                                   ctypes.c_float, _c_p]
     lib.ssn_project_weights_batched.restype = ctypes.c_int
     lib.ssn_project_weights_batched.argtypes = [ctypes.c_int, _c_i64, _c_i64,
                                                 ctypes.POINTER(_c_i64), _c_i64,
@@ -336,3 +346,98 @@ def project_weights_batched(Ws: Sequence[torch.Tensor], U: torch.Tensor, stream=
     _check("ssn_project_weights_batched", lib().ssn_project_weights_batched(
         _dt_code(t), count, d, ns, k, ps, _dev(U, "U", t, 2), _stream(stream)))
     return Ws
+
+
+# --------------------------------------------------------------------------
+# Sparse weight averaging with the delta rule (section 4.2): float32 master
+# weights theta [n]; a round's positions are an int64 list I or a segment.
+# --------------------------------------------------------------------------
+SPARTA_SEGMENTS = 20
+
+
+def sparta_segment(n: int, r: int, segments: int = SPARTA_SEGMENTS):
+    """(first, m) of the segment averaged in round r: `segments` contiguous
+    segments tile [0, n) (sizes differ by at most one) and rounds rotate
+    through them in order."""
+    if n < 0 or segments < 1:
+        raise ValueError("n >= 0 and segments >= 1")
+    s = r % segments
+    first = s * n // segments
+    return first, (s + 1) * n // segments - first
+
+
+def _positions(I, m, first):
+    if I is None:
+        if m is None:
+            raise ValueError("give the index list I or the segment length m")
+        return 0, int(m), int(first)
+    return _dev(I, "I", torch.int64, 1), I.numel(), 0
+
+
+def sparta_snapshot(theta: torch.Tensor, I: Optional[torch.Tensor] = None, first: int = 0,
+                    m: Optional[int] = None, out: Optional[torch.Tensor] = None,
+                    stream=None) -> torch.Tensor:
+    """snap = theta[P] with P = I, or the segment [first, first + m)."""
+    pI, m, first = _positions(I, m, first)
+    if out is None:
+        out = torch.empty(m, dtype=torch.float32, device=theta.device)
+    _same_device(theta, I, out)
+    _check("ssn_sparta_snapshot", lib().ssn_sparta_snapshot(
+        theta.numel(), m, pI, first, _dev(theta, "theta", torch.float32, 1),
+        _dev(out, "snap", torch.float32, 1), _stream(stream)))
+    return out
+
+
+def sparta_average(chunks: Sequence[torch.Tensor], weights: Optional[Sequence[float]] = None,
+                   acc: Optional[torch.Tensor] = None, deltas=None, stream=None):
+    """acc = sum_r w_r c_r / sum_r w_r and delta_r = acc - c_r for the R
+    senders' chunks (float32 [m] each).  deltas: None allocates them, False
+    skips them, a list (entries may be None) receives them."""
+    R = len(chunks)
+    if not 1 <= R <= SPARTA_MAX_SENDERS:
+        raise ValueError(f"1 <= len(chunks) <= {SPARTA_MAX_SENDERS}")
+    m = chunks[0].numel()
+    dev = chunks[0].device
+    if acc is None:
+        acc = torch.empty(m, dtype=torch.float32, device=dev)
+    if deltas is None:
+        deltas = [torch.empty(m, dtype=torch.float32, device=dev) for _ in range(R)]
+    cs = (_c_p * R)()
+    for r, c in enumerate(chunks):
+        if c.numel() != m:
+            raise ValueError(f"chunk {r} has {c.numel()} values, expected {m}")
+        cs[r] = _dev(c, f"chunks[{r}]", torch.float32, 1)
+    ds = None
+    if deltas is not False:
+        if len(deltas) != R:
+            raise ValueError(f"{len(deltas)} delta buffers for {R} senders")
+        ds = (_c_p * R)()
+        for r, dl in enumerate(deltas):
+            if dl is not None:
+                if dl.numel() != m:
+                    raise ValueError(f"delta {r} has {dl.numel()} values, expected {m}")
+                ds[r] = _dev(dl, f"deltas[{r}]", torch.float32, 1)
+    ws = None
+    if weights is not None:
+        if len(weights) != R:
+            raise ValueError(f"{len(weights)} weights for {R} senders")
+        ws = (ctypes.c_float * R)(*[float(w) for w in weights])
+    _same_device(acc, *chunks, *([dl for dl in deltas if dl is not None] if deltas else []))
+    _check("ssn_sparta_average", lib().ssn_sparta_average(
+        R, m, cs, ws, _dev(acc, "acc", torch.float32, 1), ds, _stream(stream)))
+    return acc, (deltas if deltas is not False else None)
+
+
+def delta_rule(theta: torch.Tensor, avg: torch.Tensor, snap: Optional[torch.Tensor] = None,
+               I: Optional[torch.Tensor] = None, first: int = 0, lam: float = 1.0,
+               stream=None) -> torch.Tensor:
+    """In place: theta[P] += lam (avg - snap), or += lam avg without snap."""
+    pI, m, first = _positions(I, avg.numel() if I is None else None, first)
+    if avg.numel() != m or (snap is not None and snap.numel() != m):
+        raise ValueError(f"avg/snap must hold {m} values")
+    _same_device(theta, avg, snap, I)
+    _check("ssn_delta_rule", lib().ssn_delta_rule(
+        theta.numel(), m, pI, first, _dev(theta, "theta", torch.float32, 1),
+        _dev(avg, "avg", torch.float32, 1),
+        0 if snap is None else _dev(snap, "snap", torch.float32, 1), float(lam), _stream(stream)))
+    return theta

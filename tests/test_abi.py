@@ -192,6 +192,61 @@ def test_project_weights_validation(ssn):
     assert g(1, 2, 64, n0, 8, w, None, None) == OK                        # all empty: no-op
 
 
+def test_sparta_validation(ssn):
+    L = ssn.lib()
+    P = ctypes.c_void_p
+    s = L.ssn_sparta_snapshot
+    assert s(100, 0, None, 0, None, None, None) == OK                       # empty round
+    assert s(100, 10, None, 95, A, B, None) == ERR_SHAPE                    # segment past n
+    assert s(100, 10, None, -1, A, B, None) == ERR_SHAPE
+    assert s(0, 10, C, 0, A, B, None) == ERR_SHAPE                          # list on empty theta
+    assert s(100, 10, None, 0, None, B, None) == ERR_NULL
+    assert s(100, 10, None, 0, A + 2, B, None) == ERR_ALIGN
+    assert s(100, 10, C + 4, 0, A, B, None) == ERR_ALIGN                    # int64 positions
+    assert s(100, 10, None, 0, A, A + 64, None) == ERR_ALIAS                # snap inside theta
+    assert s(100, 10, C, 0, A, C + 8, None) == ERR_ALIAS                    # snap on the positions
+    a = L.ssn_sparta_average
+    cs = (P * 2)(A, B)
+    ds = (P * 2)(C, D)
+    w = (ctypes.c_float * 2)(1.0, 3.0)
+    assert a(0, 10, cs, None, F, ds, None) == ERR_SHAPE
+    assert a(65, 10, cs, None, F, ds, None) == ERR_SHAPE
+    assert a(2, 0, None, w, None, None, None) == OK
+    assert a(2, 10, cs, (ctypes.c_float * 2)(1.0, -1.0), F, ds, None) == ERR_SHAPE   # negative
+    assert a(2, 10, cs, (ctypes.c_float * 2)(0.0, 0.0), F, ds, None) == ERR_SHAPE    # zero sum
+    assert a(2, 10, cs, (ctypes.c_float * 2)(1.0, float("nan")), F, ds, None) == ERR_SHAPE
+    assert a(2, 10, (P * 2)(A, None), w, F, ds, None) == ERR_NULL
+    assert a(2, 10, cs, w, F + 2, ds, None) == ERR_ALIGN
+    assert a(2, 10, cs, w, A + 8, ds, None) == ERR_ALIAS                    # acc on a chunk
+    assert a(2, 10, cs, w, F, (P * 2)(C, B), None) == ERR_ALIAS             # delta on a chunk
+    assert a(2, 10, cs, w, F, (P * 2)(C, C + 8), None) == ERR_ALIAS         # deltas overlap
+    assert a(2, 10, cs, w, F, (P * 2)(F + 4, None), None) == ERR_ALIAS      # delta on acc
+    d = L.ssn_delta_rule
+    assert d(100, 0, None, 0, None, None, None, 1.0, None) == OK
+    assert d(100, 10, None, 91, A, B, C, 1.0, None) == ERR_SHAPE
+    assert d(100, 10, None, 0, A, B, C, float("inf"), None) == ERR_SHAPE    # lambda finite
+    assert d(100, 10, None, 0, A, None, C, 1.0, None) == ERR_NULL
+    assert d(100, 10, None, 0, A, B + 1, C, 1.0, None) == ERR_ALIGN
+    assert d(100, 10, None, 0, A, A + 40, C, 1.0, None) == ERR_ALIAS        # avg inside theta
+    assert d(100, 10, None, 0, A, B, A + 396, 1.0, None) == ERR_ALIAS       # snap overlaps theta's end
+
+
+def test_sparta_segments_tile_and_rotate(ssn):
+    """Host logic of the rotation: 20 contiguous segments tile [0, n) for any
+    n, sizes differ by at most one, and round r takes segment r mod 20."""
+    for n in (0, 1, 19, 20, 21, 1000, 320_000_003):
+        seen = 0
+        sizes = []
+        for r in range(ssn.SPARTA_SEGMENTS):
+            first, m = ssn.sparta_segment(n, r)
+            assert first == seen
+            seen += m
+            sizes.append(m)
+            assert ssn.sparta_segment(n, r + 3 * ssn.SPARTA_SEGMENTS) == (first, m)
+        assert seen == n
+        assert max(sizes) - min(sizes) <= 1
+
+
 def test_binding_refuses_cpu_tensors_and_missing_library(ssn, monkeypatch):
     import torch
     x = torch.zeros(4, 64, dtype=torch.bfloat16)
