@@ -74,6 +74,9 @@ def parse_args():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle baseline sample")
     p.add_argument("--tokens", type=int, default=0, help="override N (testing only)")
+    p.add_argument("--only", choices=("reparam", "sparta"), default=None,
+                   help="profiling aid: run only this section and print its JSON (no headline; "
+                        "keeps its kernels apart from the codec's in a kernel trace)")
     p.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                    help="before the timed region, run a plain device copy of MIB MiB three times "
                         "(a known-size kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -334,6 +337,28 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
     return out
 
 
+def copy_calibration(mib: int, dev):
+    """A plain device copy of known size, three times (scales rocprofv3's
+    FETCH_SIZE / WRITE_SIZE counters to bytes)."""
+    import torch
+    src = torch.empty(mib << 20, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def run_section(name: str, args, dev):
+    from paper_2607_13332_amd import inputs as I
+    if name == "reparam":
+        return {
+            "paper8b_mlp_out": time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2), dev),
+            "stage8b_mlp_out": time_reparam(32768, 14336, 4096, 64, max(10, args.steps // 2), dev),
+        }
+    return time_sparta(I.SPARTA_BLOCK8B, args.steps, dev)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -350,6 +375,12 @@ def main():
     ssn.lib()   # fail loudly if the HIP library is missing
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.only:
+        if args.copy_calib:
+            copy_calibration(args.copy_calib, dev)
+        print(json.dumps({"section": args.only, args.only: run_section(args.only, args, dev)}),
+              flush=True)
+        return
     cfg = I.STAGE8B if args.tokens == 0 else I.with_tokens(I.STAGE8B, args.tokens)
     N, d, k, V = cfg.N, cfg.d, cfg.k, cfg.V
 
@@ -389,12 +420,7 @@ def main():
             evs[4].record()
 
     if args.copy_calib:
-        src = torch.empty(args.copy_calib << 20, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_calibration(args.copy_calib, dev)
 
     for i in range(args.warmup):
         step(sets[i % 2])
@@ -518,14 +544,11 @@ def main():
 
     # ---------------- reparameterized-SSN projections (section 4.1, Eq. (3)) ----------------
     if not args.no_reparam:
-        result["reparam"] = {
-            "paper8b_mlp_out": time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2), dev),
-            "stage8b_mlp_out": time_reparam(32768, 14336, 4096, 64, max(10, args.steps // 2), dev),
-        }
+        result["reparam"] = run_section("reparam", args, dev)
 
     # ---------------- sparse averaging with the delta rule (section 4.2) ----------------
     if not args.no_sparta:
-        result["sparta"] = time_sparta(I.SPARTA_BLOCK8B, args.steps, dev)
+        result["sparta"] = run_section("sparta", args, dev)
 
     # ---------------- CPU baseline: the oracle on a bounded sample ----------------
     if not args.no_cpu_baseline:
