@@ -558,9 +558,8 @@ constexpr int kDecompressDC = 64;
 
 // KM: 0 when k == 32*KS2; 1 when k % 8 == 0 (16-byte rows of U and Z, zero
 // groups past k); 2 for any other k: Z is read element by element, and each
-// chunk of U (DC whole rows, one contiguous span of DC*k bf16 that starts
-// 16-byte aligned) is read with 16-byte loads and scattered element by
-// element into the zero-padded fragment layout.
+// U fragment (8 columns of one row, zero past k) is read as a 4-byte aligned
+// window and realigned in registers when it is stored to LDS.
 // GZ: the coordinate row of token t is Z[ids[t]] (a gathered table of
 // coordinates, e.g. the factored embedding E U^T of section 4.1) instead of
 // Z[t]; used without the additive embedding.
@@ -642,14 +641,17 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     srow[q] = 16 * (f / (KS2 * kWave)) + (l & 15);
     scol[q] = 32 * ((f / kWave) % KS2) + 8 * (l >> 4);
   }
-  u32x4 ust[FPT];
+  // U fragments travel as 16-byte pieces, or (KM == 2) as unaligned windows
+  // that are realigned when they are stored to LDS
+  using UReg = std::conditional_t<KM == 2, Bf16Window, u32x4>;
+  UReg ust[FPT];
   auto load_u = [&](int c) {
     if constexpr (KM == 2) {
-      // pieces of 8 consecutive elements of the chunk's span of DC*k
-      const uint16_t* span = U + (int64_t)c * DC * k;
+      // the fragment's 8 columns of one U row
 #pragma unroll
       for (int q = 0; q < FPT; ++q)
-        if (stid + PT * q < DC * k / 8) ust[q] = *(const u32x4*)(span + 8 * (stid + PT * q));
+        if (stid + PT * q < FR && scol[q] < k)
+          ust[q] = load_bf16_window(U, (int64_t)(c * DC + srow[q]) * k + scol[q], (int64_t)d * k);
     } else {
 #pragma unroll
       for (int q = 0; q < FPT; ++q)
@@ -660,40 +662,19 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     }
   };
   auto store_u = [&](int buf) {
-    if constexpr (KM == 2) {
-      // element (r, col) of the chunk -> fragment (r/16)*KS2 + col/32, lane
-      // position 16*((col%32)/8) + r%16, element col%8
-      uint16_t* dst = (uint16_t*)(ufr[buf] + spart * FR);
 #pragma unroll
-      for (int q = 0; q < FPT; ++q) {
-        const int p = stid + PT * q;
-        if (p < DC * k / 8) {
-          int r = (8 * p) / k, col = 8 * p - r * k;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int f = ((r >> 4) * KS2 + (col >> 5)) * kWave + 16 * ((col & 31) >> 3) + (r & 15);
-            const uint32_t w = ust[q][e >> 1];
-            dst[8 * f + (col & 7)] = (uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu));
-            if (++col == k) {
-              col = 0;
-              ++r;
-            }
-          }
-        }
+    for (int q = 0; q < FPT; ++q)
+      if (stid + PT * q < FR) {
+        if constexpr (KM == 2)
+          // chunks start at even rows and fragments at even columns, so row
+          // parity and k decide the alignment; zero past k
+          ufr[buf][spart * FR + stid + PT * q] =
+              scol[q] < k ? realign_bf16_window(ust[q], (srow[q] & k & 1) != 0, k - scol[q])
+                          : u32x4{0u, 0u, 0u, 0u};
+        else
+          ufr[buf][spart * FR + stid + PT * q] = ust[q];
       }
-    } else {
-#pragma unroll
-      for (int q = 0; q < FPT; ++q)
-        if (stid + PT * q < FR) ufr[buf][spart * FR + stid + PT * q] = ust[q];
-    }
   };
-  if constexpr (KM == 2) {
-    // the padding (columns k .. 32*KS2) is never written by the scatter: zero
-    // both buffers once
-    for (int i = tid; i < 2 * DSPLIT * FR; i += 64 * TW * DSPLIT)
-      (&ufr[0][0])[i] = u32x4{0u, 0u, 0u, 0u};
-    __syncthreads();
-  }
   u32x4 ering[PF + 1][NQ];
   auto load_e = [&](int c, u32x4(&eo)[NQ]) {
     if constexpr (HAS_E) {

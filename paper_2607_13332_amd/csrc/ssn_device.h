@@ -147,6 +147,54 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const uint16_t* p) {
   return __builtin_bit_cast(u32x2, v);
 }
 
+// Rows of k bf16 with k % 8 != 0 start only 2-byte aligned.  Eight
+// consecutive elements M[e0 .. e0 + 8) are read as the 4-byte aligned window
+// of ten elements that starts at e0 rounded down to even (one 16-byte and one
+// 4-byte load), and realigned in registers once the loads have landed, so
+// that the loads can run ahead of their use.  Within the last ten elements of
+// the buffer (`total` elements) the window is read element by element and
+// nothing past the end is touched.
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+struct Bf16Window {
+  u32x4 v;      // elements a0 .. a0 + 7
+  uint32_t x;   // elements a0 + 8, a0 + 9
+};
+__device__ __forceinline__ Bf16Window load_bf16_window(const uint16_t* __restrict__ M, int64_t e0,
+                                                       int64_t total) {
+  const int64_t a0 = e0 & ~(int64_t)1;
+  Bf16Window w;
+  if (a0 + 10 <= total) {
+    const uint32_t* p = (const uint32_t*)(M + a0);
+    w.v = *(const u32x4_a4*)p;
+    w.x = p[4];
+  } else {
+    uint32_t r[5];
+#pragma unroll
+    for (int i = 0; i < 5; ++i) {
+      const uint32_t lo = (a0 + 2 * i < total) ? (uint32_t)M[a0 + 2 * i] : 0u;
+      const uint32_t hi = (a0 + 2 * i + 1 < total) ? (uint32_t)M[a0 + 2 * i + 1] : 0u;
+      r[i] = lo | (hi << 16);
+    }
+    w.v = u32x4{r[0], r[1], r[2], r[3]};
+    w.x = r[4];
+  }
+  return w;
+}
+// The eight elements starting at e0 (odd: e0 is odd) out of a window loaded
+// by load_bf16_window; elements at positions >= nv (past the end of a matrix
+// row) become zero.
+__device__ __forceinline__ u32x4 realign_bf16_window(const Bf16Window& w, bool odd, int nv) {
+  const uint32_t sh = odd ? 16u : 0u;
+  uint32_t r[4] = {__builtin_amdgcn_alignbit(w.v[1], w.v[0], sh),
+                   __builtin_amdgcn_alignbit(w.v[2], w.v[1], sh),
+                   __builtin_amdgcn_alignbit(w.v[3], w.v[2], sh),
+                   __builtin_amdgcn_alignbit(w.x, w.v[3], sh)};
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    r[i] = (2 * i + 1 < nv) ? r[i] : ((2 * i < nv) ? (r[i] & 0xFFFFu) : 0u);
+  return u32x4{r[0], r[1], r[2], r[3]};
+}
+
 __device__ __forceinline__ int64_t clamp_id(int32_t id, int64_t V) {
   int64_t i = id;
   return i < 0 ? 0 : (i >= V ? V - 1 : i);
