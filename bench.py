@@ -275,6 +275,31 @@ def time_sparta(cfg, steps: int, dev):
     return out
 
 
+def time_step_graph(sets, step_fn, steps: int) -> float:
+    """ms per step when each input set's step is captured once as a HIP graph
+    and replayed (the library launches kernels only: no allocation, no
+    memset, so a whole step captures)."""
+    import torch
+    graphs = []
+    for s in sets:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step_fn(s)
+        graphs.append(g)
+    for g in graphs:
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        graphs[i % len(graphs)].replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    del graphs
+    return ms
+
+
 def time_codec_config(cfg, steps: int, warmup: int, dev):
     """The four codec ops of one microbatch on a workload other than the
     headline one (two alternating input sets, HIP events per op)."""
@@ -300,15 +325,20 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
     ops = ["decompress", "project_grad", "compress", "expand_grad"]
 
     def step(s, evs):
-        evs[0].record()
+        if evs:
+            evs[0].record()
         ssn.decompress(s["Zin"], s["ids"], E, U, out=s["Y"])
-        evs[1].record()
+        if evs:
+            evs[1].record()
         ssn.project_grad(s["G"], U, out=s["GZ"])
-        evs[2].record()
+        if evs:
+            evs[2].record()
         ssn.compress(s["X"], s["ids"], E, U, out=s["Z"])
-        evs[3].record()
+        if evs:
+            evs[3].record()
         ssn.expand_grad(s["GZin"], U, out=s["GX"])
-        evs[4].record()
+        if evs:
+            evs[4].record()
 
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
     for i in range(warmup):
@@ -327,10 +357,13 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         step_bytes += byts
         per_op[op] = {"ms": round(t, 5), "algorithmic_GBps": round(byts / (t * 1e-3) / 1e9, 1),
                       "frac_hbm_peak": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    gms = time_step_graph(sets, lambda s: step(s, None), steps)
     out = {"workload": f"N={N} (B={cfg.B} x S={cfg.S}), d={d}, k={k}, V={cfg.V}, bf16, "
                        f"{cfg.ids_dist} ids",
            "ms_per_step": round(ms, 5), "tokens_per_s": round(N / (ms * 1e-3), 1),
            "step_frac_hbm_peak": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "ms_per_step_hip_graph": round(gms, 5),
+           "tokens_per_s_hip_graph": round(N / (gms * 1e-3), 1),
            "per_op": per_op}
     del sets, base, U, E
     torch.cuda.empty_cache()
@@ -521,6 +554,10 @@ def main():
         "step_with_projected_compress": {"ms_per_step": round(ms2, 5),
                                          "tokens_per_s": round(N / (ms2 * 1e-3), 1)},
     }
+    gms = time_step_graph(sets, step, args.steps)
+    result["variants"]["step_hip_graph"] = {
+        "what": "the same four ops captured once per input set as a HIP graph and replayed",
+        "ms_per_step": round(gms, 5), "tokens_per_s": round(N / (gms * 1e-3), 1)}
     del P
 
     # ---------------- weight re-projection (once per optimizer step) ----------------
