@@ -353,25 +353,34 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
 // fragment feeds TTW token tiles).  Everything a wave
 // stages is wave-private (no block barrier until the end): its 16 X rows (and
 // 16 E[ids] rows) arrive as 8 rows x 128 contiguous bytes per load
-// instruction into an XOR-swizzled row tile, and its U rows arrive as
-// 16-byte row pieces (k % 8 == 0) or as 16-byte pieces of the chunk's
-// contiguous span scattered element-wise (any k) into a zero-padded
-// row-major tile.  A fragments are plain 16-byte LDS reads, U fragments come
+// instruction into an XOR-swizzled row tile, and its U rows arrive in a
+// padded row-major tile (zero past k).  UM selects how U is staged:
+//   0  k % 8 == 0: 16-byte cells of 8 columns;
+//   1  any k (rows start only 2-byte aligned): a cell is loaded as the
+//      16-byte window at its start rounded down to even; when it is parked
+//      the one missing element comes from the next lane's window (a
+//      cross-lane shuffle) and a funnel shift realigns it;
+//   2  any k: 16-byte pieces of the chunk's contiguous span, scattered
+//      element by element.
+// Mode 1 moves fewer LDS bytes but issues misaligned loads; which one is
+// faster depends on how many token tiles share each U chunk (measured).  A fragments are plain 16-byte LDS reads, U fragments come
 // from LDS transpose reads.  Two chunks are in flight in registers.  At the
 // end the P partial (X - E[ids]).U results meet in LDS and are summed in wave
 // order (deterministic); HAS_P subtracts the projected table rows instead of
 // accumulating E[ids].U.
 // ===========================================================================
-template <int KP, bool HAS_E, bool HAS_P, bool KV, int P, int TTW>
+template <int KP, bool HAS_E, bool HAS_P, int UM, int P, int TTW>
 __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) void compress_split_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ Pt) {
   static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
+  static_assert(UM >= 0 && UM <= 2, "U staging mode");
+  constexpr bool KV = (UM == 0);
   constexpr int DC = 64;                       // d per chunk (two K steps)
   constexpr int KW = 16 * KP;                  // U tile width
   constexpr int UP = KW + 8;                   // U tile pitch (bf16), rows 16-byte aligned
-  constexpr int NUL = (DC * KW / 8 + 63) / 64;  // U pieces per lane (the span of DC*k fits too)
+  constexpr int NUL = (DC * KW / 8 + 63) / 64;  // U row cells per lane
   constexpr int NXE = HAS_E ? 2 : 1;
   constexpr int R = 16 * TTW;                  // token rows of a wave
   constexpr int NXL = 2 * TTW;                 // X (and E) pieces per lane
@@ -403,8 +412,9 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
     xr[j] = X + t * d + 8 * (q % 8);
     er[j] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * (q % 8) : nullptr;
   }
-  if constexpr (!KV) {
-    // the scatter below never writes columns k .. KW
+
+  if constexpr (UM == 2) {
+    // the span scatter never writes columns k .. KW
     for (int i = lane; i < UT_BYTES / 16; i += 64) ((u32x4*)utw)[i] = u32x4{0u, 0u, 0u, 0u};
   }
 
@@ -420,13 +430,18 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
 #pragma unroll
     for (int i = 0; i < NUL; ++i) {
       const int q = lane + 64 * i;
-      if constexpr (KV) {
-        const int row = q / (KW / 8), cell = q % (KW / 8);
-        const bool ok = q < DC * KW / 8 && 8 * cell < k;
-        u[i] = ok ? *(const u32x4*)(U + (int64_t)(dcol + row) * k + 8 * cell) : u32x4{0u, 0u, 0u, 0u};
-      } else {
+      if constexpr (UM == 2) {
+        // 16-byte piece q of the chunk's contiguous span of DC*k elements
         const bool ok = q < DC * k / 8;
         u[i] = ok ? *(const u32x4*)(U + (int64_t)dcol * k + 8 * q) : u32x4{0u, 0u, 0u, 0u};
+      } else {
+        const int row = q / (KW / 8), cell = q % (KW / 8);
+        const bool ok = q < DC * KW / 8 && 8 * cell < k;
+        const int64_t e0 = (int64_t)(dcol + row) * k + 8 * cell;
+        if constexpr (KV)
+          u[i] = ok ? *(const u32x4*)(U + e0) : u32x4{0u, 0u, 0u, 0u};
+        else
+          u[i] = ok ? load_bf16x8_even(U, e0, (int64_t)d * k) : u32x4{0u, 0u, 0u, 0u};
       }
     }
   };
@@ -437,24 +452,33 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
       xtw[row * 8 + ((q % 8) ^ (row & 7))] = x[j];
       if constexpr (HAS_E) xtw[R * 8 + row * 8 + ((q % 8) ^ (row & 7))] = e[j];
     }
-#pragma clang loop unroll(full)
+#pragma unroll
     for (int i = 0; i < NUL; ++i) {
       const int q = lane + 64 * i;
-      if constexpr (KV) {
-        if (q < DC * KW / 8) {
-          const int row = q / (KW / 8), cell = q % (KW / 8);
-          *(u32x4*)(utw + row * UP + 8 * cell) = u[i];
+      if constexpr (UM == 2) {
+        // element by element from the span into the padded tile
+        if (q < DC * k / 8) {
+          const uint32_t w[4] = {u[i][0], u[i][1], u[i][2], u[i][3]};
+          int row = (8 * q) / k, col = 8 * q - row * k;
+#pragma unroll
+          for (int e2 = 0; e2 < 8; ++e2) {
+            utw[row * UP + col] = (uint16_t)((e2 & 1) ? (w[e2 >> 1] >> 16) : (w[e2 >> 1] & 0xFFFFu));
+            const bool wrap = (col + 1 == k);
+            col = wrap ? 0 : col + 1;
+            row = wrap ? row + 1 : row;
+          }
         }
-      } else if (q < DC * k / 8) {
-        const uint32_t w[4] = {u[i][0], u[i][1], u[i][2], u[i][3]};
-        int row = (8 * q) / k, col = 8 * q - row * k;
-#pragma clang loop unroll(full)
-        for (int e2 = 0; e2 < 8; ++e2) {
-          utw[row * UP + col] = (uint16_t)((e2 & 1) ? (w[e2 >> 1] >> 16) : (w[e2 >> 1] & 0xFFFFu));
-          const bool wrap = (col + 1 == k);
-          col = wrap ? 0 : col + 1;
-          row = wrap ? row + 1 : row;
+      } else {
+        const int row = q / (KW / 8), cell = q % (KW / 8);
+        u32x4 v = u[i];
+        if constexpr (UM == 1) {
+          // a row's cells sit in consecutive lanes, so the element after this
+          // cell's window starts the next lane's window; chunks start at even
+          // rows, so row parity and k decide the alignment
+          const uint32_t next = __shfl_down(u[i][0], 1);
+          v = realign_bf16x8(u[i], next, (row & k & 1) != 0, k - 8 * cell);
         }
+        if (q < DC * KW / 8) *(u32x4*)(utw + row * UP + 8 * cell) = v;
       }
     }
   };
@@ -893,14 +917,20 @@ static hipError_t launch_split_t(int64_t N, int d, int k, int64_t V, const void*
                                  const int32_t* ids, const void* E, const void* U, float* Z,
                                  const float* Pt, hipStream_t st) {
   const dim3 grid((unsigned)((N + 16 * TTW - 1) / (16 * TTW)));
-  if (k % 8 == 0)
-    hipLaunchKernelGGL((compress_split_bf16<KP, HAS_E, HAS_P, true, P, TTW>), grid, dim3(64 * P), 0,
-                       st, (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k,
-                       V, Pt);
-  else
-    hipLaunchKernelGGL((compress_split_bf16<KP, HAS_E, HAS_P, false, P, TTW>), grid, dim3(64 * P), 0,
-                       st, (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k,
-                       V, Pt);
+#define SSN_SPLIT(UM)                                                                           \
+  hipLaunchKernelGGL((compress_split_bf16<KP, HAS_E, HAS_P, UM, P, TTW>), grid, dim3(64 * P), 0, \
+                     st, (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d, \
+                     k, V, Pt)
+  // odd k (measured at d = 5120 and 18432, k = 51): the shuffled windows win
+  // when two token tiles share each U chunk, or with eight waves and d up to
+  // 8192; otherwise the span scatter
+  if (k % 8 == 0) SSN_SPLIT(0);
+  else if constexpr (TTW == 2) SSN_SPLIT(1);
+  else if constexpr (P == 8) {
+    if (d <= 8192) SSN_SPLIT(1);
+    else SSN_SPLIT(2);
+  } else SSN_SPLIT(2);
+#undef SSN_SPLIT
   return hipGetLastError();
 }
 

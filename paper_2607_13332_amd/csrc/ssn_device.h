@@ -195,6 +195,27 @@ __device__ __forceinline__ u32x4 realign_bf16_window(const Bf16Window& w, bool o
   return u32x4{r[0], r[1], r[2], r[3]};
 }
 
+// The 16-byte window M[a0 .. a0 + 8), a0 = e0 rounded down to even, of a
+// buffer of `total` elements (elements past the end read as zero).
+__device__ __forceinline__ u32x4 load_bf16x8_even(const uint16_t* __restrict__ M, int64_t e0,
+                                                  int64_t total) {
+  const int64_t a0 = e0 & ~(int64_t)1;
+  if (a0 + 8 <= total) return *(const u32x4_a4*)(M + a0);
+  uint32_t r[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = (a0 + 2 * i < total) ? (uint32_t)M[a0 + 2 * i] : 0u;
+    const uint32_t hi = (a0 + 2 * i + 1 < total) ? (uint32_t)M[a0 + 2 * i + 1] : 0u;
+    r[i] = lo | (hi << 16);
+  }
+  return u32x4{r[0], r[1], r[2], r[3]};
+}
+// Elements e0 .. e0 + 8 out of that window and the dword that follows it
+// (`next`: elements a0 + 8, a0 + 9), zero at positions >= nv.
+__device__ __forceinline__ u32x4 realign_bf16x8(u32x4 v, uint32_t next, bool odd, int nv) {
+  return realign_bf16_window(Bf16Window{v, next}, odd, nv);
+}
+
 __device__ __forceinline__ int64_t clamp_id(int32_t id, int64_t V) {
   int64_t i = id;
   return i < 0 ? 0 : (i >= V ? V - 1 : i);
