@@ -572,9 +572,9 @@ def main():
     # ---------------- the paper's own shapes ----------------
     if not args.no_paper_shapes:
         shapes = {}
-        for cfg in I.paper_configs():
-            if cfg.B in (1, 3):
-                shapes[cfg.name] = time_codec_config(cfg, max(10, args.steps // 2), args.warmup, dev)
+        for pc in I.paper_configs():
+            if pc.B in (1, 3):
+                shapes[pc.name] = time_codec_config(pc, max(10, args.steps // 2), args.warmup, dev)
         for wc in (I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B):
             shapes[wc.name] = time_weights(wc, args.steps, dev)
         result["paper_shapes"] = shapes

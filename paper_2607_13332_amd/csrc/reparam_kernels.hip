@@ -17,6 +17,7 @@ constexpr int kFgRows = 32;      // tokens per chunk (one K step)
 constexpr int kFgTiles = 32;     // 16-column tiles of din per block (512 columns)
 constexpr int kFgThreads = 512;  // 8 waves, four tiles each
 constexpr int kFgTargetBlocks = 256;
+constexpr int kFgDepth = 2;      // chunks in flight in registers (3 measured slower)
 
 // ===========================================================================
 // MFMA kernel, bf16 H.  Block (column block x, token split y) owns din
@@ -64,9 +65,11 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
   const bool hok = h < 2 * tcount;
   const uint16_t* hsrc = H + (t_begin + row0) * din + col0 + 8 * h;
 
-  // two register sets: chunk c travels in set c % 2
-  u32x4 hv[2][NHP];
-  float gv[2][NGQ][K4 ? 4 : 1];
+  // D register sets: chunk c travels in set c % D (two when k > 64, where
+  // three sets would not fit in registers)
+  constexpr int D = KT > 4 ? 2 : kFgDepth;
+  u32x4 hv[D][NHP];
+  float gv[D][NGQ][K4 ? 4 : 1];
   auto load = [&](int c, u32x4 (&hr)[NHP], float (&gr)[NGQ][K4 ? 4 : 1]) __attribute__((always_inline)) {
     const int64_t r0 = (int64_t)c * R;
 #pragma unroll
@@ -157,24 +160,27 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
   };
 
   __syncthreads();   // padding zeroed before the first park
-  // chunk 0 parked, chunks 1 and 2 in flight
+  // chunk 0 parked, chunks 1 .. D in flight
   if (nch > 0) {
     load(0, hv[0], gv[0]);
     park(0, hv[0], gv[0]);
-    if (nch > 1) load(1, hv[1], gv[1]);
-    if (nch > 2) load(2, hv[0], gv[0]);
+#pragma unroll
+    for (int j = 1; j <= D; ++j)
+      if (nch > j) load(j, hv[j % D], gv[j % D]);
   }
   __syncthreads();
   auto step = [&](int c, auto S) __attribute__((always_inline)) {
     constexpr int sl = decltype(S)::value;      // register set of chunk c + 1
     compute(c & 1);
     if (c + 1 < nch) park((c + 1) & 1, hv[sl], gv[sl]);
-    if (c + 3 < nch) load(c + 3, hv[sl], gv[sl]);
+    if (c + 1 + D < nch) load(c + 1 + D, hv[sl], gv[sl]);
     __syncthreads();
   };
-  for (int c = 0; c < nch; c += 2) {
-    step(c, std::integral_constant<int, 1>{});
-    if (c + 1 < nch) step(c + 1, std::integral_constant<int, 0>{});
+  for (int c = 0; c < nch; c += D) {
+    step(c, std::integral_constant<int, 1 % D>{});
+    if (c + 1 < nch) step(c + 1, std::integral_constant<int, 2 % D>{});
+    if constexpr (D == 3)
+      if (c + 2 < nch) step(c + 2, std::integral_constant<int, 0>{});
   }
 
   // lane (L, g) of tile (jl, i) holds dZp[col0 + 16 jl + 4g + e][16 i + L]
