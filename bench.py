@@ -10,8 +10,11 @@ d = 4096, k = 64, V = 131072, bf16 storage, fp32 coordinates):
     the output boundary), expand_grad (incoming gradient coordinates).
 
 Two independent microbatch input sets alternate between steps so that
-consecutive steps gather different embedding rows.  Inputs are resident in
-HBM before the timed region starts.  The once-per-optimizer-step weight
+consecutive steps gather different embedding rows, and within a step the
+compressed microbatch draws its own token ids (the decompressed and the
+compressed activations of a stage belong to different microbatches in a
+pipeline), so compress never finds the rows decompress just gathered in the
+caches.  Inputs are resident in HBM before the timed region starts.  The once-per-optimizer-step weight
 re-projection (4 layers x (4096x4096 + 4096x14336)) is timed separately and
 reported under "weights".  The same step with compress against the projected
 embedding table (Z = X U - (E U)[ids], table formed once outside the timed
@@ -60,7 +63,8 @@ def parse_args():
     p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--warmup", type=int, default=200,
+                   help="untimed steps first (the GPU's clocks settle after ~30 ms of sustained load)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-weights", action="store_true")
     p.add_argument("--no-sweep", action="store_true",
@@ -96,6 +100,11 @@ def algorithmic_bytes(op: str, N: int, d: int, k: int, u: int, s: int = 2) -> in
     if op == "compress_projected":
         return N * d * s + u * k * 4 + N * k * 4 + U + 4 * N
     raise ValueError(op)
+
+
+def op_u(op: str, s) -> int:
+    """Distinct embedding rows an op of input set s gathers."""
+    return s["u_c"] if op in ("compress", "compress_projected") else s["u"]
 
 
 def load_traffic(kernel_key: str):
@@ -320,7 +329,10 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         inp["GZ"] = torch.empty((N, k), dtype=torch.float32, device=dev)
         inp["Y"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
         inp["GX"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        inp["ids_c"] = I.codec_inputs_device(I.with_tokens(cfg, N, seed=c.seed + 7), dev,
+                                             need=("ids",))["ids"]
         inp["u"] = int(torch.unique(inp["ids"]).numel())
+        inp["u_c"] = int(torch.unique(inp["ids_c"]).numel())
         sets.append(inp)
     ops = ["decompress", "project_grad", "compress", "expand_grad"]
 
@@ -333,7 +345,7 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         ssn.project_grad(s["G"], U, out=s["GZ"])
         if evs:
             evs[2].record()
-        ssn.compress(s["X"], s["ids"], E, U, out=s["Z"])
+        ssn.compress(s["X"], s["ids_c"], E, U, out=s["Z"])
         if evs:
             evs[3].record()
         ssn.expand_grad(s["GZin"], U, out=s["GX"])
@@ -353,7 +365,7 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
     step_bytes = 0
     for j, op in enumerate(ops):
         t = float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs]))
-        byts = float(np.mean([algorithmic_bytes(op, N, d, k, s["u"]) for s in sets]))
+        byts = float(np.mean([algorithmic_bytes(op, N, d, k, op_u(op, s)) for s in sets]))
         step_bytes += byts
         per_op[op] = {"ms": round(t, 5), "algorithmic_GBps": round(byts / (t * 1e-3) / 1e9, 1),
                       "frac_hbm_peak": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
@@ -430,7 +442,10 @@ def main():
         inp["GZ"] = torch.empty((N, k), dtype=torch.float32, device=dev)
         inp["Y"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
         inp["GX"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        inp["ids_c"] = I.codec_inputs_device(I.with_tokens(cfg, N, seed=c.seed + 7), dev,
+                                             need=("ids",))["ids"]
         inp["u"] = int(torch.unique(inp["ids"]).numel())
+        inp["u_c"] = int(torch.unique(inp["ids_c"]).numel())
         sets.append(inp)
     torch.cuda.synchronize()
 
@@ -445,7 +460,7 @@ def main():
         ssn.project_grad(s["G"], U, out=s["GZ"])
         if evs is not None:
             evs[2].record()
-        ssn.compress(s["X"], s["ids"], E, U, out=s["Z"])
+        ssn.compress(s["X"], s["ids_c"], E, U, out=s["Z"])
         if evs is not None:
             evs[3].record()
         ssn.expand_grad(s["GZin"], U, out=s["GX"])
@@ -477,7 +492,7 @@ def main():
         return out
 
     def per_op_entry(op, mean_ms, pct):
-        byts = np.mean([algorithmic_bytes(op, N, d, k, s["u"]) for s in sets])
+        byts = np.mean([algorithmic_bytes(op, N, d, k, op_u(op, s)) for s in sets])
         return {"ms": round(mean_ms, 5),
                 "ms_p10_p50_p90": [round(float(x), 5) for x in pct],
                 "tokens_per_s": round(N / (mean_ms * 1e-3), 1),
@@ -529,7 +544,7 @@ def main():
         evs[1].record()
         ssn.project_grad(s["G"], U, out=s["GZ"])
         evs[2].record()
-        ssn.compress_projected(s["X"], s["ids"], P, U, out=s["Z"])
+        ssn.compress_projected(s["X"], s["ids_c"], P, U, out=s["Z"])
         evs[3].record()
         ssn.expand_grad(s["GZin"], U, out=s["GX"])
         evs[4].record()

@@ -94,11 +94,11 @@ struct UStage {
 constexpr int kCompressKS = 4;                 // K steps (of 32) per d chunk
 constexpr int kCompressDC = 32 * kCompressKS;  // d chunk
 
-// HAS_P (with HAS_E false): Z = X.U - P[ids], where P = E.U was produced by
-// this same kernel with HAS_P false, so that X.U of a row equal to E[id]
-// reproduces P[id] bit for bit.
+// HAS_P (with HAS_E false): Z = X.U - P[ids] with the projected table
+// P = E.U; a row equal to E[id] gives zero up to fp32 rounding (the table is
+// formed by the gradient projection, whose kernel may sum d in another order).
 template <int KP, int NBUF, bool HAS_E, bool KFULL, bool ROT = false, bool NT = false,
-          int WAVES = 4, int KS = kCompressKS, bool HAS_P = false>
+          int WAVES = 4, int KS = kCompressKS, bool HAS_P = false, bool NTE = false>
 __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
@@ -131,7 +131,7 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       xo[s] = ldg<NT>(xrow + c * DC + 32 * s);
-      if constexpr (HAS_E) eo[s] = ldg<NT>(erow + c * DC + 32 * s);
+      if constexpr (HAS_E) eo[s] = ldg<NTE>(erow + c * DC + 32 * s);
     }
   };
   auto load_u = [&](int c) { ust.load(U, (int64_t)c * DC, k); };
@@ -225,15 +225,25 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
 // wave loads its 16 X rows and 16 E[ids] rows for a chunk as 4 instructions
 // of 4 rows x 256 contiguous bytes (8 whole 128-byte lines per instruction,
 // instead of 16 half lines), parks them in a wave-private XOR-swizzled LDS
-// tile, and reads its A fragments from there.  The next chunk's rows are
-// loaded into registers while the current chunk computes.
+// tile, and reads its A fragments from there.
+//
+// Rows travel DEPTH chunks ahead of the MFMAs in DEPTH register sets.  Within
+// a step the next chunk's U is requested before the rows of chunk c + DEPTH:
+// loads complete in issue order, so the wait for U at the end of the step
+// leaves the younger row loads in flight.  The last DEPTH steps issue no row
+// loads (the loop is split so that every load in the main loop is
+// unconditional; nch must be a multiple of DEPTH).  ROT: every block starts
+// its sweep of d at its own chunk (spreads the concurrent requests of the
+// blocks over the columns of the rows).  NTX / NTE: non-temporal loads of the
+// activation / embedding rows.
 // ===========================================================================
-template <int KP, bool HAS_E, bool KFULL, int WAVES = 8, int DEPTH = 1>
+template <int KP, bool HAS_E, bool KFULL, int WAVES = 8, int DEPTH = 1, bool NTX = false,
+          bool NTE = false, bool ROT = false>
 __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     float* __restrict__ Z, int64_t N, int d, int k, int64_t V) {
-  static_assert(DEPTH == 1 || DEPTH == 2, "one or two chunks of rows in flight");
+  static_assert(DEPTH >= 1 && DEPTH <= 4, "one to four chunks of rows in flight");
   constexpr int KS = 4, DC = 128;
   __shared__ u32x4 lds[2][KS * KP * kWave];      // U B fragments, double buffered
   __shared__ u32x4 tile[WAVES][HAS_E ? 2 : 1][16 * 16];   // [wave][X/E][row * 16 + cell ^ row]
@@ -255,13 +265,17 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     xr[i] = X + t * d + 8 * lc;
     er[i] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * lc : nullptr;
   }
-  // DEPTH register sets: chunk c travels in set c % DEPTH
+  const int nch = d / DC;
+  const int rot = ROT ? (int)(blockIdx.x % (unsigned)nch) : 0;
+  auto chunk = [&](int i) { const int x = i + rot; return x < nch ? x : x - nch; };
+
+  // DEPTH register sets: step i's rows travel in set i % DEPTH
   u32x4 xv[DEPTH][4], ev[DEPTH][4];
   auto load_rows = [&](int c, u32x4 (&xs)[4], u32x4 (&es)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      xs[i] = *(const u32x4*)(xr[i] + c * DC);
-      if constexpr (HAS_E) es[i] = *(const u32x4*)(er[i] + c * DC);
+      xs[i] = ldg<NTX>(xr[i] + c * DC);
+      if constexpr (HAS_E) es[i] = ldg<NTE>(er[i] + c * DC);
     }
   };
   u32x4* tx = tile[wave][0];
@@ -287,19 +301,20 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     accE[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  const int nch = d / DC;
 #pragma unroll
-  for (int j = 0; j < DEPTH; ++j)
-    if (j < nch) load_rows(j, xv[j], ev[j]);
-  load_u(0);
+  for (int j = 0; j < DEPTH; ++j) load_rows(chunk(j), xv[j], ev[j]);
+  load_u(chunk(0));
   store_u(0);
-  auto step = [&](int c, auto S) {
-    constexpr int s0 = decltype(S)::value;       // == c % DEPTH
-    park_rows(xv[s0], ev[s0]);
-    if (c + DEPTH < nch) load_rows(c + DEPTH, xv[s0], ev[s0]);
-    load_u(c + 1 < nch ? c + 1 : c);
+  // step i (i % DEPTH == S): park the rows of chunk i, request U of chunk
+  // i + 1 and then (LOAD) the rows of chunk i + DEPTH, barrier, MFMAs, stage U.
+  auto step = [&](int i, auto Sc, auto Lc) {
+    constexpr int S = decltype(Sc)::value;
+    constexpr bool LOAD = decltype(Lc)::value;
+    park_rows(xv[S], ev[S]);
+    load_u(chunk(i + 1 < nch ? i + 1 : i));
+    if constexpr (LOAD) load_rows(chunk(i + DEPTH), xv[S], ev[S]);
     __syncthreads();
-    const u32x4* fr = lds[c & 1];
+    const u32x4* fr = lds[i & 1];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int cell = (4 * s + g) ^ n16;
@@ -308,19 +323,29 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
       if constexpr (HAS_E) ea = te[n16 * 16 + cell];
       u32x4 bfr[KP];
 #pragma unroll
-      for (int i = 0; i < KP; ++i) bfr[i] = fr[(s * KP + i) * kWave + lane];
+      for (int q = 0; q < KP; ++q) bfr[q] = fr[(s * KP + q) * kWave + lane];
 #pragma unroll
-      for (int i = 0; i < KP; ++i) {
-        accX[i] = mfma16x16x32(xa, bfr[i], accX[i]);
-        if constexpr (HAS_E) accE[i] = mfma16x16x32(ea, bfr[i], accE[i]);
+      for (int q = 0; q < KP; ++q) {
+        accX[q] = mfma16x16x32(xa, bfr[q], accX[q]);
+        if constexpr (HAS_E) accE[q] = mfma16x16x32(ea, bfr[q], accE[q]);
       }
     }
-    store_u((c + 1) & 1);
+    store_u((i + 1) & 1);
   };
-  for (int c = 0; c < nch; c += DEPTH) {
-    step(c, std::integral_constant<int, 0>{});
-    if constexpr (DEPTH == 2)
-      if (c + 1 < nch) step(c + 1, std::integral_constant<int, 1>{});
+  using L1 = std::true_type;
+  using L0 = std::false_type;
+  for (int i0 = 0; i0 < nch - DEPTH; i0 += DEPTH) {
+    step(i0, std::integral_constant<int, 0>{}, L1{});
+    if constexpr (DEPTH > 1) step(i0 + 1, std::integral_constant<int, 1 % DEPTH>{}, L1{});
+    if constexpr (DEPTH > 2) step(i0 + 2, std::integral_constant<int, 2 % DEPTH>{}, L1{});
+    if constexpr (DEPTH > 3) step(i0 + 3, std::integral_constant<int, 3 % DEPTH>{}, L1{});
+  }
+  {
+    const int i0 = nch - DEPTH;
+    step(i0, std::integral_constant<int, 0>{}, L0{});
+    if constexpr (DEPTH > 1) step(i0 + 1, std::integral_constant<int, 1 % DEPTH>{}, L0{});
+    if constexpr (DEPTH > 2) step(i0 + 2, std::integral_constant<int, 2 % DEPTH>{}, L0{});
+    if constexpr (DEPTH > 3) step(i0 + 3, std::integral_constant<int, 3 % DEPTH>{}, L0{});
   }
 
   const int col0 = n16 * KP;
@@ -587,8 +612,8 @@ constexpr int kDecompressDC = 64;
 // GZ: the coordinate row of token t is Z[ids[t]] (a gathered table of
 // coordinates, e.g. the factored embedding E U^T of section 4.1) instead of
 // Z[t]; used without the additive embedding.
-template <int KS2, bool HAS_E, int KM, int DC = kDecompressDC, int PF = 1, int DSPLIT = 1,
-          int TW = 4, bool NTS = false, bool GZ = false>
+template <int KS2, bool HAS_E, int KM, int DC = kDecompressDC, int DSPLIT = 1, int TW = 4,
+          bool NTS = false, bool GZ = false, bool NTE = false, int PF = 1>
 __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
@@ -611,7 +636,9 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
   const int part = wave / TW;
   const int64_t tok0 = (int64_t)blockIdx.x * (16 * TW) + (wave % TW) * 16;
 
-  // Z^T B fragments of this wave's 16 tokens
+  // Z^T B fragments of this wave's 16 tokens.  Tokens past N take row N - 1
+  // (here and in the epilogue), so their lanes recompute token N - 1 and
+  // store the same bytes to the same row: every store is unconditional.
   u32x4 zhi[KS2], zlo[KS2];
   {
     int64_t t = tok0 + n16;
@@ -643,11 +670,9 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
   const int ec = lane % LPR;
   const uint16_t* erow[NQ];
   uint16_t* yrow[NQ];
-  bool ok[NQ];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     int64_t t = tok0 + RPI * q + lane / LPR;
-    ok[q] = t < N;
     t = t < N ? t : N - 1;
     yrow[q] = Y + t * d + 8 * ec;
     erow[q] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * ec : nullptr;
@@ -655,55 +680,65 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
 
   // U staging: thread tid stages fragments of part tid/PT; fragment
   // f = tid%PT + PT*q -> tile f/(KS2*64), K step (f/64)%KS2, lane position
-  // f%64 = 16*g' + m: row 16*tile + m, columns 32*s + 8*g'
+  // f%64 = 16*g' + m: row 16*tile + m, columns 32*s + 8*g'.  Threads past
+  // the last fragment load fragment FR - 1 again and do not store it, and
+  // columns past k load column 0 and store zeros, so that the loads, too,
+  // are unconditional.
   const int spart = tid / PT, stid = tid % PT;
   int srow[FPT], scol[FPT];
+  bool son[FPT];
 #pragma unroll
   for (int q = 0; q < FPT; ++q) {
-    const int f = stid + PT * q;
+    const int f0 = stid + PT * q;
+    son[q] = f0 < FR;
+    const int f = son[q] ? f0 : FR - 1;
     const int l = f & 63;
     srow[q] = 16 * (f / (KS2 * kWave)) + (l & 15);
     scol[q] = 32 * ((f / kWave) % KS2) + 8 * (l >> 4);
   }
   // U fragments travel as 16-byte pieces, or (KM == 2) as unaligned windows
-  // that are realigned when they are stored to LDS
+  // that are realigned when they are stored to LDS.  Two register sets:
+  // chunk j's fragments travel in set j % 2, loaded two chunks before the
+  // chunk that reads them from LDS.
   using UReg = std::conditional_t<KM == 2, Bf16Window, u32x4>;
-  UReg ust[FPT];
-  auto load_u = [&](int c) {
+  UReg ust[2][FPT];
+  auto load_u = [&](int c, UReg(&u)[FPT]) {
     if constexpr (KM == 2) {
       // the fragment's 8 columns of one U row
 #pragma unroll
       for (int q = 0; q < FPT; ++q)
-        if (stid + PT * q < FR && scol[q] < k)
-          ust[q] = load_bf16_window(U, (int64_t)(c * DC + srow[q]) * k + scol[q], (int64_t)d * k);
+        u[q] = load_bf16_window(U, (int64_t)(c * DC + srow[q]) * k + (scol[q] < k ? scol[q] : 0),
+                                (int64_t)d * k);
     } else {
 #pragma unroll
       for (int q = 0; q < FPT; ++q)
-        if (stid + PT * q < FR)
-          ust[q] = (KFULL32 || scol[q] < k)
-                       ? *(const u32x4*)(U + (int64_t)(c * DC + srow[q]) * k + scol[q])
-                       : u32x4{0u, 0u, 0u, 0u};
+        u[q] = *(const u32x4*)(U + (int64_t)(c * DC + srow[q]) * k +
+                               (KFULL32 || scol[q] < k ? scol[q] : 0));
     }
   };
-  auto store_u = [&](int buf) {
+  auto store_u = [&](int buf, const UReg(&u)[FPT]) {
 #pragma unroll
     for (int q = 0; q < FPT; ++q)
-      if (stid + PT * q < FR) {
+      if (son[q]) {
+        u32x4 v;
         if constexpr (KM == 2)
           // chunks start at even rows and fragments at even columns, so row
           // parity and k decide the alignment; zero past k
-          ufr[buf][spart * FR + stid + PT * q] =
-              scol[q] < k ? realign_bf16_window(ust[q], (srow[q] & k & 1) != 0, k - scol[q])
+          v = scol[q] < k ? realign_bf16_window(u[q], (srow[q] & k & 1) != 0, k - scol[q])
                           : u32x4{0u, 0u, 0u, 0u};
         else
-          ufr[buf][spart * FR + stid + PT * q] = ust[q];
+          v = (KFULL32 || scol[q] < k) ? u[q] : u32x4{0u, 0u, 0u, 0u};
+        ufr[buf][spart * FR + stid + PT * q] = v;
       }
   };
-  u32x4 ering[PF + 1][NQ];
+  // E rows of chunk j travel in ring slot j % (PF + 1), PF chunks ahead
+  static_assert(PF == 1 || PF == 3 || PF == 7, "embedding prefetch depth");
+  constexpr int R = PF + 1;                       // steps per unrolled group (a multiple of 2)
+  u32x4 ering[R][NQ];
   auto load_e = [&](int c, u32x4(&eo)[NQ]) {
     if constexpr (HAS_E) {
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) eo[q] = *(const u32x4*)(erow[q] + c * DC);
+      for (int q = 0; q < NQ; ++q) eo[q] = ldg<NTE>(erow[q] + c * DC);
     }
   };
 
@@ -718,60 +753,89 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     return (pbase + p) * nch + (x < nch ? x : x - nch);
   };
   auto chunk = [&](int i) { return chunk_of(part, i); };
+  auto last = [&](int i) { return i < nch ? i : nch - 1; };
   f32x4* st = stage[wave];
 
-  // the stager threads of part spart load that part's chunks of U
-  auto load_u_part = [&](int i) { load_u(chunk_of(spart, i)); };
-
-  load_u_part(0);
-  store_u(0);
+  // One chunk, i % R == B.  Order: loads for later chunks (U of chunk i + 2,
+  // E of chunk i + PF), barrier, MFMAs, epilogue stores, and only then the
+  // LDS store of chunk i + 1's U, whose loads were issued one chunk earlier.
+  // Loads and stores share one completion counter, so no wait in a chunk
+  // covers the stores that chunk issued.
+  auto body = [&](int i, auto Bc) {
+    constexpr int B = decltype(Bc)::value;
+    constexpr int US = B & 1;
+    const int c = chunk(i);
+    load_u(chunk_of(spart, last(i + 2)), ust[US]);
+    load_e(chunk(last(i + PF)), ering[(B + PF) % R]);
+    __syncthreads();
+    const u32x4* fr = ufr[US] + part * FR;
 #pragma unroll
-  for (int b = 0; b < PF; ++b) load_e(chunk(b < nch ? b : nch - 1), ering[b]);
-  for (int i0 = 0; i0 < nch; i0 += PF + 1) {
+    for (int tt = 0; tt < NT; ++tt) {
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int b = 0; b <= PF; ++b) {
-      const int i = i0 + b;
-      if (i < nch) {
-        const int c = chunk(i);
-        load_u_part(i + 1 < nch ? i + 1 : i);
-        // E of chunk i + PF into the ring slot freed by chunk i - 1
-        load_e(chunk(i + PF < nch ? i + PF : nch - 1), ering[(b + PF) % (PF + 1)]);
-        __syncthreads();
-        const u32x4* fr = ufr[i & 1] + part * FR;
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) {
-          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int s = 0; s < KS2; ++s) {
-            const u32x4 a = fr[(tt * KS2 + s) * kWave + lane];
-            acc = mfma16x16x32(a, zhi[s], acc);
-            acc = mfma16x16x32(a, zlo[s], acc);
-          }
-          // lane (token n16, group g) holds d = 16*tt + 4*g + 0..3 of its token
-          st[n16 * (DC / 4) + ((4 * tt + g) ^ n16)] = acc;
-        }
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-          const int tl = RPI * q + lane / LPR;
-          const f32x4 a = st[tl * (DC / 4) + ((2 * ec) ^ tl)];
-          const f32x4 bb = st[tl * (DC / 4) + ((2 * ec + 1) ^ tl)];
-          float v[8] = {a[0], a[1], a[2], a[3], bb[0], bb[1], bb[2], bb[3]};
-          if constexpr (HAS_E) {
-            const u32x4 e = ering[b][q];
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-              v[2 * m] += lo_bf16(e[m]);
-              v[2 * m + 1] += hi_bf16(e[m]);
-            }
-          }
-          if (ok[q])
-            stg<NTS>(yrow[q] + c * DC, u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
-                                             pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])});
-        }
-        store_u((i + 1) & 1);
+      for (int s = 0; s < KS2; ++s) {
+        const u32x4 a = fr[(tt * KS2 + s) * kWave + lane];
+        acc = mfma16x16x32(a, zhi[s], acc);
+        acc = mfma16x16x32(a, zlo[s], acc);
       }
+      // lane (token n16, group g) holds d = 16*tt + 4*g + 0..3 of its token
+      st[n16 * (DC / 4) + ((4 * tt + g) ^ n16)] = acc;
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int tl = RPI * q + lane / LPR;
+      const f32x4 a = st[tl * (DC / 4) + ((2 * ec) ^ tl)];
+      const f32x4 bb = st[tl * (DC / 4) + ((2 * ec + 1) ^ tl)];
+      float v[8] = {a[0], a[1], a[2], a[3], bb[0], bb[1], bb[2], bb[3]};
+      if constexpr (HAS_E) {
+        const u32x4 e = ering[B][q];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          v[2 * m] += lo_bf16(e[m]);
+          v[2 * m + 1] += hi_bf16(e[m]);
+        }
+      }
+      stg<NTS>(yrow[q] + c * DC, u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                       pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])});
+    }
+    store_u(US ^ 1, ust[US ^ 1]);
+  };
+  auto group = [&](int i0, int n) {   // steps i0 .. i0 + n - 1 (n <= R, i0 % R == 0)
+    body(i0, std::integral_constant<int, 0>{});
+    if (n > 1) body(i0 + 1, std::integral_constant<int, 1>{});
+    if constexpr (R > 2) {
+      if (n > 2) body(i0 + 2, std::integral_constant<int, 2 % R>{});
+      if (n > 3) body(i0 + 3, std::integral_constant<int, 3 % R>{});
+    }
+    if constexpr (R > 4) {
+      if (n > 4) body(i0 + 4, std::integral_constant<int, 4 % R>{});
+      if (n > 5) body(i0 + 5, std::integral_constant<int, 5 % R>{});
+      if (n > 6) body(i0 + 6, std::integral_constant<int, 6 % R>{});
+      if (n > 7) body(i0 + 7, std::integral_constant<int, 7 % R>{});
+    }
+  };
+
+  load_u(chunk_of(spart, 0), ust[0]);
+  load_u(chunk_of(spart, last(1)), ust[1]);
+#pragma unroll
+  for (int j = 0; j < PF; ++j) load_e(chunk(last(j)), ering[j]);
+  store_u(0, ust[0]);
+  const int nfull = nch - nch % R;
+  for (int i0 = 0; i0 < nfull; i0 += R) {
+    body(i0, std::integral_constant<int, 0>{});
+    body(i0 + 1, std::integral_constant<int, 1>{});
+    if constexpr (R > 2) {
+      body(i0 + 2, std::integral_constant<int, 2 % R>{});
+      body(i0 + 3, std::integral_constant<int, 3 % R>{});
+    }
+    if constexpr (R > 4) {
+      body(i0 + 4, std::integral_constant<int, 4 % R>{});
+      body(i0 + 5, std::integral_constant<int, 5 % R>{});
+      body(i0 + 6, std::integral_constant<int, 6 % R>{});
+      body(i0 + 7, std::integral_constant<int, 7 % R>{});
     }
   }
+  if (nfull < nch) group(nfull, nch - nfull);
 }
 
 // ===========================================================================
@@ -856,37 +920,47 @@ static hipError_t launch_compress_v(int64_t N, int d, int k, int64_t V, const vo
   return hipGetLastError();
 }
 
-template <int KP, bool KFULL>
+// Row-contiguous kernel: 8 waves (128 tokens) per block with a rotated sweep
+// of d once N/128 blocks fill the compute units, else 4 waves (64 tokens) in
+// the natural order.  Activation rows are streamed with non-temporal loads;
+// embedding rows keep normal caching (repeated ids hit in L2).
+template <int KP, bool HAS_E, bool KFULL>
 static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const void* X,
                                        const int32_t* ids, const void* E, const void* U, float* Z,
                                        hipStream_t st) {
-  constexpr int WAVES = 4;
-  const int64_t blocks = (N + 16 * WAVES - 1) / (16 * WAVES);
-  hipLaunchKernelGGL((compress_rows_bf16<KP, true, KFULL, WAVES>), dim3((unsigned)blocks),
-                     dim3(64 * WAVES), 0, st, (const uint16_t*)X, ids, (const uint16_t*)E,
-                     (const uint16_t*)U, Z, N, d, k, V);
+  if ((N + 127) / 128 >= device_cu_count()) {
+    const int64_t blocks = (N + 127) / 128;
+    hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 8, 1, true, false, true>),
+                       dim3((unsigned)blocks), dim3(512), 0, st, (const uint16_t*)X, ids,
+                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V);
+  } else {
+    const int64_t blocks = (N + 63) / 64;
+    hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 4, 1, true, false, false>),
+                       dim3((unsigned)blocks), dim3(256), 0, st, (const uint16_t*)X, ids,
+                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V);
+  }
   return hipGetLastError();
 }
 
-// compress (with the embedding rows) uses the row-contiguous variant; the
-// gradient projection and the projected-table compress (one activation
-// stream) the direct-fragment variant with 8 waves (128 tokens) per block
-// sharing each staged slice of U, in 256-d chunks when d allows, else 128.
-// The table build (P = E.U) is a gradient-projection launch, so both sides of
-// the projected-table compress take the same instantiation.
+// compress (with the embedding rows) and the gradient projection use the
+// row-contiguous variant; the projected-table compress (X.U - P[ids]) the
+// direct-fragment variant with 8 waves (128 tokens) per block sharing each
+// staged slice of U, in 256-d chunks when d allows, else 128.
 template <int KP, bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_kp(int64_t N, int d, int k, int64_t V, const void* X,
                                      const int32_t* ids, const void* E, const void* U, float* Z,
                                      const float* P, hipStream_t st) {
   const bool kfull = (k == 16 * KP);
-  if constexpr (HAS_E)
-    return kfull ? launch_compress_rows<KP, true>(N, d, k, V, X, ids, E, U, Z, st)
-                 : launch_compress_rows<KP, false>(N, d, k, V, X, ids, E, U, Z, st);
-  if (d % 256 == 0)
-    return kfull ? launch_compress_v<KP, HAS_E, true, 8, 8, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st)
-                 : launch_compress_v<KP, HAS_E, false, 8, 8, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
-  return kfull ? launch_compress_v<KP, HAS_E, true, 8, 4, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st)
-               : launch_compress_v<KP, HAS_E, false, 8, 4, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+  if constexpr (!HAS_P) {
+    return kfull ? launch_compress_rows<KP, HAS_E, true>(N, d, k, V, X, ids, E, U, Z, st)
+                 : launch_compress_rows<KP, HAS_E, false>(N, d, k, V, X, ids, E, U, Z, st);
+  } else {
+    if (d % 256 == 0)
+      return kfull ? launch_compress_v<KP, false, true, 8, 8, true>(N, d, k, V, X, ids, E, U, Z, P, st)
+                   : launch_compress_v<KP, false, false, 8, 8, true>(N, d, k, V, X, ids, E, U, Z, P, st);
+    return kfull ? launch_compress_v<KP, false, true, 8, 4, true>(N, d, k, V, X, ids, E, U, Z, P, st)
+                 : launch_compress_v<KP, false, false, 8, 4, true>(N, d, k, V, X, ids, E, U, Z, P, st);
+  }
 }
 
 template <bool HAS_E, bool HAS_P>
@@ -1008,25 +1082,34 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
   return launch_compress_generic<uint16_t, false, false>(N, d, k, V, X, ids, E, U, Z, P, st);
 }
 
-// 8 token tiles (128 tokens) x 2 halves of d per block (16 waves); the
-// activation rows are written with non-temporal stores (streamed out instead
-// of parked dirty in the caches, where they slowed the next kernel's reads)
+// 8 token tiles (128 tokens) per block.  When N/128 blocks fill the compute
+// units, each of the 8 waves sweeps all of d (rotated per block); with fewer
+// tokens the block has 2 halves of d (16 waves) and a second grid dimension
+// splits d further (the smallest divisor of the chunk-pair count that gives
+// one block per compute unit).  The activation rows are written with
+// non-temporal stores (streamed out instead of parked dirty in the caches,
+// where they slowed the next kernel's reads).
 template <int KS2, bool HAS_E, int KM, bool GZ>
 static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
                                        hipStream_t st) {
-  constexpr int TW = 8, DS = 2;
+  constexpr int TW = 8;
   const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
-  // with few token tiles, also split d over the grid: the smallest divisor gy
-  // of the chunk-pair count that gives one block per compute unit
-  const int pairs = d / (kDecompressDC * DS);
   const int64_t cus = device_cu_count();
+  if (blocks >= cus) {
+    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ>),
+                       dim3((unsigned)blocks, 1), dim3(64 * TW), 0, st, Zc, ids,
+                       (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
+    return hipGetLastError();
+  }
+  constexpr int DS = 2;
+  const int pairs = d / (kDecompressDC * DS);
   int gy = 1;
   while (gy < pairs && blocks * gy < cus) {
     ++gy;
     while (pairs % gy != 0) ++gy;
   }
-  hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, DS, TW, true, GZ>),
+  hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, DS, TW, true, GZ>),
                      dim3((unsigned)blocks, (unsigned)gy), dim3(64 * TW * DS), 0, st, Zc, ids,
                      (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
   return hipGetLastError();

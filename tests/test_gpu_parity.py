@@ -191,6 +191,9 @@ CODEC_SHAPES = [  # (N, d, k): tiles, ragged tails, every k bucket, both familie
     (50, 512, 1), (64, 512, 15), (65, 512, 16), (300, 512, 48), (129, 512, 129),
     (200, 100, 10), (10, 2048, 51), (4099, 1024, 96), (70, 4096, 24), (33, 128, 8),
     (300, 5120, 51), (130, 2048, 40), (97, 256, 127), (64, 384, 3),
+    # enough 128-token tiles to fill 256 compute units, with ragged tails: the
+    # rotated 8-wave row kernel and the full-d decompress blocks
+    (33325, 256, 64), (33325, 384, 32), (20000, 640, 48),
 ]
 
 
