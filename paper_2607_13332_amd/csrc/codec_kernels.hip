@@ -238,7 +238,7 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
 // activation / embedding rows.
 // ===========================================================================
 template <int KP, bool HAS_E, bool KFULL, int WAVES = 8, int DEPTH = 1, bool NTX = false,
-          bool NTE = false, bool ROT = false>
+          bool NTE = false, bool ROT = false, int ROTG = 1>
 __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
@@ -266,7 +266,9 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     er[i] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * lc : nullptr;
   }
   const int nch = d / DC;
-  const int rot = ROT ? (int)(blockIdx.x % (unsigned)nch) : 0;
+  // rotation in units of ROTG chunks (when they divide nch)
+  const int rg = (ROTG > 1 && nch % ROTG == 0) ? ROTG : 1;
+  const int rot = ROT ? (int)(blockIdx.x % (unsigned)(nch / rg)) * rg : 0;
   auto chunk = [&](int i) { const int x = i + rot; return x < nch ? x : x - nch; };
 
   // DEPTH register sets: step i's rows travel in set i % DEPTH
@@ -613,7 +615,8 @@ constexpr int kDecompressDC = 64;
 // coordinates, e.g. the factored embedding E U^T of section 4.1) instead of
 // Z[t]; used without the additive embedding.
 template <int KS2, bool HAS_E, int KM, int DC = kDecompressDC, int DSPLIT = 1, int TW = 4,
-          bool NTS = false, bool GZ = false, bool NTE = false, int PF = 1>
+          bool NTS = false, bool GZ = false, bool NTE = false, int PF = 1, int SG = 1,
+          int ROTG = 1>
 __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
@@ -731,10 +734,15 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
         ufr[buf][spart * FR + stid + PT * q] = v;
       }
   };
-  // E rows of chunk j travel in ring slot j % (PF + 1), PF chunks ahead
+  // E rows of chunk j travel in ring slot j % (PF + 1), PF chunks ahead.
+  // SG > 1: the packed outputs of SG consecutive chunks are kept in
+  // registers and stored together (SG * DC * 2 contiguous bytes per row);
+  // then nch must be a multiple of R.
   static_assert(PF == 1 || PF == 3 || PF == 7, "embedding prefetch depth");
-  constexpr int R = PF + 1;                       // steps per unrolled group (a multiple of 2)
-  u32x4 ering[R][NQ];
+  static_assert(SG == 1 || SG == 2 || SG == 4 || SG == 8, "store group");
+  constexpr int R = (PF + 1) > SG ? (PF + 1) : SG;   // steps per unrolled group
+  u32x4 ering[PF + 1][NQ];
+  u32x4 ypk[SG][NQ];
   auto load_e = [&](int c, u32x4(&eo)[NQ]) {
     if constexpr (HAS_E) {
 #pragma unroll
@@ -746,7 +754,9 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
   // there are few tokens); part p of the block walks chunks
   // [(y*DSPLIT + p)*nch, +nch) of that range, rotated per block
   const int nch = d / (DC * DSPLIT * (int)gridDim.y);
-  const int rot = (int)(blockIdx.x % (unsigned)nch);
+  // rotation in units of ROTG chunks (when they divide nch)
+  const int rg = (ROTG > 1 && nch % ROTG == 0) ? ROTG : 1;
+  const int rot = (int)(blockIdx.x % (unsigned)(nch / rg)) * rg;
   const int pbase = (int)blockIdx.y * DSPLIT;
   auto chunk_of = [&](int p, int i) {
     const int x = i + rot;
@@ -766,7 +776,7 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     constexpr int US = B & 1;
     const int c = chunk(i);
     load_u(chunk_of(spart, last(i + 2)), ust[US]);
-    load_e(chunk(last(i + PF)), ering[(B + PF) % R]);
+    load_e(chunk(last(i + PF)), ering[(B + PF) % (PF + 1)]);
     __syncthreads();
     const u32x4* fr = ufr[US] + part * FR;
 #pragma unroll
@@ -788,19 +798,29 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
       const f32x4 bb = st[tl * (DC / 4) + ((2 * ec + 1) ^ tl)];
       float v[8] = {a[0], a[1], a[2], a[3], bb[0], bb[1], bb[2], bb[3]};
       if constexpr (HAS_E) {
-        const u32x4 e = ering[B][q];
+        const u32x4 e = ering[B % (PF + 1)][q];
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
           v[2 * m] += lo_bf16(e[m]);
           v[2 * m + 1] += hi_bf16(e[m]);
         }
       }
-      stg<NTS>(yrow[q] + c * DC, u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
-                                       pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])});
+      const u32x4 y = u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                            pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+      if constexpr (SG == 1) stg<NTS>(yrow[q] + c * DC, y);
+      else ypk[B % SG][q] = y;
+    }
+    if constexpr (SG > 1 && B % SG == SG - 1) {
+#pragma unroll
+      for (int j = 0; j < SG; ++j) {
+        const int cj = chunk(i - (SG - 1) + j);
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) stg<NTS>(yrow[q] + cj * DC, ypk[j][q]);
+      }
     }
     store_u(US ^ 1, ust[US ^ 1]);
   };
-  auto group = [&](int i0, int n) {   // steps i0 .. i0 + n - 1 (n <= R, i0 % R == 0)
+  auto group = [&](int i0, int n) {   // steps i0 .. i0 + n - 1 (n < R, i0 % R == 0, SG == 1)
     body(i0, std::integral_constant<int, 0>{});
     if (n > 1) body(i0 + 1, std::integral_constant<int, 1>{});
     if constexpr (R > 2) {
@@ -811,7 +831,6 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
       if (n > 4) body(i0 + 4, std::integral_constant<int, 4 % R>{});
       if (n > 5) body(i0 + 5, std::integral_constant<int, 5 % R>{});
       if (n > 6) body(i0 + 6, std::integral_constant<int, 6 % R>{});
-      if (n > 7) body(i0 + 7, std::integral_constant<int, 7 % R>{});
     }
   };
 
@@ -835,7 +854,9 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
       body(i0 + 7, std::integral_constant<int, 7 % R>{});
     }
   }
-  if (nfull < nch) group(nfull, nch - nfull);
+  if constexpr (SG == 1) {
+    if (nfull < nch) group(nfull, nch - nfull);
+  }
 }
 
 // ===========================================================================
@@ -922,15 +943,18 @@ static hipError_t launch_compress_v(int64_t N, int d, int k, int64_t V, const vo
 
 // Row-contiguous kernel: 8 waves (128 tokens) per block with a rotated sweep
 // of d once N/128 blocks fill the compute units, else 4 waves (64 tokens) in
-// the natural order.  Activation rows are streamed with non-temporal loads;
-// embedding rows keep normal caching (repeated ids hit in L2).
+// the natural order.  The rotation moves in steps of 4 chunks (1 KB of a bf16
+// row): on MI355X, start offsets in 256- or 512-byte steps let the blocks'
+// concurrent requests collide (measured 1.1-1.8x slower at d = 4096).
+// Activation rows are streamed with non-temporal loads; embedding rows keep
+// normal caching (repeated ids hit in L2).
 template <int KP, bool HAS_E, bool KFULL>
 static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const void* X,
                                        const int32_t* ids, const void* E, const void* U, float* Z,
                                        hipStream_t st) {
   if ((N + 127) / 128 >= device_cu_count()) {
     const int64_t blocks = (N + 127) / 128;
-    hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 8, 1, true, false, true>),
+    hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 8, 1, true, false, true, 4>),
                        dim3((unsigned)blocks), dim3(512), 0, st, (const uint16_t*)X, ids,
                        (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V);
   } else {
@@ -1083,7 +1107,9 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
 }
 
 // 8 token tiles (128 tokens) per block.  When N/128 blocks fill the compute
-// units, each of the 8 waves sweeps all of d (rotated per block); with fewer
+// units, each of the 8 waves sweeps all of d (rotated per block, in steps of
+// one chunk); the gradient expansion (no embedding rows to gather) then
+// stores two chunks at a time (256 contiguous bytes per row).  With fewer
 // tokens the block has 2 halves of d (16 waves) and a second grid dimension
 // splits d further (the smallest divisor of the chunk-pair count that gives
 // one block per compute unit).  The activation rows are written with
@@ -1097,7 +1123,10 @@ static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const
   const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
   const int64_t cus = device_cu_count();
   if (blocks >= cus) {
-    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ>),
+    // d % 128 == 0, so the chunk count d / 64 is even (store groups of two)
+    constexpr int SG = HAS_E ? 1 : 2;
+    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ, false,
+                                             1, SG>),
                        dim3((unsigned)blocks, 1), dim3(64 * TW), 0, st, Zc, ids,
                        (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
     return hipGetLastError();
