@@ -241,7 +241,18 @@ constexpr int cols_max_waves(int kt, bool kv, int ct) { return (kt > 4 || !kv ||
 // U (64 whole rows, one contiguous span of 64*k bf16 that starts 16-byte
 // aligned) is read with 16-byte loads and scattered element by element into
 // the zero-padded row tile.
-template <int KT, bool NTS, int DEPTH, bool KV, int CT = 2>
+// NTL: W is read with non-temporal loads (each piece is read once and then
+// overwritten by pass 2).  The 128-byte lines at the boundary of two strips
+// are fetched by both blocks, and a streamed line is not kept for the
+// neighbour, so streaming pays only while few lines are shared (measured on
+// MI355X: 4 x (4096^2, 4096 x 14336), k = 64, 576-byte strips: 224 -> 202 us;
+// 288-byte strips at d = 2048 and 736-byte strips at k = 51: slower).
+// XCD: blocks are dispatched to the 8 XCDs round robin (block b on XCD
+// b mod 8); with XCD the block of launch index b takes strip
+// (b mod 8) * (grid / 8) + b / 8, so that neighbouring strips, which share
+// the 128-byte lines at their boundary, run on the same XCD and share its L2
+// (needs grid % 8 == 0).
+template <int KT, bool NTS, int DEPTH, bool KV, int CT = 2, bool NTL = false, bool XCD = false>
 __global__ __launch_bounds__(kWave * cols_max_waves(KT, KV, CT)) void project_weights_cols_bf16(
     ColumnBatch cb, const uint16_t* __restrict__ U, int d, int k) {
   static_assert(DEPTH == 1 || DEPTH == 2, "one or two chunks in flight");
@@ -264,7 +275,8 @@ __global__ __launch_bounds__(kWave * cols_max_waves(KT, KV, CT)) void project_we
   const int L = lane & 15, g = lane >> 4;
   const int tpb = cb.tpb;
   const int H = 2 * tpb, WP = H + 1;
-  const int t0 = blockIdx.x * tpb;
+  const int bx = XCD ? (int)((blockIdx.x % 8u) * (gridDim.x / 8u) + blockIdx.x / 8u) : (int)blockIdx.x;
+  const int t0 = bx * tpb;
   const int tcount = min(tpb, cb.tiles - t0);
   const int nch = (d + R - 1) / R;
 
@@ -288,7 +300,7 @@ __global__ __launch_bounds__(kWave * cols_max_waves(KT, KV, CT)) void project_we
     for (int i = 0; i < NPW; ++i) {
       const int r = c * R + RP * i;
       const bool ok = wok && r + row0 < d;
-      v[i] = ok ? *(const u32x4*)(wsrc + (int64_t)r * ld) : u32x4{0u, 0u, 0u, 0u};
+      v[i] = ok ? ldg<NTL>(wsrc + (int64_t)r * ld) : u32x4{0u, 0u, 0u, 0u};
     }
   };
   auto park_w = [&](int buf, const u32x4 (&v)[NPW]) {
@@ -546,16 +558,31 @@ static hipError_t launch_cols_kv(ColumnBatch cb, int cus, const void* U, int d, 
   int tpb = (cb.tiles + cus - 1) / cus;
   cb.tpb = tpb < 1 ? 1 : (tpb > kMaxTpb ? kMaxTpb : tpb);
   const unsigned grid = (unsigned)((cb.tiles + cb.tpb - 1) / cb.tpb);
+  // XCD-aware strip order when the grid is a multiple of the 8 XCDs;
+  // streamed W loads with k % 8 == 0 and strips of at least 512 bytes
+  const bool xcd = grid % 8 == 0;
+  const bool ntl = KV && cb.tpb * 32 >= 512;
+#define SSN_COLS(CT)                                                                              \
+  do {                                                                                            \
+    if (xcd && ntl)                                                                               \
+      hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, DEPTH, KV, CT, true, true>), dim3(grid), \
+                         dim3(kWave * waves), 0, st, cb, (const uint16_t*)U, d, k);               \
+    else if (xcd)                                                                                 \
+      hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, DEPTH, KV, CT, false, true>), dim3(grid), \
+                         dim3(kWave * waves), 0, st, cb, (const uint16_t*)U, d, k);               \
+    else                                                                                          \
+      hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, DEPTH, KV, CT, false, false>), dim3(grid), \
+                         dim3(kWave * waves), 0, st, cb, (const uint16_t*)U, d, k);               \
+  } while (0)
   if (cb.tpb <= 2 * W2) {
     int waves = (cb.tpb + 1) / 2;
     waves = waves < kColMinWaves ? kColMinWaves : waves;
-    hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, DEPTH, KV, 2>), dim3(grid),
-                       dim3(kWave * waves), 0, st, cb, (const uint16_t*)U, d, k);
+    SSN_COLS(2);
   } else if constexpr (KT <= 4) {
     const int waves = (cb.tpb + 2) / 3;
-    hipLaunchKernelGGL((project_weights_cols_bf16<KT, true, DEPTH, KV, 3>), dim3(grid),
-                       dim3(kWave * waves), 0, st, cb, (const uint16_t*)U, d, k);
+    SSN_COLS(3);
   }
+#undef SSN_COLS
   return hipGetLastError();
 }
 
