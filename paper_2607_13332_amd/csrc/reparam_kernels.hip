@@ -33,7 +33,13 @@ constexpr int kFgDepth = 2;      // chunks in flight in registers (3 measured sl
 // partial sums for its token split; a second kernel adds the splits in order
 // (deterministic).
 // ===========================================================================
-template <int KT, bool K4>
+// FULL: every block owns kFgTiles whole tiles, every split a whole number of
+// chunks and every GT chunk is whole 16-byte pieces for all threads (k a
+// multiple of 64).  Then every load is issued unconditionally (the prefetch
+// past the last chunk re-reads the last chunk): with conditional loads the
+// wait before parking a chunk compiles to a full drain of the prefetch.
+// NTH: H is read with non-temporal loads (each element is read once).
+template <int KT, bool K4, bool FULL = false, bool NTH = false>
 __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* __restrict__ H,
                                                                const float* __restrict__ GT,
                                                                float* __restrict__ out, int64_t N,
@@ -75,12 +81,19 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
 #pragma unroll
     for (int i = 0; i < NHP; ++i) {
       const int64_t t = t_begin + r0 + row0 + RP * i;
-      hr[i] = (hok && t < t_end) ? *(const u32x4*)(hsrc + (r0 + RP * i) * din) : u32x4{0u, 0u, 0u, 0u};
+      if constexpr (FULL)
+        hr[i] = ldg<NTH>(hsrc + (r0 + RP * i) * din);
+      else
+        hr[i] = (hok && t < t_end) ? ldg<NTH>(hsrc + (r0 + RP * i) * din) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int j = 0; j < NGQ; ++j) {
       const int q = tid + NT * j;
-      if constexpr (K4) {
+      if constexpr (FULL) {
+        const int row = q / (k / 4), c4 = q - (q / (k / 4)) * (k / 4);
+        const f32x4 v = *(const f32x4*)(GT + (t_begin + r0 + row) * k + 4 * c4);
+        gr[j][0] = v[0]; gr[j][1] = v[1]; gr[j][2] = v[2]; gr[j][3] = v[3];
+      } else if constexpr (K4) {
         const int row = q / (k / 4), c4 = q - (q / (k / 4)) * (k / 4);
         const int64_t t = t_begin + r0 + row;
         const bool ok = q < R * (k / 4) && t < t_end;
@@ -173,7 +186,8 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
     constexpr int sl = decltype(S)::value;      // register set of chunk c + 1
     compute(c & 1);
     if (c + 1 < nch) park((c + 1) & 1, hv[sl], gv[sl]);
-    if (c + 1 + D < nch) load(c + 1 + D, hv[sl], gv[sl]);
+    if constexpr (FULL) load(c + 1 + D < nch ? c + 1 + D : nch - 1, hv[sl], gv[sl]);
+    else if (c + 1 + D < nch) load(c + 1 + D, hv[sl], gv[sl]);
     __syncthreads();
   };
   for (int c = 0; c < nch; c += D) {
@@ -253,11 +267,18 @@ template <int KT>
 static hipError_t launch_factor_grad_kt(int64_t N, int din, int k, const void* H, const float* GT,
                                         float* dst, int64_t S, int64_t tps, hipStream_t st) {
   const dim3 grid((unsigned)((din / 16 + kFgTiles - 1) / kFgTiles), (unsigned)S);
-  if (k % 4 == 0 && ((uintptr_t)GT & 15u) == 0)
-    hipLaunchKernelGGL((factor_grad_bf16<KT, true>), grid, dim3(kFgThreads), 0, st,
+  const bool k4 = k % 4 == 0 && ((uintptr_t)GT & 15u) == 0;
+  // whole tiles, whole chunks in every split (tps is a multiple of the
+  // chunk), and k filling the K slots of its tile bucket
+  const bool full = k4 && din % (16 * kFgTiles) == 0 && N % kFgRows == 0 && k == 32 * ((KT + 1) / 2);
+  if (full)
+    hipLaunchKernelGGL((factor_grad_bf16<KT, true, true, true>), grid, dim3(kFgThreads), 0, st,
+                       (const uint16_t*)H, GT, dst, N, din, k, tps);
+  else if (k4)
+    hipLaunchKernelGGL((factor_grad_bf16<KT, true, false, true>), grid, dim3(kFgThreads), 0, st,
                        (const uint16_t*)H, GT, dst, N, din, k, tps);
   else
-    hipLaunchKernelGGL((factor_grad_bf16<KT, false>), grid, dim3(kFgThreads), 0, st,
+    hipLaunchKernelGGL((factor_grad_bf16<KT, false, false, true>), grid, dim3(kFgThreads), 0, st,
                        (const uint16_t*)H, GT, dst, N, din, k, tps);
   return hipGetLastError();
 }

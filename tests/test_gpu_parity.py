@@ -321,6 +321,9 @@ REPARAM_SHAPES = [  # (N, din, d, k, dtype): every kernel family and tail
     (64, 256, 128, 16, "f32"), (300, 512, 256, 40, "bf16"), (1000, 2048, 1024, 51, "bf16"),
     (777, 1024, 512, 64, "bf16"), (130, 4096, 2048, 128, "bf16"), (33, 100, 96, 10, "bf16"),
     (5000, 384, 256, 8, "bf16"),
+    # whole 512-column blocks, whole 32-token chunks, k filling its tile
+    # bucket: the factor gradient's unconditional path (k = 32, 64, 128)
+    (2048, 512, 256, 32, "bf16"), (1024, 1024, 512, 64, "bf16"), (256, 512, 256, 128, "bf16"),
 ]
 
 
@@ -347,11 +350,14 @@ def test_reparam_shapes(N, din, d, k, dtype):
     assert torch.equal(GZ, GZ2)
 
 
-def test_reparam_paper_shape_sampled():
-    """Pluralis-8B MLP output projection: din = 18432, d = 5120, k = 51,
-    one 4096-token sequence; checked on sampled rows / factor rows."""
-    N, din, d, k = 4096, 18432, 5120, 51
-    print(f"[case] reparam paper shape N={N} din={din} d={d} k={k}", flush=True)
+@pytest.mark.parametrize("N,din,d,k", [(4096, 18432, 5120, 51), (32768, 14336, 4096, 64)],
+                         ids=["paper8b", "stage8b"])
+def test_reparam_paper_shape_sampled(N, din, d, k):
+    """MLP output projections at full size, checked on sampled rows / factor
+    rows: Pluralis-8B (din = 18432, d = 5120, k = 51, one 4096-token
+    sequence) and the 8B-stage shape (din = 14336, d = 4096, k = 64, 32768
+    tokens; the factor gradient's unconditional path)."""
+    print(f"[case] reparam full shape N={N} din={din} d={d} k={k}", flush=True)
     g = torch.Generator(device=DEV).manual_seed(2024)
     H = torch.randn((N, din), generator=g, device=DEV).to(torch.bfloat16)
     G = torch.randn((N, d), generator=g, device=DEV).to(torch.bfloat16)
