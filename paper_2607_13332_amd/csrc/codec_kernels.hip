@@ -14,23 +14,13 @@ namespace ssn {
 // ===========================================================================
 // compress / project_grad, bf16 storage, MFMA 16x16x32 with fp32 accumulate.
 //
-// Block = 4 waves; wave w owns 16 consecutive tokens (one MFMA M tile).  d is
-// walked in chunks of 128 (4 K steps of 32).  For every chunk the 256 threads
-// stage that slice of U into LDS already in B-fragment order (double
-// buffered, one barrier per chunk), while each wave's X and E[ids] rows go
-// from HBM straight into A-fragment registers with 16-byte loads, NBUF-1
-// chunks ahead of the MFMAs (a ring of NBUF register buffers).
-//
-// B-fragment construction (U is [d][k], k contiguous; a fragment needs 8
-// consecutive d of one column): thread (s, g, n) of the staging pass loads
-// the 8 x KP block U[d0+32s+8g .. +7][n*KP .. n*KP+KP-1] and transposes it in
-// registers into KP fragments; fragment i carries column n*KP + i.  MFMA N
-// tile i therefore produces columns {n*KP + i}, so after the KP tiles each
-// lane holds KP consecutive columns of Z per token: contiguous stores.
-//
-// The embedding subtraction is fused by linearity: X.U and E[ids].U are
-// accumulated by identical MFMA sequences into separate fp32 accumulators
-// and subtracted once at the end (compress(E[ids]) is exactly zero).
+// U is [d][k] (k contiguous) and a B fragment needs 8 consecutive d of one
+// column, so U is staged per d chunk into LDS already in B-fragment order:
+// thread (s, g, n) of the staging pass loads the 8 x KP block
+// U[d0+32s+8g .. +7][n*KP .. n*KP+KP-1] and transposes it in registers into
+// KP fragments; fragment i carries column n*KP + i.  MFMA N tile i therefore
+// produces columns {n*KP + i}, so after the KP tiles each lane holds KP
+// consecutive columns of Z per token: contiguous stores.
 // ===========================================================================
 // Stages one d chunk of U (KS K steps of 32 rows) into LDS in B-fragment
 // order for the "contract over d" kernels.  Fragment (K step s, column tile i)
@@ -94,138 +84,18 @@ struct UStage {
 constexpr int kCompressKS = 4;                 // K steps (of 32) per d chunk
 constexpr int kCompressDC = 32 * kCompressKS;  // d chunk
 
-// HAS_P (with HAS_E false): Z = X.U - P[ids] with the projected table
-// P = E.U; a row equal to E[id] gives zero up to fp32 rounding (the table is
-// formed by the gradient projection, whose kernel may sum d in another order).
-template <int KP, int NBUF, bool HAS_E, bool KFULL, bool ROT = false, bool NT = false,
-          int WAVES = 4, int KS = kCompressKS, bool HAS_P = false, bool NTE = false>
-__global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
-    const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
-    const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
-    float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ P) {
-  static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
-  constexpr int DC = 32 * KS;
-  __shared__ u32x4 lds[2][KS * KP * kWave];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int n16 = lane & 15, g = lane >> 4;
-  const int64_t tok0 = ((int64_t)blockIdx.x * WAVES + wave) * 16;
-  int64_t t = tok0 + n16;
-  t = t < N ? t : N - 1;
-  const uint16_t* xrow = X + t * d + 8 * g;
-  const uint16_t* erow = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * g : nullptr;
-
-  UStage<KP, KFULL, KS, 64 * WAVES> ust;
-  ust.init(tid);
-  const int nch = d / DC;
-  // Each block sweeps the d chunks starting at its own offset: if every wave
-  // read the same column range of its rows at the same time, the requests
-  // would pile onto a few HBM channels.
-  const int rot = ROT ? (int)(blockIdx.x % (unsigned)nch) : 0;
-  auto chunk = [&](int c) { const int x = c + rot; return x < nch ? x : x - nch; };
-
-  u32x4 xf[NBUF][KS], ef[NBUF][KS];
-
-  auto load_xe = [&](int c, u32x4(&xo)[KS], u32x4(&eo)[KS]) {
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      xo[s] = ldg<NT>(xrow + c * DC + 32 * s);
-      if constexpr (HAS_E) eo[s] = ldg<NTE>(erow + c * DC + 32 * s);
-    }
-  };
-  auto load_u = [&](int c) { ust.load(U, (int64_t)c * DC, k); };
-  auto store_u = [&](int buf) { ust.store(lds[buf]); };
-
-  f32x4 accX[KP], accE[KP];
-#pragma unroll
-  for (int i = 0; i < KP; ++i) {
-    accX[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    accE[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-#pragma unroll
-  for (int b = 0; b + 1 < NBUF; ++b) load_xe(chunk(b < nch ? b : nch - 1), xf[b], ef[b]);
-  load_u(chunk(0));
-  store_u(0);
-
-  for (int c0 = 0; c0 < nch; c0 += NBUF) {
-#pragma unroll
-    for (int b = 0; b < NBUF; ++b) {
-      const int c = c0 + b;
-      if (c < nch) {
-        // U of the next chunk first (it is consumed at the end of this
-        // iteration), then X / E of chunk c+NBUF-1 (consumed NBUF-1
-        // iterations later): in-order completion lets the staging wait skip
-        // the younger X / E loads.
-        const int cu = (c + 1 < nch) ? c + 1 : nch - 1;
-        load_u(chunk(cu));
-        const int pb = (b + NBUF - 1) % NBUF;   // compile-time after unrolling
-        const int pf = (c + NBUF - 1 < nch) ? c + NBUF - 1 : nch - 1;
-        load_xe(chunk(pf), xf[pb], ef[pb]);
-        __syncthreads();
-        const u32x4* fr = lds[c & 1];
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          u32x4 bfr[KP];
-#pragma unroll
-          for (int i = 0; i < KP; ++i) bfr[i] = fr[(s * KP + i) * kWave + lane];
-#pragma unroll
-          for (int i = 0; i < KP; ++i) {
-            accX[i] = mfma16x16x32(xf[b][s], bfr[i], accX[i]);
-            if constexpr (HAS_E) accE[i] = mfma16x16x32(ef[b][s], bfr[i], accE[i]);
-          }
-        }
-        store_u((c + 1) & 1);
-      }
-    }
-  }
-
-  // ---- epilogue: lane (n16, g) holds Z[tok0+4g+j][n16*KP + i] ----
-  const int col0 = n16 * KP;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int64_t tj = tok0 + 4 * g + j;
-    if (tj < N) {
-      float v[KP];
-#pragma unroll
-      for (int i = 0; i < KP; ++i) v[i] = HAS_E ? accX[i][j] - accE[i][j] : accX[i][j];
-      if constexpr (HAS_P) {
-        const float* pp = P + clamp_id(ids[tj], V) * k + col0;
-        if constexpr (KFULL && KP % 4 == 0) {
-#pragma unroll
-          for (int i = 0; i < KP; i += 4) {
-            const f32x4 q = *(const f32x4*)(pp + i);
-            v[i] -= q[0]; v[i + 1] -= q[1]; v[i + 2] -= q[2]; v[i + 3] -= q[3];
-          }
-        } else {
-#pragma unroll
-          for (int i = 0; i < KP; ++i)
-            if (col0 + i < k) v[i] -= pp[i];
-        }
-      }
-      float* zp = Z + tj * k + col0;
-      if constexpr (KFULL && KP % 4 == 0) {
-#pragma unroll
-        for (int i = 0; i < KP; i += 4) *(f32x4*)(zp + i) = f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
-      } else {
-#pragma unroll
-        for (int i = 0; i < KP; ++i)
-          if (col0 + i < k) zp[i] = v[i];
-      }
-    }
-  }
-}
-
 // ===========================================================================
-// compress / project_grad, variant with row-contiguous activation loads.
+// compress / project_grad / projected-table compress, many tokens.
 //
-// Same MFMA scheme as compress_mfma_bf16 (U staged per 128-wide d chunk in
-// B-fragment order, X.U and E[ids].U in separate fp32 accumulators), but each
-// wave loads its 16 X rows and 16 E[ids] rows for a chunk as 4 instructions
-// of 4 rows x 256 contiguous bytes (8 whole 128-byte lines per instruction,
-// instead of 16 half lines), parks them in a wave-private XOR-swizzled LDS
-// tile, and reads its A fragments from there.
+// Wave w of the block owns 16 consecutive tokens (one MFMA M tile); d is
+// walked in chunks of 128 (4 K steps of 32), U staged per chunk by UStage
+// (double buffered, one barrier per chunk).  Each wave loads its 16 X rows
+// and 16 E[ids] rows for a chunk as 4 instructions of 4 rows x 256 contiguous
+// bytes (8 whole 128-byte lines per instruction), parks them in a
+// wave-private XOR-swizzled LDS tile, and reads its A fragments from there.
+// The embedding subtraction is fused by linearity: X.U and E[ids].U are
+// accumulated by identical MFMA sequences into separate fp32 accumulators and
+// subtracted once at the end (compress(E[ids]) is exactly zero).
 //
 // Rows travel DEPTH chunks ahead of the MFMAs in DEPTH register sets.  Within
 // a step the next chunk's U is requested before the rows of chunk c + DEPTH:
@@ -237,13 +107,18 @@ __global__ __launch_bounds__(64 * WAVES) void compress_mfma_bf16(
 // blocks over the columns of the rows).  NTX / NTE: non-temporal loads of the
 // activation / embedding rows.
 // ===========================================================================
+//
+// HAS_P (with HAS_E false): Z = X.U - P[ids] with the projected table
+// P = E.U (section 4.1: E and U are fixed, so the subtraction commutes with
+// the projection); the table rows are subtracted in the epilogue.
 template <int KP, bool HAS_E, bool KFULL, int WAVES = 8, int DEPTH = 1, bool NTX = false,
-          bool NTE = false, bool ROT = false, int ROTG = 1>
+          bool NTE = false, bool ROT = false, int ROTG = 1, bool HAS_P = false>
 __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
-    float* __restrict__ Z, int64_t N, int d, int k, int64_t V) {
+    float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ P) {
   static_assert(DEPTH >= 1 && DEPTH <= 4, "one to four chunks of rows in flight");
+  static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
   constexpr int KS = 4, DC = 128;
   __shared__ u32x4 lds[2][KS * KP * kWave];      // U B fragments, double buffered
   __shared__ u32x4 tile[WAVES][HAS_E ? 2 : 1][16 * 16];   // [wave][X/E][row * 16 + cell ^ row]
@@ -358,6 +233,20 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
       float v[KP];
 #pragma unroll
       for (int i = 0; i < KP; ++i) v[i] = HAS_E ? accX[i][j] - accE[i][j] : accX[i][j];
+      if constexpr (HAS_P) {
+        const float* pp = P + clamp_id(ids[tj], V) * k + col0;
+        if constexpr (KFULL && KP % 4 == 0) {
+#pragma unroll
+          for (int i = 0; i < KP; i += 4) {
+            const f32x4 q = *(const f32x4*)(pp + i);
+            v[i] -= q[0]; v[i + 1] -= q[1]; v[i + 2] -= q[2]; v[i + 3] -= q[3];
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < KP; ++i)
+            if (col0 + i < k) v[i] -= pp[i];
+        }
+      }
       float* zp = Z + tj * k + col0;
       if constexpr (KFULL && KP % 4 == 0) {
 #pragma unroll
@@ -930,17 +819,6 @@ bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) {
   return dtype == kBF16 && d % (2 * kDecompressDC) == 0 && d <= INT32_MAX && k >= 1 && k <= 128;
 }
 
-template <int KP, bool HAS_E, bool KFULL, int WAVES, int KS, bool HAS_P>
-static hipError_t launch_compress_v(int64_t N, int d, int k, int64_t V, const void* X,
-                                    const int32_t* ids, const void* E, const void* U, float* Z,
-                                    const float* P, hipStream_t st) {
-  const int64_t blocks = (N + 16 * WAVES - 1) / (16 * WAVES);
-  hipLaunchKernelGGL((compress_mfma_bf16<KP, 1, HAS_E, KFULL, false, false, WAVES, KS, HAS_P>),
-                     dim3((unsigned)blocks), dim3(64 * WAVES), 0, st, (const uint16_t*)X, ids,
-                     (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P);
-  return hipGetLastError();
-}
-
 // Row-contiguous kernel: 8 waves (128 tokens) per block with a rotated sweep
 // of d once N/128 blocks fill the compute units, else 4 waves (64 tokens) in
 // the natural order.  The rotation moves in steps of 4 chunks (1 KB of a bf16
@@ -948,43 +826,32 @@ static hipError_t launch_compress_v(int64_t N, int d, int k, int64_t V, const vo
 // concurrent requests collide (measured 1.1-1.8x slower at d = 4096).
 // Activation rows are streamed with non-temporal loads; embedding rows keep
 // normal caching (repeated ids hit in L2).
-template <int KP, bool HAS_E, bool KFULL>
+template <int KP, bool HAS_E, bool KFULL, bool HAS_P>
 static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const void* X,
                                        const int32_t* ids, const void* E, const void* U, float* Z,
-                                       hipStream_t st) {
+                                       const float* P, hipStream_t st) {
   if ((N + 127) / 128 >= device_cu_count()) {
     const int64_t blocks = (N + 127) / 128;
-    hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 8, 1, true, false, true, 4>),
+    hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 8, 1, true, false, true, 4, HAS_P>),
                        dim3((unsigned)blocks), dim3(512), 0, st, (const uint16_t*)X, ids,
-                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V);
+                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P);
   } else {
     const int64_t blocks = (N + 63) / 64;
-    hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 4, 1, true, false, false>),
+    hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 4, 1, true, false, false, 1, HAS_P>),
                        dim3((unsigned)blocks), dim3(256), 0, st, (const uint16_t*)X, ids,
-                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V);
+                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P);
   }
   return hipGetLastError();
 }
 
-// compress (with the embedding rows) and the gradient projection use the
-// row-contiguous variant; the projected-table compress (X.U - P[ids]) the
-// direct-fragment variant with 8 waves (128 tokens) per block sharing each
-// staged slice of U, in 256-d chunks when d allows, else 128.
+// compress (with the embedding rows), the gradient projection and the
+// projected-table compress all use the row-contiguous kernel.
 template <int KP, bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_kp(int64_t N, int d, int k, int64_t V, const void* X,
                                      const int32_t* ids, const void* E, const void* U, float* Z,
                                      const float* P, hipStream_t st) {
-  const bool kfull = (k == 16 * KP);
-  if constexpr (!HAS_P) {
-    return kfull ? launch_compress_rows<KP, HAS_E, true>(N, d, k, V, X, ids, E, U, Z, st)
-                 : launch_compress_rows<KP, HAS_E, false>(N, d, k, V, X, ids, E, U, Z, st);
-  } else {
-    if (d % 256 == 0)
-      return kfull ? launch_compress_v<KP, false, true, 8, 8, true>(N, d, k, V, X, ids, E, U, Z, P, st)
-                   : launch_compress_v<KP, false, false, 8, 8, true>(N, d, k, V, X, ids, E, U, Z, P, st);
-    return kfull ? launch_compress_v<KP, false, true, 8, 4, true>(N, d, k, V, X, ids, E, U, Z, P, st)
-                 : launch_compress_v<KP, false, false, 8, 4, true>(N, d, k, V, X, ids, E, U, Z, P, st);
-  }
+  return k == 16 * KP ? launch_compress_rows<KP, HAS_E, true, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st)
+                      : launch_compress_rows<KP, HAS_E, false, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
 }
 
 template <bool HAS_E, bool HAS_P>
