@@ -973,13 +973,15 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
   return launch_compress_generic<uint16_t, false, false>(N, d, k, V, X, ids, E, U, Z, P, st);
 }
 
-// 8 token tiles (128 tokens) per block.  When N/128 blocks fill the compute
-// units, each of the 8 waves sweeps all of d (rotated per block, in steps of
-// one chunk); the gradient expansion (no embedding rows to gather) then
-// stores two chunks at a time (256 contiguous bytes per row).  With fewer
-// tokens the block has 2 halves of d (16 waves) and a second grid dimension
-// splits d further (the smallest divisor of the chunk-pair count that gives
-// one block per compute unit).  The activation rows are written with
+// 8 token tiles (128 tokens) per block, each of the 8 waves sweeping the
+// block's range of d (rotated per block, in steps of one chunk).  When N/128
+// blocks fill the compute units the range is all of d; with fewer tokens a
+// second grid dimension splits d (the smallest divisor of the chunk count
+// that gives one block per compute unit; measured at N = 4096 against blocks
+// holding two halves of d in 16 waves: expansion 12.0 -> 9.2 us at d = 4096,
+// decompress 13.8 -> 13.2 us).  The gradient expansion (no embedding rows to
+// gather) stores two chunks at a time (256 contiguous bytes per row) when
+// each block's chunk count is even.  The activation rows are written with
 // non-temporal stores (streamed out instead of parked dirty in the caches,
 // where they slowed the next kernel's reads).
 template <int KS2, bool HAS_E, int KM, bool GZ>
@@ -989,25 +991,22 @@ static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const
   constexpr int TW = 8;
   const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
   const int64_t cus = device_cu_count();
-  if (blocks >= cus) {
-    // d % 128 == 0, so the chunk count d / 64 is even (store groups of two)
-    constexpr int SG = HAS_E ? 1 : 2;
-    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ, false,
-                                             1, SG>),
-                       dim3((unsigned)blocks, 1), dim3(64 * TW), 0, st, Zc, ids,
-                       (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
-    return hipGetLastError();
-  }
-  constexpr int DS = 2;
-  const int pairs = d / (kDecompressDC * DS);
+  const int chunks = d / kDecompressDC;
   int gy = 1;
-  while (gy < pairs && blocks * gy < cus) {
+  while (gy < chunks && blocks * gy < cus) {
     ++gy;
-    while (pairs % gy != 0) ++gy;
+    while (chunks % gy != 0) ++gy;
   }
-  hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, DS, TW, true, GZ>),
-                     dim3((unsigned)blocks, (unsigned)gy), dim3(64 * TW * DS), 0, st, Zc, ids,
-                     (const uint16_t*)E, (const uint16_t*)U, (uint16_t*)Y, N, d, k, V);
+  const dim3 grid((unsigned)blocks, (unsigned)gy);
+  if (!HAS_E && (chunks / gy) % 2 == 0)
+    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ, false,
+                                             1, 2>),
+                       grid, dim3(64 * TW), 0, st, Zc, ids, (const uint16_t*)E, (const uint16_t*)U,
+                       (uint16_t*)Y, N, d, k, V);
+  else
+    hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ>), grid,
+                       dim3(64 * TW), 0, st, Zc, ids, (const uint16_t*)E, (const uint16_t*)U,
+                       (uint16_t*)Y, N, d, k, V);
   return hipGetLastError();
 }
 
