@@ -208,7 +208,11 @@ ssn_status_t ssn_project_weights_batched(ssn_dtype_t dtype, int64_t count, int64
  *                      only G, H and Zp, but T is what crosses to U^T)
  *   Y [N, d] dtype     output
  * Two launches on `stream` (the projection of H by Zp, then the expansion
- * by U^T).  Outputs must not overlap inputs or each other.
+ * by U^T), or three when, with few tokens, the projection splits din into
+ * up to four ranges: their float32 partial products are staged in Y's
+ * memory (before Y is written) and summed in a fixed order.  The number of
+ * ranges depends on the shape and the device's compute-unit count.
+ * Outputs must not overlap inputs or each other.
  */
 ssn_status_t ssn_reparam_forward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,
                                  const void *H, const void *Zp, const void *U, float *T, void *Y,
@@ -229,7 +233,8 @@ size_t ssn_reparam_workspace_bytes(ssn_dtype_t dtype, int64_t N, int64_t din, in
  * `workspace` (device, 4-byte aligned, caller-owned) holds at least
  * ssn_reparam_workspace_bytes(dtype, N, din, k) bytes, else SSN_ERR_SHAPE.
  * The factor gradient is summed over token splits in a fixed order
- * (deterministic).  Three or four launches on `stream`.
+ * (deterministic).  Like the forward, G U may split d into ranges staged in
+ * GH's memory before GH is written.  Three to five launches on `stream`.
  */
 ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,
                                   const void *H, const void *Zp, const void *U, const void *G,

@@ -312,8 +312,12 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n16 = lane & 15, g = lane >> 4;
   const int64_t tok0 = (int64_t)blockIdx.x * R;
-  const int nchp = d / (DC * P);               // chunks of this wave
-  const int c0 = wave * nchp;
+  // gridDim.y > 1 (plain projections only): block y covers the y-th of
+  // gridDim.y equal ranges of d and writes its partial product to
+  // Z + y * N * k (summed by a second kernel)
+  const int nchp = d / (DC * P * (int)gridDim.y);   // chunks of this wave
+  const int c0 = ((int)blockIdx.y * P + wave) * nchp;
+  if constexpr (!HAS_E && !HAS_P) Z += (int64_t)blockIdx.y * N * k;
   u32x4* const xtw = (u32x4*)(smem + wave * WAVE_BYTES);           // [X/E][row * 8 + cell']
   uint16_t* const utw = (uint16_t*)(smem + wave * WAVE_BYTES + XT_BYTES);
 
@@ -880,8 +884,8 @@ static unsigned generic_blocks(int64_t N) {
 template <int KP, bool HAS_E, bool HAS_P, int P, int TTW>
 static hipError_t launch_split_t(int64_t N, int d, int k, int64_t V, const void* X,
                                  const int32_t* ids, const void* E, const void* U, float* Z,
-                                 const float* Pt, hipStream_t st) {
-  const dim3 grid((unsigned)((N + 16 * TTW - 1) / (16 * TTW)));
+                                 const float* Pt, hipStream_t st, int S) {
+  const dim3 grid((unsigned)((N + 16 * TTW - 1) / (16 * TTW)), (unsigned)S);
 #define SSN_SPLIT(UM)                                                                           \
   hipLaunchKernelGGL((compress_split_bf16<KP, HAS_E, HAS_P, UM, P, TTW>), grid, dim3(64 * P), 0, \
                      st, (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d, \
@@ -902,14 +906,14 @@ static hipError_t launch_split_t(int64_t N, int d, int k, int64_t V, const void*
 template <int KP, bool HAS_E, bool HAS_P>
 static hipError_t launch_split_kp(int P, int TTW, int64_t N, int d, int k, int64_t V, const void* X,
                                   const int32_t* ids, const void* E, const void* U, float* Z,
-                                  const float* Pt, hipStream_t st) {
+                                  const float* Pt, hipStream_t st, int S) {
   if constexpr (KP <= 4) {
-    if (P == 8) return launch_split_t<KP, HAS_E, HAS_P, 8, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st);
+    if (P == 8) return launch_split_t<KP, HAS_E, HAS_P, 8, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
     if (P == 4 && TTW == 2)
-      return launch_split_t<KP, HAS_E, HAS_P, 4, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st);
+      return launch_split_t<KP, HAS_E, HAS_P, 4, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
   }
-  if (P >= 4) return launch_split_t<KP, HAS_E, HAS_P, 4, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st);
-  return launch_split_t<KP, HAS_E, HAS_P, 2, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st);
+  if (P >= 4) return launch_split_t<KP, HAS_E, HAS_P, 4, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
+  return launch_split_t<KP, HAS_E, HAS_P, 2, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
 }
 
 // When the d-split kernel runs (measured on MI355X at d = 4096 and 5120):
@@ -923,19 +927,79 @@ static bool compress_uses_split(int64_t N, int64_t d, int64_t k, bool has_e) {
   return N <= (has_e ? 8192 : 16384);
 }
 
+// Waves over d (P) and token tiles per wave (TTW) of the few-token kernel:
+// eight waves while that gives about eight waves per compute unit, else
+// four; two token tiles per wave for the projections (with one stream of
+// rows the registers allow it); with k > 64 at most four waves and one tile
+// (LDS); fewer waves where S ranges of d would not split into whole chunks.
+static void split_shape(int64_t N, int d, int k, bool has_e, int S, int& P, int& TTW) {
+  P = N <= 6144 ? 8 : 4;
+  TTW = (P == 4 && !has_e) ? 2 : 1;
+  if (k > 64) { P = 4; TTW = 1; }
+  while (P > 2 && d % (64 * P * S) != 0) P /= 2;
+}
+
 template <bool HAS_E, bool HAS_P>
 static hipError_t launch_split(int64_t N, int d, int k, int64_t V, const void* X, const int32_t* ids,
                                const void* E, const void* U, float* Z, const float* Pt,
-                               hipStream_t st) {
-  // eight waves over d while that gives about eight waves per compute unit,
-  // else four; two token tiles per wave for the projections (with one stream
-  // of rows the registers allow it)
-  int P = N <= 6144 ? 8 : 4;
-  const int TTW = (P == 4 && !HAS_E) ? 2 : 1;
-  while (P > 2 && d % (64 * P) != 0) P /= 2;
-  if (k <= 32) return launch_split_kp<2, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st);
-  if (k <= 64) return launch_split_kp<4, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st);
-  return launch_split_kp<8, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st);
+                               hipStream_t st, int S = 1) {
+  int P, TTW;
+  split_shape(N, d, k, HAS_E, S, P, TTW);
+  if (k <= 32) return launch_split_kp<2, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, S);
+  if (k <= 64) return launch_split_kp<4, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, S);
+  return launch_split_kp<8, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, S);
+}
+
+// Ranges of d for the plain projection Z = X.U on the few-token kernel; 1
+// when that kernel does not run.  A compute unit holds 8/P blocks (two waves
+// per SIMD); the count taken (at most smax, whole chunks per wave) fills the
+// last round of blocks best, the smallest such count unless a larger one
+// fills it clearly better (measured on MI355X at din = 5120, 14336 and
+// 18432: with N/16 blocks of eight waves, one round of one block per compute
+// unit beats every split; half a round is best split in two).
+int project_split_count(int dtype, int64_t N, int64_t d, int64_t k, int smax) {
+  if (!compress_uses_mfma(dtype, d, k) || !compress_uses_split(N, d, k, false)) return 1;
+  const int64_t cus = device_cu_count();
+  int S = 1;
+  double best = 0.0;
+  for (int s = 1; s <= smax; ++s) {
+    int P, TTW;
+    split_shape(N, (int)d, (int)k, false, s, P, TTW);
+    if (d % (64 * P * s) != 0) continue;
+    const int64_t blocks = s * ((N + 16 * TTW - 1) / (16 * TTW));
+    const int64_t slots = cus * (8 / P);
+    const int64_t rounds = (blocks + slots - 1) / slots;
+    const double fill = (double)blocks / (double)(rounds * slots);
+    if (fill > best + 0.05) {
+      best = fill;
+      S = s;
+    }
+  }
+  return S;
+}
+
+// Sum of S partial results [S][n], in range order (deterministic).
+__global__ __launch_bounds__(256) void sum_partials(const float* __restrict__ ws,
+                                                    float* __restrict__ out, int64_t n, int S) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    float v = ws[i];
+    for (int j = 1; j < S; ++j) v += ws[(int64_t)j * n + i];
+    out[i] = v;
+  }
+}
+
+// Z [N, k] = X . U as S partial products over ranges of d into ws [S][N][k],
+// then their sum.
+hipError_t launch_project_ranges(int64_t N, int64_t d, int64_t k, const void* X, const void* U,
+                                 float* Z, float* ws, int S, hipStream_t st) {
+  hipError_t e =
+      launch_split<false, false>(N, (int)d, (int)k, 1, X, nullptr, nullptr, U, ws, nullptr, st, S);
+  if (e != hipSuccess) return e;
+  const int64_t n = N * k;
+  const int64_t blocks = (n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048;
+  hipLaunchKernelGGL(sum_partials, dim3((unsigned)blocks), dim3(256), 0, st, ws, Z, n, S);
+  return hipGetLastError();
 }
 
 template <typename T, bool HAS_E, bool HAS_P>

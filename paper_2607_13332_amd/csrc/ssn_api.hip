@@ -12,6 +12,7 @@
 namespace {
 
 constexpr int64_t kMaxElems = (int64_t)1 << 56;   // keeps every byte offset in int64
+constexpr int kReparamMaxRanges = 4;               // ranges of din in the forward projection
 
 inline int64_t elem_size(int dtype) { return dtype == SSN_BF16 ? 2 : 4; }
 
@@ -160,6 +161,19 @@ static ssn_status_t reparam_shape(ssn_dtype_t dtype, int64_t N, int64_t din, int
   return SSN_OK;
 }
 
+// Z [N, k] = X [N, dx] . W [dx, k].  With few tokens the projection splits
+// dx into ranges whose partial products go to `scratch` (row_bytes bytes per
+// token, free until Z is complete) when it is large enough.
+static hipError_t project_in_ranges(ssn_dtype_t dtype, int64_t N, int64_t dx, int64_t k,
+                                    const void* X, const void* W, float* Z, void* scratch,
+                                    int64_t row_bytes, hipStream_t st) {
+  int64_t smax = aligned_to(scratch, 4) ? row_bytes / (k * 4) : 1;
+  smax = smax < kReparamMaxRanges ? smax : kReparamMaxRanges;
+  const int S = ssn::project_split_count(dtype, N, dx, k, (int)smax);
+  if (S > 1) return ssn::launch_project_ranges(N, dx, k, X, W, Z, (float*)scratch, S, st);
+  return ssn::launch_compress(dtype, N, dx, k, 1, X, nullptr, nullptr, W, Z, nullptr, st);
+}
+
 ssn_status_t ssn_reparam_forward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,
                                  const void* H, const void* Zp, const void* U, float* T, void* Y,
                                  void* stream) {
@@ -176,7 +190,8 @@ ssn_status_t ssn_reparam_forward(ssn_dtype_t dtype, int64_t N, int64_t din, int6
     if (overlap(ts, in) || overlap(ys, in)) return SSN_ERR_ALIAS;
   if (overlap(ts, ys)) return SSN_ERR_ALIAS;
   hipStream_t st = (hipStream_t)stream;
-  hipError_t e = ssn::launch_compress(dtype, N, din, k, 1, H, nullptr, nullptr, Zp, T, nullptr, st);
+  // Y is written only after T is complete: it holds the partial products
+  hipError_t e = project_in_ranges(dtype, N, din, k, H, Zp, T, Y, d * s, st);
   if (e != hipSuccess) return SSN_ERR_LAUNCH;
   return launch_status(ssn::launch_decompress(dtype, N, d, k, 1, T, nullptr, nullptr, U, Y, false, st));
 }
@@ -217,7 +232,8 @@ ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int
   hipStream_t st = (hipStream_t)stream;
   if (N == 0)   // no tokens: the factor-gradient kernel writes zeros (no memset, capture-safe)
     return launch_status(ssn::launch_factor_grad(dtype, 0, din, k, H, GT, GZp, (float*)workspace, st));
-  hipError_t e = ssn::launch_compress(dtype, N, d, k, 1, G, nullptr, nullptr, U, GT, nullptr, st);
+  // GH is written only after GT is complete: it holds the partial products
+  hipError_t e = project_in_ranges(dtype, N, d, k, G, U, GT, GH, din * s, st);
   if (e != hipSuccess) return SSN_ERR_LAUNCH;
   e = ssn::launch_decompress(dtype, N, din, k, 1, GT, nullptr, nullptr, Zp, GH, false, st);
   if (e != hipSuccess) return SSN_ERR_LAUNCH;

@@ -324,6 +324,10 @@ REPARAM_SHAPES = [  # (N, din, d, k, dtype): every kernel family and tail
     # whole 512-column blocks, whole 32-token chunks, k filling its tile
     # bucket: the factor gradient's unconditional path (k = 32, 64, 128)
     (2048, 512, 256, 32, "bf16"), (1024, 1024, 512, 64, "bf16"), (256, 512, 256, 128, "bf16"),
+    # few tokens: the projections split din (forward) or d (backward) into
+    # two to four ranges staged in the output's memory
+    (1000, 3072, 1024, 40, "bf16"), (777, 1536, 2048, 51, "bf16"), (1024, 1024, 1024, 128, "bf16"),
+    (6144, 3072, 1536, 51, "bf16"),
 ]
 
 
