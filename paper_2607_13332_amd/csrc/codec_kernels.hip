@@ -908,6 +908,9 @@ static hipError_t launch_split_kp(int P, int TTW, int64_t N, int d, int k, int64
                                   const int32_t* ids, const void* E, const void* U, float* Z,
                                   const float* Pt, hipStream_t st, int S) {
   if constexpr (KP <= 4) {
+    if constexpr (!HAS_E)
+      if (P == 8 && TTW == 2)
+        return launch_split_t<KP, HAS_E, HAS_P, 8, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
     if (P == 8) return launch_split_t<KP, HAS_E, HAS_P, 8, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
     if (P == 4 && TTW == 2)
       return launch_split_t<KP, HAS_E, HAS_P, 4, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
@@ -927,55 +930,68 @@ static bool compress_uses_split(int64_t N, int64_t d, int64_t k, bool has_e) {
   return N <= (has_e ? 8192 : 16384);
 }
 
-// Waves over d (P) and token tiles per wave (TTW) of the few-token kernel:
-// eight waves while that gives about eight waves per compute unit, else
-// four; two token tiles per wave for the projections (with one stream of
-// rows the registers allow it); with k > 64 at most four waves and one tile
-// (LDS); fewer waves where S ranges of d would not split into whole chunks.
-static void split_shape(int64_t N, int d, int k, bool has_e, int S, int& P, int& TTW) {
-  P = N <= 6144 ? 8 : 4;
-  TTW = (P == 4 && !has_e) ? 2 : 1;
-  if (k > 64) { P = 4; TTW = 1; }
-  while (P > 2 && d % (64 * P * S) != 0) P /= 2;
+// Shape of a few-token launch: P waves over d, TTW token tiles per wave, S
+// ranges of d (grid.y; S > 1 only for plain projections with room for the
+// partial products).
+struct SplitPlan {
+  int P, TTW, S;
+};
+
+// compress (E[ids] rows stream beside X): one tile per wave, eight waves
+// while that gives about eight waves per compute unit, else four.  k > 64:
+// four waves, one tile (LDS).  Projections: two tiles per wave (each U chunk
+// staged then feeds 32 tokens, half the U traffic through L2) unless their
+// blocks would fill under 60% of the last round on the compute units (a
+// unit holds 8/P blocks: two waves per SIMD); for the tile count taken, the
+// number of ranges S <= smax whose blocks fill the last round best, fewer
+// ranges unless the fill is 5% better; eight waves while the blocks of one
+// range fit one round.  P drops where the ranges would not split d into
+// whole chunks.  Measured on MI355X (din = 14336 and 18432, k = 51 and 64,
+// N = 1000 to 16384), e.g. N = 4096, k = 51: 62 us with one tile, 46 us
+// with two tiles in two ranges; N = 3000 without ranges: one tile 58 us,
+// two tiles 61 us; N = 6144: two tiles 80 us, 74 us in four ranges.
+static SplitPlan split_plan(int64_t N, int d, int k, bool has_e, int smax) {
+  if (has_e || k > 64) {
+    SplitPlan p{k > 64 ? 4 : (N <= 6144 ? 8 : 4), 1, 1};
+    while (p.P > 2 && d % (64 * p.P) != 0) p.P /= 2;
+    return p;
+  }
+  const int64_t cus = device_cu_count();
+  auto best_for = [&](int ttw, double& bfill) {
+    SplitPlan best{2, 1, 1};
+    bfill = 0.0;
+    for (int s = 1; s <= smax; ++s) {
+      int P = (N + 16 * ttw - 1) / (16 * ttw) <= cus ? 8 : 4;
+      while (P > 2 && d % (64 * P * s) != 0) P /= 2;
+      if (d % (64 * P * s) != 0) continue;
+      const int t = P == 2 ? 1 : ttw;          // two-wave blocks take one tile
+      const int64_t blocks = s * ((N + 16 * t - 1) / (16 * t));
+      const int64_t slots = cus * (8 / P);
+      const int64_t rounds = (blocks + slots - 1) / slots;
+      const double fill = (double)blocks / (double)(rounds * slots);
+      if (fill > 1.05 * bfill) {
+        bfill = fill;
+        best = SplitPlan{P, t, s};
+      }
+    }
+    return best;
+  };
+  double f2, f1;
+  const SplitPlan p2 = best_for(2, f2);
+  if (f2 >= 0.6) return p2;
+  const SplitPlan p1 = best_for(1, f1);
+  return f1 > f2 ? p1 : p2;
 }
 
 template <bool HAS_E, bool HAS_P>
 static hipError_t launch_split(int64_t N, int d, int k, int64_t V, const void* X, const int32_t* ids,
                                const void* E, const void* U, float* Z, const float* Pt,
-                               hipStream_t st, int S = 1) {
-  int P, TTW;
-  split_shape(N, d, k, HAS_E, S, P, TTW);
-  if (k <= 32) return launch_split_kp<2, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, S);
-  if (k <= 64) return launch_split_kp<4, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, S);
-  return launch_split_kp<8, HAS_E, HAS_P>(P, TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, S);
-}
-
-// Ranges of d for the plain projection Z = X.U on the few-token kernel; 1
-// when that kernel does not run.  A compute unit holds 8/P blocks (two waves
-// per SIMD); the count taken (at most smax, whole chunks per wave) fills the
-// last round of blocks best, the smallest such count unless a larger one
-// fills it clearly better (measured on MI355X at din = 5120, 14336 and
-// 18432: with N/16 blocks of eight waves, one round of one block per compute
-// unit beats every split; half a round is best split in two).
-int project_split_count(int dtype, int64_t N, int64_t d, int64_t k, int smax) {
-  if (!compress_uses_mfma(dtype, d, k) || !compress_uses_split(N, d, k, false)) return 1;
-  const int64_t cus = device_cu_count();
-  int S = 1;
-  double best = 0.0;
-  for (int s = 1; s <= smax; ++s) {
-    int P, TTW;
-    split_shape(N, (int)d, (int)k, false, s, P, TTW);
-    if (d % (64 * P * s) != 0) continue;
-    const int64_t blocks = s * ((N + 16 * TTW - 1) / (16 * TTW));
-    const int64_t slots = cus * (8 / P);
-    const int64_t rounds = (blocks + slots - 1) / slots;
-    const double fill = (double)blocks / (double)(rounds * slots);
-    if (fill > best + 0.05) {
-      best = fill;
-      S = s;
-    }
-  }
-  return S;
+                               hipStream_t st, const SplitPlan& p) {
+  if (k <= 32)
+    return launch_split_kp<2, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S);
+  if (k <= 64)
+    return launch_split_kp<4, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S);
+  return launch_split_kp<8, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S);
 }
 
 // Sum of S partial results [S][n], in range order (deterministic).
@@ -987,19 +1003,6 @@ __global__ __launch_bounds__(256) void sum_partials(const float* __restrict__ ws
     for (int j = 1; j < S; ++j) v += ws[(int64_t)j * n + i];
     out[i] = v;
   }
-}
-
-// Z [N, k] = X . U as S partial products over ranges of d into ws [S][N][k],
-// then their sum.
-hipError_t launch_project_ranges(int64_t N, int64_t d, int64_t k, const void* X, const void* U,
-                                 float* Z, float* ws, int S, hipStream_t st) {
-  hipError_t e =
-      launch_split<false, false>(N, (int)d, (int)k, 1, X, nullptr, nullptr, U, ws, nullptr, st, S);
-  if (e != hipSuccess) return e;
-  const int64_t n = N * k;
-  const int64_t blocks = (n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048;
-  hipLaunchKernelGGL(sum_partials, dim3((unsigned)blocks), dim3(256), 0, st, ws, Z, n, S);
-  return hipGetLastError();
 }
 
 template <typename T, bool HAS_E, bool HAS_P>
@@ -1019,9 +1022,10 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
   if (compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(Z) && (!has_e || al16(E)) &&
       (!has_p || al16(P))) {
     if (compress_uses_split(N, d, k, has_e)) {
-      if (has_e) return launch_split<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
-      if (has_p) return launch_split<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
-      return launch_split<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
+      const SplitPlan sp = split_plan(N, (int)d, (int)k, has_e, 1);
+      if (has_e) return launch_split<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp);
+      if (has_p) return launch_split<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp);
+      return launch_split<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp);
     }
     if (has_e) return launch_compress_mfma<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
     if (has_p) return launch_compress_mfma<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
@@ -1035,6 +1039,26 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
   if (has_e) return launch_compress_generic<uint16_t, true, false>(N, d, k, V, X, ids, E, U, Z, P, st);
   if (has_p) return launch_compress_generic<uint16_t, false, true>(N, d, k, V, X, ids, E, U, Z, P, st);
   return launch_compress_generic<uint16_t, false, false>(N, d, k, V, X, ids, E, U, Z, P, st);
+}
+
+// Z = X.U; with few tokens the few-token kernel may split d into up to
+// smax ranges whose partial products go to ws [S][N][k] and are then summed.
+hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, const void* X,
+                                 const void* U, float* Z, float* ws, int smax, hipStream_t st) {
+  if (smax > 1 && ws && compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(Z) &&
+      compress_uses_split(N, d, k, false)) {
+    const SplitPlan sp = split_plan(N, (int)d, (int)k, false, smax);
+    if (sp.S > 1) {
+      hipError_t e = launch_split<false, false>(N, (int)d, (int)k, 1, X, nullptr, nullptr, U, ws,
+                                                nullptr, st, sp);
+      if (e != hipSuccess) return e;
+      const int64_t n = N * k;
+      const int64_t blocks = (n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048;
+      hipLaunchKernelGGL(sum_partials, dim3((unsigned)blocks), dim3(256), 0, st, ws, Z, n, sp.S);
+      return hipGetLastError();
+    }
+  }
+  return launch_compress(dtype, N, d, k, 1, X, nullptr, nullptr, U, Z, nullptr, st);
 }
 
 // 8 token tiles (128 tokens) per block, each of the 8 waves sweeping the

@@ -169,9 +169,7 @@ static hipError_t project_in_ranges(ssn_dtype_t dtype, int64_t N, int64_t dx, in
                                     int64_t row_bytes, hipStream_t st) {
   int64_t smax = aligned_to(scratch, 4) ? row_bytes / (k * 4) : 1;
   smax = smax < kReparamMaxRanges ? smax : kReparamMaxRanges;
-  const int S = ssn::project_split_count(dtype, N, dx, k, (int)smax);
-  if (S > 1) return ssn::launch_project_ranges(N, dx, k, X, W, Z, (float*)scratch, S, st);
-  return ssn::launch_compress(dtype, N, dx, k, 1, X, nullptr, nullptr, W, Z, nullptr, st);
+  return ssn::launch_project_ranges(dtype, N, dx, k, X, W, Z, (float*)scratch, (int)smax, st);
 }
 
 ssn_status_t ssn_reparam_forward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,

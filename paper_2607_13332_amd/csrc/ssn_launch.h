@@ -23,12 +23,11 @@ bool weights_use_mfma(int dtype, int64_t d, int64_t k);
 hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                            const int32_t* ids, const void* E, const void* U, float* Z,
                            const float* P, hipStream_t st);
-// Ranges of d (1 = none) for Z = X.U with few tokens, at most smax; with
-// S > 1, launch_project_ranges writes S partial products to ws [S][N][k]
-// (float32, 4-byte aligned) and sums them into Z.
-int project_split_count(int dtype, int64_t N, int64_t d, int64_t k, int smax);
-hipError_t launch_project_ranges(int64_t N, int64_t d, int64_t k, const void* X, const void* U,
-                                 float* Z, float* ws, int S, hipStream_t st);
+// Z = X.U (no E, no P).  With few tokens it may split d into up to smax
+// ranges whose partial products go to ws [S][N][k] (float32, S <= smax,
+// written before Z) and are summed into Z; ws NULL or smax <= 1: one launch.
+hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, const void* X,
+                                 const void* U, float* Z, float* ws, int smax, hipStream_t st);
 // E non-NULL: Y = E[ids] + Z U^T; gather_z: Y = Z[ids] U^T; else Y = Z U^T.
 hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const float* Z,
                              const int32_t* ids, const void* E, const void* U, void* Y,

@@ -26,13 +26,11 @@ hipError_t launch_decompress(int, int64_t, int64_t, int64_t, int64_t, const floa
   ++g_launches;
   return hipSuccess;
 }
-// splits whenever the staging memory allows (exercises both host paths)
-int project_split_count(int dtype, int64_t, int64_t, int64_t, int smax) {
-  return dtype == kBF16 && smax >= 2 ? 2 : 1;
-}
-hipError_t launch_project_ranges(int64_t, int64_t, int64_t, const void*, const void*, float*, float*,
-                                 int, hipStream_t) {
-  g_launches += 2;
+// two launches when the staging memory allows ranges (the real launcher
+// writes ws only then)
+hipError_t launch_project_ranges(int dtype, int64_t, int64_t, int64_t, const void*, const void*,
+                                 float*, float* ws, int smax, hipStream_t) {
+  g_launches += (dtype == kBF16 && ws && smax >= 2) ? 2 : 1;
   return hipSuccess;
 }
 size_t factor_grad_workspace_bytes(int dtype, int64_t N, int64_t din, int64_t k) {

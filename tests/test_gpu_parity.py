@@ -194,6 +194,8 @@ CODEC_SHAPES = [  # (N, d, k): tiles, ragged tails, every k bucket, both familie
     # enough 128-token tiles to fill 256 compute units, with ragged tails: the
     # rotated 8-wave row kernel and the full-d decompress blocks
     (33325, 256, 64), (33325, 384, 32), (20000, 640, 48),
+    # few-token projections with two token tiles per wave
+    (5000, 1024, 64), (4500, 2048, 51),
 ]
 
 
@@ -328,6 +330,8 @@ REPARAM_SHAPES = [  # (N, din, d, k, dtype): every kernel family and tail
     # two to four ranges staged in the output's memory
     (1000, 3072, 1024, 40, "bf16"), (777, 1536, 2048, 51, "bf16"), (1024, 1024, 1024, 128, "bf16"),
     (6144, 3072, 1536, 51, "bf16"),
+    # two token tiles per wave, in two to four ranges (k = 24, 40, 51)
+    (2500, 1536, 1024, 51, "bf16"), (5000, 2048, 1024, 40, "bf16"), (3000, 1024, 1024, 24, "bf16"),
 ]
 
 
