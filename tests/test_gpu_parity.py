@@ -358,6 +358,41 @@ def test_reparam_shapes(N, din, d, k, dtype):
     assert torch.equal(GZ, GZ2)
 
 
+def test_reparam_staging_memory_alignment():
+    """With few tokens the projections stage partial products over ranges of
+    the inner dimension in the output's memory (Y forward, dL/dH backward).
+    Outputs only 2-byte aligned take the single-launch path instead; both
+    paths match the oracle, and each is deterministic."""
+    N, din, d, k = 4096, 2048, 1024, 51
+    print(f"[case] reparam staging alignment N={N} din={din} d={d} k={k}", flush=True)
+    r = np.random.default_rng(77)
+    Hh = I.store(r.standard_normal((N, din)), "bf16")
+    Zh = I.store(0.05 * r.standard_normal((din, k)), "bf16")
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, 77), "bf16")
+    Gh = I.store(r.standard_normal((N, d)), "bf16")
+    H, Zp, U, G = dev(Hh, "bf16"), dev(Zh, "bf16"), dev(Uh, "bf16"), dev(Gh, "bf16")
+    T_ref, Y_ref = O.project_grad(Hh, Zh), O.reparam_forward(Hh, Zh, Uh)
+    GT_ref, GH_ref = O.project_grad(Gh, Uh), O.reparam_grad_input(Gh, Zh, Uh)
+    ybuf = torch.empty(N * d + 1, dtype=torch.bfloat16, device=DEV)
+    hbuf = torch.empty(N * din + 1, dtype=torch.bfloat16, device=DEV)
+    outs = {}
+    for off in (0, 1):                       # 0: 4-byte aligned (ranges), 1: 2-byte aligned
+        Y = ybuf[off:off + N * d].view(N, d)
+        GH = hbuf[off:off + N * din].view(N, din)
+        T, _ = ssn.reparam_forward(H, Zp, U, Y=Y)
+        check(f"T (offset {off})", host(T), T_ref, "bf16", "f32out")
+        check(f"Y (offset {off})", host(Y), Y_ref, "bf16", "bf16out")
+        GT, _, _ = ssn.reparam_backward(H, Zp, U, G, GH=GH)
+        check(f"GT (offset {off})", host(GT), GT_ref, "bf16", "f32out")
+        check(f"dL/dH (offset {off})", host(GH), GH_ref, "bf16", "bf16out")
+        T2, _ = ssn.reparam_forward(H, Zp, U, Y=Y)
+        GT2, _, _ = ssn.reparam_backward(H, Zp, U, G, GH=GH)
+        assert torch.equal(T, T2) and torch.equal(GT, GT2)
+        outs[off] = (T, GT)
+    # the two paths sum the inner dimension in different groupings
+    assert not torch.equal(outs[0][0], outs[1][0]) or not torch.equal(outs[0][1], outs[1][1])
+
+
 @pytest.mark.parametrize("N,din,d,k", [(4096, 18432, 5120, 51), (32768, 14336, 4096, 64)],
                          ids=["paper8b", "stage8b"])
 def test_reparam_paper_shape_sampled(N, din, d, k):
