@@ -287,10 +287,11 @@ def time_sparta(cfg, steps: int, dev):
     return out
 
 
-def time_step_graph(sets, step_fn, steps: int) -> float:
+def time_step_graph(sets, step_fn, steps: int, warmup: int) -> float:
     """ms per step when each input set's step is captured once as a HIP graph
     and replayed (the library launches kernels only: no allocation, no
-    memset, so a whole step captures)."""
+    memset, so a whole step captures).  The untimed replays let the clocks
+    settle again after the idle time of the capture."""
     import torch
     graphs = []
     for s in sets:
@@ -298,8 +299,8 @@ def time_step_graph(sets, step_fn, steps: int) -> float:
         with torch.cuda.graph(g):
             step_fn(s)
         graphs.append(g)
-    for g in graphs:
-        g.replay()
+    for i in range(max(warmup, len(graphs))):
+        graphs[i % len(graphs)].replay()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
@@ -372,7 +373,7 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         step_bytes += byts
         per_op[op] = {"ms": round(t, 5), "algorithmic_GBps": round(byts / (t * 1e-3) / 1e9, 1),
                       "frac_hbm_peak": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-    gms = time_step_graph(sets, lambda s: step(s, None), steps)
+    gms = time_step_graph(sets, lambda s: step(s, None), steps, warmup)
     out = {"workload": f"N={N} (B={cfg.B} x S={cfg.S}), d={d}, k={k}, V={cfg.V}, bf16, "
                        f"{cfg.ids_dist} ids",
            "ms_per_step": round(ms, 5), "tokens_per_s": round(N / (ms * 1e-3), 1),
@@ -572,7 +573,7 @@ def main():
         "step_with_projected_compress": {"ms_per_step": round(ms2, 5),
                                          "tokens_per_s": round(N / (ms2 * 1e-3), 1)},
     }
-    gms = time_step_graph(sets, step, args.steps)
+    gms = time_step_graph(sets, step, args.steps, args.warmup)
     result["variants"]["step_hip_graph"] = {
         "what": "the same four ops captured once per input set as a HIP graph and replayed",
         "ms_per_step": round(gms, 5), "tokens_per_s": round(N / (gms * 1e-3), 1)}

@@ -892,9 +892,10 @@ static hipError_t launch_split_t(int64_t N, int d, int k, int64_t V, const void*
                      k, V, Pt)
   // odd k (measured at d = 5120 and 18432, k = 51): the shuffled windows win
   // when two token tiles share each U chunk, or with eight waves and d up to
-  // 8192; otherwise the span scatter
+  // 8192; otherwise the span scatter, except for compress with eight waves,
+  // where the scatter's registers beside the E rows would spill
   if (k % 8 == 0) SSN_SPLIT(0);
-  else if constexpr (TTW == 2) SSN_SPLIT(1);
+  else if constexpr (TTW == 2 || (P == 8 && HAS_E)) SSN_SPLIT(1);
   else if constexpr (P == 8) {
     if (d <= 8192) SSN_SPLIT(1);
     else SSN_SPLIT(2);

@@ -14,26 +14,29 @@
 namespace ssn {
 
 constexpr int kFgRows = 32;      // tokens per chunk (one K step)
-constexpr int kFgTiles = 32;     // 16-column tiles of din per block (512 columns)
+// 16-column tiles of din per block: 32 (512 columns) for k <= 64; 16 for
+// k > 64, whose accumulators for 32 tiles would not fit in the registers of
+// two waves per SIMD (they spilled)
+constexpr int fg_tiles(int kt) { return kt > 4 ? 16 : 32; }
 constexpr int kFgThreads = 512;  // 8 waves, four tiles each
 constexpr int kFgTargetBlocks = 256;
 constexpr int kFgDepth = 2;      // chunks in flight in registers (3 measured slower)
 
 // ===========================================================================
 // MFMA kernel, bf16 H.  Block (column block x, token split y) owns din
-// columns [512x, 512x + 512) and tokens [y*tps, (y+1)*tps).  Per chunk of 32
-// tokens the block loads H rows (16-byte pieces; thread t moves piece t mod
-// 64 of rows t/64 + 8i) into a row-major LDS tile, and GT rows split into
+// columns [16 TILES x, 16 TILES (x + 1)) (512 columns for k <= 64) and
+// tokens [y*tps, (y+1)*tps).  Per chunk of 32 tokens the block loads H rows
+// (16-byte pieces, 2 TILES per row) into a row-major LDS tile, and GT rows split into
 // bf16 hi + lo parts into two row-major LDS tiles (zero past k).  Both MFMA
 // operands are token-contiguous fragments read with LDS transpose reads:
 // A = H^T (16 din x 32 tokens), B = GT (32 tokens x 16 of k), two MFMAs per
 // pair (hi, lo) so GT keeps ~fp32 accuracy.  Wave w owns tiles w + 8j for
 // all of k.  The wide column block makes each block's GT rows serve 512
-// columns (GT comes from L2 once per 512 columns).  The block writes its
+// columns (GT comes from L2 once per block).  The block writes its
 // partial sums for its token split; a second kernel adds the splits in order
 // (deterministic).
 // ===========================================================================
-// FULL: every block owns kFgTiles whole tiles, every split a whole number of
+// FULL: every block owns TILES whole tiles, every split a whole number of
 // chunks and every GT chunk is whole 16-byte pieces for all threads (k a
 // multiple of 64).  Then every load is issued unconditionally (the prefetch
 // past the last chunk re-reads the last chunk): with conditional loads the
@@ -45,8 +48,9 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
                                                                float* __restrict__ out, int64_t N,
                                                                int din, int k, int64_t tps) {
   constexpr int R = kFgRows, NT = kFgThreads, NW = NT / kWave;
-  constexpr int CT = kFgTiles / NW;                    // tiles per wave
-  constexpr int HP = 2 * kFgTiles, WP = HP + 1;      // H pieces per row, pitch in pieces
+  constexpr int TILES = fg_tiles(KT);
+  constexpr int CT = TILES / NW;                       // tiles per wave
+  constexpr int HP = 2 * TILES, WP = HP + 1;           // H pieces per row, pitch in pieces
   constexpr int RP = NT / HP;                          // H rows per pass
   constexpr int KS2 = (KT + 1) / 2, KW = 32 * KS2;   // GT tile width (bf16)
   constexpr int GPI = KW + 8;                          // GT tile pitch (bf16)
@@ -58,8 +62,8 @@ __global__ __launch_bounds__(kFgThreads) void factor_grad_bf16(const uint16_t* _
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = lane & 15, g = lane >> 4;
-  const int col0 = (int)blockIdx.x * 16 * kFgTiles;
-  const int tcount = min(kFgTiles, din / 16 - (int)blockIdx.x * kFgTiles);
+  const int col0 = (int)blockIdx.x * 16 * TILES;
+  const int tcount = min(TILES, din / 16 - (int)blockIdx.x * TILES);
   const int64_t t_begin = (int64_t)blockIdx.y * tps;
   const int64_t t_end = min(N, t_begin + tps);
   const int nch = (int)((t_end - t_begin + R - 1) / R);
@@ -246,11 +250,14 @@ static bool factor_grad_uses_mfma(int dtype, int64_t din, int64_t k) {
   return dtype == kBF16 && din % 16 == 0 && din <= INT32_MAX / 2 && k >= 1 && k <= 128;
 }
 
+static int fg_tiles_for_k(int64_t k) { return fg_tiles((int)((k + 15) / 16)); }
+
 // Token splits: as many as keep the grid within one round of one block per
 // compute unit of an MI355X (256), at least one chunk of tokens per split.
-// Depends on (N, din) only, so results are the same on every device.
-static int64_t factor_grad_splits(int64_t N, int64_t din) {
-  const int64_t cb = (din / 16 + kFgTiles - 1) / kFgTiles;
+// Depends on (N, din, k) only, so results are the same on every device.
+static int64_t factor_grad_splits(int64_t N, int64_t din, int64_t k) {
+  const int tiles = fg_tiles_for_k(k);
+  const int64_t cb = (din / 16 + tiles - 1) / tiles;
   int64_t S = kFgTargetBlocks / cb;
   const int64_t chunks = (N + kFgRows - 1) / kFgRows;
   S = S > chunks ? chunks : S;
@@ -259,18 +266,19 @@ static int64_t factor_grad_splits(int64_t N, int64_t din) {
 
 size_t factor_grad_workspace_bytes(int dtype, int64_t N, int64_t din, int64_t k) {
   if (!factor_grad_uses_mfma(dtype, din, k)) return 0;
-  const int64_t S = factor_grad_splits(N, din);
+  const int64_t S = factor_grad_splits(N, din, k);
   return S > 1 ? (size_t)S * (size_t)din * (size_t)k * sizeof(float) : 0;
 }
 
 template <int KT>
 static hipError_t launch_factor_grad_kt(int64_t N, int din, int k, const void* H, const float* GT,
                                         float* dst, int64_t S, int64_t tps, hipStream_t st) {
-  const dim3 grid((unsigned)((din / 16 + kFgTiles - 1) / kFgTiles), (unsigned)S);
+  constexpr int TILES = fg_tiles(KT);
+  const dim3 grid((unsigned)((din / 16 + TILES - 1) / TILES), (unsigned)S);
   const bool k4 = k % 4 == 0 && ((uintptr_t)GT & 15u) == 0;
   // whole tiles, whole chunks in every split (tps is a multiple of the
   // chunk), and k filling the K slots of its tile bucket
-  const bool full = k4 && din % (16 * kFgTiles) == 0 && N % kFgRows == 0 && k == 32 * ((KT + 1) / 2);
+  const bool full = k4 && din % (16 * TILES) == 0 && N % kFgRows == 0 && k == 32 * ((KT + 1) / 2);
   if (full)
     hipLaunchKernelGGL((factor_grad_bf16<KT, true, true, true>), grid, dim3(kFgThreads), 0, st,
                        (const uint16_t*)H, GT, dst, N, din, k, tps);
@@ -286,7 +294,7 @@ static hipError_t launch_factor_grad_kt(int64_t N, int din, int k, const void* H
 hipError_t launch_factor_grad(int dtype, int64_t N, int64_t din, int64_t k, const void* H,
                               const float* GT, float* dZp, float* ws, hipStream_t st) {
   if (factor_grad_uses_mfma(dtype, din, k) && ((uintptr_t)H & 15u) == 0) {
-    const int64_t S = factor_grad_splits(N, din);
+    const int64_t S = factor_grad_splits(N, din, k);
     const int64_t chunks = (N + kFgRows - 1) / kFgRows;
     const int64_t tps = ((chunks + S - 1) / S) * kFgRows;
     float* dst = S > 1 ? ws : dZp;

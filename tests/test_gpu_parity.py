@@ -332,6 +332,9 @@ REPARAM_SHAPES = [  # (N, din, d, k, dtype): every kernel family and tail
     (6144, 3072, 1536, 51, "bf16"),
     # two token tiles per wave, in two to four ranges (k = 24, 40, 51)
     (2500, 1536, 1024, 51, "bf16"), (5000, 2048, 1024, 40, "bf16"), (3000, 1024, 1024, 24, "bf16"),
+    # k > 64 with k % 4 != 0: the factor gradient's element-wise G U staging
+    # on 256-column blocks
+    (500, 1024, 512, 97, "bf16"),
 ]
 
 
