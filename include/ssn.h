@@ -135,6 +135,27 @@ ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k
                               const void *G, const void *U, float *GZ, void *stream);
 
 /*
+ * Coordinate dtype on the wire.  The paper sizes the boundary traffic with
+ * activations sent in FP32 (section 3.5.2, its estimate of per-node
+ * communication), which the three entry points above keep.  These variants take the dtype of Z (or GZ) as
+ * `z_dtype`: SSN_F32 gives exactly the entry points above; SSN_BF16 halves
+ * the message.  Compress / project_grad then round each fp32 result once to
+ * bf16 (nearest even) as they store it; decompress reads bf16 coordinates,
+ * which are exact in its fp32 arithmetic, so decompress_ex(compress_ex(X))
+ * differs from the fp32 round trip only by the coordinate rounding.  Z is
+ * `void *` [N, k] of z_dtype, aligned to its element size; otherwise the
+ * arguments, validation and error codes are those of the entry points above.
+ */
+ssn_status_t ssn_compress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
+                             int64_t k, int64_t V, const void *X, const int32_t *ids,
+                             const void *E, const void *U, void *Z, void *stream);
+ssn_status_t ssn_decompress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
+                               int64_t k, int64_t V, const void *Z, const int32_t *ids,
+                               const void *E, const void *U, void *Xout, void *stream);
+ssn_status_t ssn_project_grad_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
+                                 int64_t k, const void *G, const void *U, void *GZ, void *stream);
+
+/*
  * ssn_project_table -- the fixed token embedding projected onto the basis,
  * once:  P[v, :] = E[v, :] . U  for v in [0, V).
  *   E [V, d] dtype, U [d, k] dtype, P [V, k] float32 output

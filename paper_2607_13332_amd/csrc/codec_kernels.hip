@@ -116,7 +116,8 @@ template <int KP, bool HAS_E, bool KFULL, int WAVES = 8, int DEPTH = 1, bool NTX
 __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
-    float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ P) {
+    float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ P,
+    uint16_t* __restrict__ Zb) {
   static_assert(DEPTH >= 1 && DEPTH <= 4, "one to four chunks of rows in flight");
   static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
   constexpr int KS = 4, DC = 128;
@@ -247,14 +248,28 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
             if (col0 + i < k) v[i] -= pp[i];
         }
       }
-      float* zp = Z + tj * k + col0;
-      if constexpr (KFULL && KP % 4 == 0) {
+      if (Zb) {
+        // bf16 coordinates: rounded once, to nearest even
+        uint16_t* zb = Zb + tj * k + col0;
+        if constexpr (KFULL && KP % 4 == 0) {
 #pragma unroll
-        for (int i = 0; i < KP; i += 4) *(f32x4*)(zp + i) = f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
+          for (int i = 0; i < KP; i += 4)
+            *(u32x2*)(zb + i) = u32x2{pack_bf16x2(v[i], v[i + 1]), pack_bf16x2(v[i + 2], v[i + 3])};
+        } else {
+#pragma unroll
+          for (int i = 0; i < KP; ++i)
+            if (col0 + i < k) zb[i] = (uint16_t)f32_to_bf16(v[i]);
+        }
       } else {
+        float* zp = Z + tj * k + col0;
+        if constexpr (KFULL && KP % 4 == 0) {
 #pragma unroll
-        for (int i = 0; i < KP; ++i)
-          if (col0 + i < k) zp[i] = v[i];
+          for (int i = 0; i < KP; i += 4) *(f32x4*)(zp + i) = f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
+        } else {
+#pragma unroll
+          for (int i = 0; i < KP; ++i)
+            if (col0 + i < k) zp[i] = v[i];
+        }
       }
     }
   }
@@ -289,7 +304,8 @@ template <int KP, bool HAS_E, bool HAS_P, int UM, int P, int TTW>
 __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) void compress_split_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
-    float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ Pt) {
+    float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ Pt,
+    uint16_t* __restrict__ Zb) {
   static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
   static_assert(UM >= 0 && UM <= 2, "U staging mode");
   constexpr bool KV = (UM == 0);
@@ -473,7 +489,10 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
         if (t < N) {
           float v = sum[e];
           if constexpr (HAS_P) v -= Pt[clamp_id(ids[t], V) * k + col];
-          Z[t * k + col] = v;
+          if (Zb)
+            Zb[t * k + col] = (uint16_t)f32_to_bf16(v);
+          else
+            Z[t * k + col] = v;
         }
       }
     }
@@ -513,7 +532,8 @@ template <int KS2, bool HAS_E, int KM, int DC = kDecompressDC, int DSPLIT = 1, i
 __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
-    uint16_t* __restrict__ Y, int64_t N, int d, int k, int64_t V) {
+    uint16_t* __restrict__ Y, int64_t N, int d, int k, int64_t V,
+    const uint16_t* __restrict__ Zb) {
   static_assert(DC == 64 || DC == 128, "chunk of 64 or 128 d");
   static_assert(KM >= 0 && KM <= 2, "k layout mode");
   static_assert(!(HAS_E && GZ), "gathered coordinates carry no additive embedding");
@@ -539,12 +559,32 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
   {
     int64_t t = tok0 + n16;
     t = t < N ? t : N - 1;
-    const float* zp = Zc + (GZ ? clamp_id(ids[t], V) : t) * k;
+    const int64_t zrow = (GZ ? clamp_id(ids[t], V) : t) * k;
+    // bf16 coordinates when Zb is non-NULL (exact in the hi part; the lo
+    // part is zero), else float32 ones from Zc
+    const bool zb16 = Zb != nullptr;
+    const float* zp = zb16 ? nullptr : Zc + zrow;
+    const uint16_t* zq = zb16 ? Zb + zrow : nullptr;
 #pragma unroll
     for (int s = 0; s < KS2; ++s) {
       const int c0 = 32 * s + 8 * g;
       float v[8];
-      if constexpr (KM == 2) {
+      if (zb16) {
+        if constexpr (KM == 2) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = (c0 + e < k) ? bf16_to_f32(zq[c0 + e]) : 0.f;
+        } else if (KFULL32 || c0 + 8 <= k) {
+          const u32x4 a = *(const u32x4*)(zq + c0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] = bf16_to_f32(a[e] & 0xFFFFu);
+            v[2 * e + 1] = bf16_to_f32(a[e] >> 16);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = 0.f;
+        }
+      } else if constexpr (KM == 2) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = (c0 + e < k) ? zp[c0 + e] : 0.f;
       } else if (KFULL32 || c0 + 8 <= k) {
@@ -761,7 +801,7 @@ template <typename T, bool HAS_E, bool HAS_P = false>
 __global__ __launch_bounds__(256) void compress_generic(
     const T* __restrict__ X, const int32_t* __restrict__ ids, const T* __restrict__ E,
     const T* __restrict__ U, float* __restrict__ Z, int64_t N, int64_t d, int64_t k, int64_t V,
-    const float* __restrict__ P) {
+    const float* __restrict__ P, uint16_t* __restrict__ Zb) {
   const int lane = threadIdx.x & 63;
   const int64_t nw = (int64_t)gridDim.x * 4;
   for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < N; t += nw) {
@@ -786,7 +826,10 @@ __global__ __launch_bounds__(256) void compress_generic(
       }
       if (lane < 16 && kc + lane < k) {
         if constexpr (HAS_P) mine -= P[clamp_id(ids[t], V) * k + kc + lane];
-        Z[t * k + kc + lane] = mine;
+        if (Zb)
+          Zb[t * k + kc + lane] = (uint16_t)f32_to_bf16(mine);
+        else
+          Z[t * k + kc + lane] = mine;
       }
     }
   }
@@ -795,16 +838,22 @@ __global__ __launch_bounds__(256) void compress_generic(
 template <typename T, bool HAS_E, bool GZ = false>
 __global__ __launch_bounds__(256) void decompress_generic(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids, const T* __restrict__ E,
-    const T* __restrict__ U, T* __restrict__ Y, int64_t N, int64_t d, int64_t k, int64_t V) {
+    const T* __restrict__ U, T* __restrict__ Y, int64_t N, int64_t d, int64_t k, int64_t V,
+    const uint16_t* __restrict__ Zb) {
   const int lane = threadIdx.x & 63;
   const int64_t nw = (int64_t)gridDim.x * 4;
   for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < N; t += nw) {
-    const float* zr = Zc + (GZ ? clamp_id(ids[t], V) : t) * k;
+    const int64_t zrow = (GZ ? clamp_id(ids[t], V) : t) * k;
+    const float* zr = Zb ? nullptr : Zc + zrow;
+    const uint16_t* zq = Zb ? Zb + zrow : nullptr;
     const T* er = HAS_E ? E + clamp_id(ids[t], V) * d : nullptr;
     for (int64_t j = lane; j < d; j += 64) {
       float acc = HAS_E ? load_as_f32(er + j) : 0.f;
       const T* ur = U + j * k;
-      for (int64_t c = 0; c < k; ++c) acc = fmaf(zr[c], load_as_f32(ur + c), acc);
+      if (Zb)
+        for (int64_t c = 0; c < k; ++c) acc = fmaf(bf16_to_f32(zq[c]), load_as_f32(ur + c), acc);
+      else
+        for (int64_t c = 0; c < k; ++c) acc = fmaf(zr[c], load_as_f32(ur + c), acc);
       store_from_f32(Y + t * d + j, acc);
     }
   }
@@ -833,17 +882,17 @@ bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) {
 template <int KP, bool HAS_E, bool KFULL, bool HAS_P>
 static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const void* X,
                                        const int32_t* ids, const void* E, const void* U, float* Z,
-                                       const float* P, hipStream_t st) {
+                                       const float* P, hipStream_t st, uint16_t* Zb) {
   if ((N + 127) / 128 >= device_cu_count()) {
     const int64_t blocks = (N + 127) / 128;
     hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 8, 1, true, false, true, 4, HAS_P>),
                        dim3((unsigned)blocks), dim3(512), 0, st, (const uint16_t*)X, ids,
-                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P);
+                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P, Zb);
   } else {
     const int64_t blocks = (N + 63) / 64;
     hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 4, 1, true, false, false, 1, HAS_P>),
                        dim3((unsigned)blocks), dim3(256), 0, st, (const uint16_t*)X, ids,
-                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P);
+                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P, Zb);
   }
   return hipGetLastError();
 }
@@ -853,24 +902,25 @@ static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const
 template <int KP, bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_kp(int64_t N, int d, int k, int64_t V, const void* X,
                                      const int32_t* ids, const void* E, const void* U, float* Z,
-                                     const float* P, hipStream_t st) {
-  return k == 16 * KP ? launch_compress_rows<KP, HAS_E, true, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st)
-                      : launch_compress_rows<KP, HAS_E, false, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+                                     const float* P, hipStream_t st, uint16_t* Zb) {
+  return k == 16 * KP
+             ? launch_compress_rows<KP, HAS_E, true, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb)
+             : launch_compress_rows<KP, HAS_E, false, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
 }
 
 template <bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_mfma(int64_t N, int d, int k, int64_t V, const void* X,
                                        const int32_t* ids, const void* E, const void* U, float* Z,
-                                       const float* P, hipStream_t st) {
+                                       const float* P, hipStream_t st, uint16_t* Zb) {
   switch ((k + 15) / 16) {
-    case 1: return launch_compress_kp<1, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
-    case 2: return launch_compress_kp<2, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
-    case 3: return launch_compress_kp<3, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
-    case 4: return launch_compress_kp<4, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
-    case 5: return launch_compress_kp<5, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
-    case 6: return launch_compress_kp<6, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
-    case 7: return launch_compress_kp<7, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
-    default: return launch_compress_kp<8, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st);
+    case 1: return launch_compress_kp<1, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    case 2: return launch_compress_kp<2, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    case 3: return launch_compress_kp<3, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    case 4: return launch_compress_kp<4, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    case 5: return launch_compress_kp<5, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    case 6: return launch_compress_kp<6, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    case 7: return launch_compress_kp<7, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    default: return launch_compress_kp<8, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
   }
 }
 
@@ -884,12 +934,12 @@ static unsigned generic_blocks(int64_t N) {
 template <int KP, bool HAS_E, bool HAS_P, int P, int TTW>
 static hipError_t launch_split_t(int64_t N, int d, int k, int64_t V, const void* X,
                                  const int32_t* ids, const void* E, const void* U, float* Z,
-                                 const float* Pt, hipStream_t st, int S) {
+                                 const float* Pt, hipStream_t st, int S, uint16_t* Zb) {
   const dim3 grid((unsigned)((N + 16 * TTW - 1) / (16 * TTW)), (unsigned)S);
 #define SSN_SPLIT(UM)                                                                           \
   hipLaunchKernelGGL((compress_split_bf16<KP, HAS_E, HAS_P, UM, P, TTW>), grid, dim3(64 * P), 0, \
                      st, (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d, \
-                     k, V, Pt)
+                     k, V, Pt, Zb)
   // odd k (measured at d = 5120 and 18432, k = 51): the shuffled windows win
   // when two token tiles share each U chunk, or with eight waves and d up to
   // 8192; otherwise the span scatter, except for compress with eight waves,
@@ -907,17 +957,17 @@ static hipError_t launch_split_t(int64_t N, int d, int k, int64_t V, const void*
 template <int KP, bool HAS_E, bool HAS_P>
 static hipError_t launch_split_kp(int P, int TTW, int64_t N, int d, int k, int64_t V, const void* X,
                                   const int32_t* ids, const void* E, const void* U, float* Z,
-                                  const float* Pt, hipStream_t st, int S) {
+                                  const float* Pt, hipStream_t st, int S, uint16_t* Zb) {
   if constexpr (KP <= 4) {
     if constexpr (!HAS_E)
       if (P == 8 && TTW == 2)
-        return launch_split_t<KP, HAS_E, HAS_P, 8, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
-    if (P == 8) return launch_split_t<KP, HAS_E, HAS_P, 8, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
+        return launch_split_t<KP, HAS_E, HAS_P, 8, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
+    if (P == 8) return launch_split_t<KP, HAS_E, HAS_P, 8, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
     if (P == 4 && TTW == 2)
-      return launch_split_t<KP, HAS_E, HAS_P, 4, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
+      return launch_split_t<KP, HAS_E, HAS_P, 4, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
   }
-  if (P >= 4) return launch_split_t<KP, HAS_E, HAS_P, 4, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
-  return launch_split_t<KP, HAS_E, HAS_P, 2, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S);
+  if (P >= 4) return launch_split_t<KP, HAS_E, HAS_P, 4, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
+  return launch_split_t<KP, HAS_E, HAS_P, 2, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
 }
 
 // When the d-split kernel runs (measured on MI355X at d = 4096 and 5120):
@@ -987,12 +1037,12 @@ static SplitPlan split_plan(int64_t N, int d, int k, bool has_e, int smax) {
 template <bool HAS_E, bool HAS_P>
 static hipError_t launch_split(int64_t N, int d, int k, int64_t V, const void* X, const int32_t* ids,
                                const void* E, const void* U, float* Z, const float* Pt,
-                               hipStream_t st, const SplitPlan& p) {
+                               hipStream_t st, const SplitPlan& p, uint16_t* Zb = nullptr) {
   if (k <= 32)
-    return launch_split_kp<2, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S);
+    return launch_split_kp<2, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb);
   if (k <= 64)
-    return launch_split_kp<4, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S);
-  return launch_split_kp<8, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S);
+    return launch_split_kp<4, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb);
+  return launch_split_kp<8, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb);
 }
 
 // Sum of S partial results [S][n], in range order (deterministic).
@@ -1009,37 +1059,39 @@ __global__ __launch_bounds__(256) void sum_partials(const float* __restrict__ ws
 template <typename T, bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_generic(int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                                           const int32_t* ids, const void* E, const void* U,
-                                          float* Z, const float* P, hipStream_t st) {
+                                          float* Z, const float* P, hipStream_t st, uint16_t* Zb) {
   hipLaunchKernelGGL((compress_generic<T, HAS_E, HAS_P>), dim3(generic_blocks(N)), dim3(256), 0, st,
-                     (const T*)X, ids, (const T*)E, (const T*)U, Z, N, d, k, V, P);
+                     (const T*)X, ids, (const T*)E, (const T*)U, Z, N, d, k, V, P, Zb);
   return hipGetLastError();
 }
 
 // E non-NULL: Z = (X - E[ids]).U; P non-NULL: Z = X.U - P[ids]; neither: Z = X.U.
+// Zb non-NULL: the coordinates go to Zb in bf16 (Z unused).
 hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                            const int32_t* ids, const void* E, const void* U, float* Z,
-                           const float* P, hipStream_t st) {
+                           const float* P, hipStream_t st, uint16_t* Zb) {
   const bool has_e = (E != nullptr), has_p = (P != nullptr);
-  if (compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(Z) && (!has_e || al16(E)) &&
+  const void* zout = Zb ? (const void*)Zb : (const void*)Z;
+  if (compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(zout) && (!has_e || al16(E)) &&
       (!has_p || al16(P))) {
     if (compress_uses_split(N, d, k, has_e)) {
       const SplitPlan sp = split_plan(N, (int)d, (int)k, has_e, 1);
-      if (has_e) return launch_split<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp);
-      if (has_p) return launch_split<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp);
-      return launch_split<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp);
+      if (has_e) return launch_split<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp, Zb);
+      if (has_p) return launch_split<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp, Zb);
+      return launch_split<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp, Zb);
     }
-    if (has_e) return launch_compress_mfma<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
-    if (has_p) return launch_compress_mfma<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
-    return launch_compress_mfma<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st);
+    if (has_e) return launch_compress_mfma<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, Zb);
+    if (has_p) return launch_compress_mfma<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, Zb);
+    return launch_compress_mfma<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, Zb);
   }
   if (dtype == kF32) {
-    if (has_e) return launch_compress_generic<float, true, false>(N, d, k, V, X, ids, E, U, Z, P, st);
-    if (has_p) return launch_compress_generic<float, false, true>(N, d, k, V, X, ids, E, U, Z, P, st);
-    return launch_compress_generic<float, false, false>(N, d, k, V, X, ids, E, U, Z, P, st);
+    if (has_e) return launch_compress_generic<float, true, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    if (has_p) return launch_compress_generic<float, false, true>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    return launch_compress_generic<float, false, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
   }
-  if (has_e) return launch_compress_generic<uint16_t, true, false>(N, d, k, V, X, ids, E, U, Z, P, st);
-  if (has_p) return launch_compress_generic<uint16_t, false, true>(N, d, k, V, X, ids, E, U, Z, P, st);
-  return launch_compress_generic<uint16_t, false, false>(N, d, k, V, X, ids, E, U, Z, P, st);
+  if (has_e) return launch_compress_generic<uint16_t, true, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+  if (has_p) return launch_compress_generic<uint16_t, false, true>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+  return launch_compress_generic<uint16_t, false, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
 }
 
 // Z = X.U; with few tokens the few-token kernel may split d into up to
@@ -1059,7 +1111,7 @@ hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, con
       return hipGetLastError();
     }
   }
-  return launch_compress(dtype, N, d, k, 1, X, nullptr, nullptr, U, Z, nullptr, st);
+  return launch_compress(dtype, N, d, k, 1, X, nullptr, nullptr, U, Z, nullptr, st, nullptr);
 }
 
 // 8 token tiles (128 tokens) per block, each of the 8 waves sweeping the
@@ -1076,7 +1128,7 @@ hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, con
 template <int KS2, bool HAS_E, int KM, bool GZ>
 static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
-                                       hipStream_t st) {
+                                       hipStream_t st, const uint16_t* Zb) {
   constexpr int TW = 8;
   const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
   const int64_t cus = device_cu_count();
@@ -1091,61 +1143,63 @@ static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const
     hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ, false,
                                              1, 2>),
                        grid, dim3(64 * TW), 0, st, Zc, ids, (const uint16_t*)E, (const uint16_t*)U,
-                       (uint16_t*)Y, N, d, k, V);
+                       (uint16_t*)Y, N, d, k, V, Zb);
   else
     hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ>), grid,
                        dim3(64 * TW), 0, st, Zc, ids, (const uint16_t*)E, (const uint16_t*)U,
-                       (uint16_t*)Y, N, d, k, V);
+                       (uint16_t*)Y, N, d, k, V, Zb);
   return hipGetLastError();
 }
 
 template <int KS2, bool HAS_E, bool GZ>
 static hipError_t launch_decompress_ks(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
-                                       hipStream_t st) {
-  if (k == 32 * KS2) return launch_decompress_km<KS2, HAS_E, 0, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
-  if (k % 8 == 0) return launch_decompress_km<KS2, HAS_E, 1, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
-  return launch_decompress_km<KS2, HAS_E, 2, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
+                                       hipStream_t st, const uint16_t* Zb) {
+  if (k == 32 * KS2) return launch_decompress_km<KS2, HAS_E, 0, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+  if (k % 8 == 0) return launch_decompress_km<KS2, HAS_E, 1, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+  return launch_decompress_km<KS2, HAS_E, 2, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
 }
 
 template <bool HAS_E, bool GZ>
 static hipError_t launch_decompress_mfma(int64_t N, int d, int k, int64_t V, const float* Zc,
                                          const int32_t* ids, const void* E, const void* U, void* Y,
-                                         hipStream_t st) {
+                                         hipStream_t st, const uint16_t* Zb) {
   switch ((k + 31) / 32) {
-    case 1: return launch_decompress_ks<1, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
-    case 2: return launch_decompress_ks<2, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
-    case 3: return launch_decompress_ks<3, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
-    default: return launch_decompress_ks<4, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st);
+    case 1: return launch_decompress_ks<1, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+    case 2: return launch_decompress_ks<2, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+    case 3: return launch_decompress_ks<3, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+    default: return launch_decompress_ks<4, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
   }
 }
 
 template <typename T, bool HAS_E, bool GZ>
 static hipError_t launch_decompress_generic(int64_t N, int64_t d, int64_t k, int64_t V,
                                             const float* Zc, const int32_t* ids, const void* E,
-                                            const void* U, void* Y, hipStream_t st) {
+                                            const void* U, void* Y, hipStream_t st,
+                                            const uint16_t* Zb) {
   hipLaunchKernelGGL((decompress_generic<T, HAS_E, GZ>), dim3(generic_blocks(N)), dim3(256), 0, st, Zc,
-                     ids, (const T*)E, (const T*)U, (T*)Y, N, d, k, V);
+                     ids, (const T*)E, (const T*)U, (T*)Y, N, d, k, V, Zb);
   return hipGetLastError();
 }
 
 hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const float* Zc,
                              const int32_t* ids, const void* E, const void* U, void* Y,
-                             bool gather_z, hipStream_t st) {
+                             bool gather_z, hipStream_t st, const uint16_t* Zb) {
   const bool has_e = (E != nullptr);
-  if (decompress_uses_mfma(dtype, d, k) && al16(Zc) && al16(U) && al16(Y) && (!has_e || al16(E))) {
-    if (has_e) return launch_decompress_mfma<true, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st);
-    if (gather_z) return launch_decompress_mfma<false, true>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st);
-    return launch_decompress_mfma<false, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st);
+  const void* zin = Zb ? (const void*)Zb : (const void*)Zc;
+  if (decompress_uses_mfma(dtype, d, k) && al16(zin) && al16(U) && al16(Y) && (!has_e || al16(E))) {
+    if (has_e) return launch_decompress_mfma<true, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb);
+    if (gather_z) return launch_decompress_mfma<false, true>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb);
+    return launch_decompress_mfma<false, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb);
   }
   if (dtype == kF32) {
-    if (has_e) return launch_decompress_generic<float, true, false>(N, d, k, V, Zc, ids, E, U, Y, st);
-    if (gather_z) return launch_decompress_generic<float, false, true>(N, d, k, V, Zc, ids, E, U, Y, st);
-    return launch_decompress_generic<float, false, false>(N, d, k, V, Zc, ids, E, U, Y, st);
+    if (has_e) return launch_decompress_generic<float, true, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+    if (gather_z) return launch_decompress_generic<float, false, true>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+    return launch_decompress_generic<float, false, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
   }
-  if (has_e) return launch_decompress_generic<uint16_t, true, false>(N, d, k, V, Zc, ids, E, U, Y, st);
-  if (gather_z) return launch_decompress_generic<uint16_t, false, true>(N, d, k, V, Zc, ids, E, U, Y, st);
-  return launch_decompress_generic<uint16_t, false, false>(N, d, k, V, Zc, ids, E, U, Y, st);
+  if (has_e) return launch_decompress_generic<uint16_t, true, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+  if (gather_z) return launch_decompress_generic<uint16_t, false, true>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+  return launch_decompress_generic<uint16_t, false, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
 }
 
 }  // namespace ssn

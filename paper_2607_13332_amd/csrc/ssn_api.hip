@@ -67,24 +67,36 @@ const char* ssn_kernel_family(ssn_op_t op, ssn_dtype_t dtype, int64_t d, int64_t
   return mfma ? "mfma" : "generic";
 }
 
-ssn_status_t ssn_compress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
-                          const void* X, const int32_t* ids, const void* E, const void* U,
-                          float* Z, void* stream) {
-  if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;
+// Coordinates in float32 (Z) or bf16 (Zb): the launchers take one of the two.
+static float* z_f32(ssn_dtype_t z_dtype, void* Z) { return z_dtype == SSN_F32 ? (float*)Z : nullptr; }
+static uint16_t* z_b16(ssn_dtype_t z_dtype, void* Z) {
+  return z_dtype == SSN_BF16 ? (uint16_t*)Z : nullptr;
+}
+
+ssn_status_t ssn_compress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
+                             int64_t k, int64_t V, const void* X, const int32_t* ids,
+                             const void* E, const void* U, void* Z, void* stream) {
+  if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
   if (N < 0 || d < 1 || k < 1 || k > d || V < 1) return SSN_ERR_SHAPE;
   if (!mul_ok(N, d) || !mul_ok(V, d) || !mul_ok(d, k) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
   if (N == 0) return SSN_OK;
   if (!X || !ids || !E || !U || !Z) return SSN_ERR_NULL;
-  const int64_t s = elem_size(dtype);
+  const int64_t s = elem_size(dtype), zs = elem_size(z_dtype);
   if (!aligned_to(X, s) || !aligned_to(E, s) || !aligned_to(U, s) || !aligned_to(ids, 4) ||
-      !aligned_to(Z, 4))
+      !aligned_to(Z, zs))
     return SSN_ERR_ALIGN;
-  const Span out = span(Z, N * k * 4);
+  const Span out = span(Z, N * k * zs);
   if (overlap(out, span(X, N * d * s)) || overlap(out, span(E, V * d * s)) ||
       overlap(out, span(U, d * k * s)) || overlap(out, span(ids, N * 4)))
     return SSN_ERR_ALIAS;
-  return launch_status(
-      ssn::launch_compress(dtype, N, d, k, V, X, ids, E, U, Z, nullptr, (hipStream_t)stream));
+  return launch_status(ssn::launch_compress(dtype, N, d, k, V, X, ids, E, U, z_f32(z_dtype, Z),
+                                            nullptr, (hipStream_t)stream, z_b16(z_dtype, Z)));
+}
+
+ssn_status_t ssn_compress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
+                          const void* X, const int32_t* ids, const void* E, const void* U,
+                          float* Z, void* stream) {
+  return ssn_compress_ex(dtype, SSN_F32, N, d, k, V, X, ids, E, U, Z, stream);
 }
 
 ssn_status_t ssn_compress_projected(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
@@ -107,10 +119,10 @@ ssn_status_t ssn_compress_projected(ssn_dtype_t dtype, int64_t N, int64_t d, int
       ssn::launch_compress(dtype, N, d, k, V, X, ids, nullptr, U, Z, P, (hipStream_t)stream));
 }
 
-ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
-                            const float* Z, const int32_t* ids, const void* E, const void* U,
-                            void* Xout, void* stream) {
-  if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;
+ssn_status_t ssn_decompress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
+                               int64_t k, int64_t V, const void* Z, const int32_t* ids,
+                               const void* E, const void* U, void* Xout, void* stream) {
+  if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
   const bool has_e = (E != nullptr);
   if (N < 0 || d < 1 || k < 1 || k > d || (has_e && V < 1)) return SSN_ERR_SHAPE;
   if (!mul_ok(N, d) || !mul_ok(d, k) || !mul_ok(N, k) || (has_e && !mul_ok(V, d)))
@@ -118,31 +130,45 @@ ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, 
   if (N == 0) return SSN_OK;
   if ((E == nullptr) != (ids == nullptr)) return SSN_ERR_NULL;
   if (!Z || !U || !Xout) return SSN_ERR_NULL;
-  const int64_t s = elem_size(dtype);
-  if (!aligned_to(Z, 4) || !aligned_to(U, s) || !aligned_to(Xout, s) ||
+  const int64_t s = elem_size(dtype), zs = elem_size(z_dtype);
+  if (!aligned_to(Z, zs) || !aligned_to(U, s) || !aligned_to(Xout, s) ||
       (has_e && (!aligned_to(E, s) || !aligned_to(ids, 4))))
     return SSN_ERR_ALIGN;
   const Span out = span(Xout, N * d * s);
-  if (overlap(out, span(Z, N * k * 4)) || overlap(out, span(U, d * k * s)) ||
+  if (overlap(out, span(Z, N * k * zs)) || overlap(out, span(U, d * k * s)) ||
       (has_e && (overlap(out, span(E, V * d * s)) || overlap(out, span(ids, N * 4)))))
     return SSN_ERR_ALIAS;
-  return launch_status(ssn::launch_decompress(dtype, N, d, k, has_e ? V : 1, Z, ids, E, U, Xout,
-                                              false, (hipStream_t)stream));
+  void* zm = const_cast<void*>(Z);
+  return launch_status(ssn::launch_decompress(dtype, N, d, k, has_e ? V : 1, z_f32(z_dtype, zm),
+                                              ids, E, U, Xout, false, (hipStream_t)stream,
+                                              z_b16(z_dtype, zm)));
 }
 
-ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, const void* G,
-                              const void* U, float* GZ, void* stream) {
-  if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;
+ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
+                            const float* Z, const int32_t* ids, const void* E, const void* U,
+                            void* Xout, void* stream) {
+  return ssn_decompress_ex(dtype, SSN_F32, N, d, k, V, Z, ids, E, U, Xout, stream);
+}
+
+ssn_status_t ssn_project_grad_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
+                                 int64_t k, const void* G, const void* U, void* GZ, void* stream) {
+  if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
   if (N < 0 || d < 1 || k < 1 || k > d) return SSN_ERR_SHAPE;
   if (!mul_ok(N, d) || !mul_ok(d, k) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
   if (N == 0) return SSN_OK;
   if (!G || !U || !GZ) return SSN_ERR_NULL;
-  const int64_t s = elem_size(dtype);
-  if (!aligned_to(G, s) || !aligned_to(U, s) || !aligned_to(GZ, 4)) return SSN_ERR_ALIGN;
-  const Span out = span(GZ, N * k * 4);
+  const int64_t s = elem_size(dtype), zs = elem_size(z_dtype);
+  if (!aligned_to(G, s) || !aligned_to(U, s) || !aligned_to(GZ, zs)) return SSN_ERR_ALIGN;
+  const Span out = span(GZ, N * k * zs);
   if (overlap(out, span(G, N * d * s)) || overlap(out, span(U, d * k * s))) return SSN_ERR_ALIAS;
-  return launch_status(ssn::launch_compress(dtype, N, d, k, 1, G, nullptr, nullptr, U, GZ,
-                                            nullptr, (hipStream_t)stream));
+  return launch_status(ssn::launch_compress(dtype, N, d, k, 1, G, nullptr, nullptr, U,
+                                            z_f32(z_dtype, GZ), nullptr, (hipStream_t)stream,
+                                            z_b16(z_dtype, GZ)));
+}
+
+ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, const void* G,
+                              const void* U, float* GZ, void* stream) {
+  return ssn_project_grad_ex(dtype, SSN_F32, N, d, k, G, U, GZ, stream);
 }
 
 ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t k, const void* E,

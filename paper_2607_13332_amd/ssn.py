@@ -47,6 +47,15 @@ def _declare(lib):
                                    _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_project_grad.restype = ctypes.c_int
     lib.ssn_project_grad.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_compress_ex.restype = ctypes.c_int
+    lib.ssn_compress_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
+                                    _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_decompress_ex.restype = ctypes.c_int
+    lib.ssn_decompress_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
+                                      _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_project_grad_ex.restype = ctypes.c_int
+    lib.ssn_project_grad_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
+                                        _c_p, _c_p, _c_p, _c_p]
     lib.ssn_project_table.restype = ctypes.c_int
     lib.ssn_project_table.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_compress_projected.restype = ctypes.c_int
@@ -143,26 +152,29 @@ def _same_device(*ts):
 
 
 def compress(X: torch.Tensor, ids: torch.Tensor, E: torch.Tensor, U: torch.Tensor,
-             out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """Z = (X - E[ids]) U  (float32 [N, k])."""
+             out: Optional[torch.Tensor] = None, stream=None,
+             z_dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    """Z = (X - E[ids]) U  ([N, k] in z_dtype: float32, or bfloat16 rounded once)."""
     N, d = X.shape
     V, k = E.shape[0], U.shape[1]
     if E.shape[1] != d or U.shape[0] != d or ids.shape != (N,):
         raise ValueError(f"shape mismatch X{tuple(X.shape)} ids{tuple(ids.shape)} "
                          f"E{tuple(E.shape)} U{tuple(U.shape)}")
     if out is None:
-        out = torch.empty((N, k), dtype=torch.float32, device=X.device)
+        out = torch.empty((N, k), dtype=z_dtype, device=X.device)
     _same_device(X, ids, E, U, out)
     t = X.dtype
-    _check("ssn_compress", lib().ssn_compress(
-        _dt_code(t), N, d, k, V, _dev(X, "X", t, 2), _dev(ids, "ids", torch.int32, 1),
-        _dev(E, "E", t, 2), _dev(U, "U", t, 2), _dev(out, "out", torch.float32, 2), _stream(stream)))
+    _check("ssn_compress_ex", lib().ssn_compress_ex(
+        _dt_code(t), _dt_code(z_dtype), N, d, k, V, _dev(X, "X", t, 2),
+        _dev(ids, "ids", torch.int32, 1), _dev(E, "E", t, 2), _dev(U, "U", t, 2),
+        _dev(out, "out", z_dtype, 2), _stream(stream)))
     return out
 
 
 def decompress(Z: torch.Tensor, ids: Optional[torch.Tensor], E: Optional[torch.Tensor],
                U: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """X' = E[ids] + Z U^T (storage dtype of U); with ids = E = None, Z U^T."""
+    """X' = E[ids] + Z U^T (storage dtype of U); with ids = E = None, Z U^T.
+    Z is float32 or bfloat16 (the coordinate dtype on the wire)."""
     N, k = Z.shape
     d = U.shape[0]
     if U.shape[1] != k:
@@ -178,8 +190,8 @@ def decompress(Z: torch.Tensor, ids: Optional[torch.Tensor], E: Optional[torch.T
     if out is None:
         out = torch.empty((N, d), dtype=t, device=Z.device)
     _same_device(Z, ids, E, U, out)
-    _check("ssn_decompress", lib().ssn_decompress(
-        _dt_code(t), N, d, k, V, _dev(Z, "Z", torch.float32, 2),
+    _check("ssn_decompress_ex", lib().ssn_decompress_ex(
+        _dt_code(t), _dt_code(Z.dtype), N, d, k, V, _dev(Z, "Z", Z.dtype, 2),
         None if ids is None else _dev(ids, "ids", torch.int32, 1),
         None if E is None else _dev(E, "E", t, 2), _dev(U, "U", t, 2),
         _dev(out, "out", t, 2), _stream(stream)))
@@ -193,19 +205,19 @@ def expand_grad(GZ: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] =
 
 
 def project_grad(G: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] = None,
-                 stream=None) -> torch.Tensor:
-    """G_Z = G U (float32 [N, k])."""
+                 stream=None, z_dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    """G_Z = G U ([N, k] in z_dtype: float32, or bfloat16 rounded once)."""
     N, d = G.shape
     k = U.shape[1]
     if U.shape[0] != d:
         raise ValueError(f"shape mismatch G{tuple(G.shape)} U{tuple(U.shape)}")
     if out is None:
-        out = torch.empty((N, k), dtype=torch.float32, device=G.device)
+        out = torch.empty((N, k), dtype=z_dtype, device=G.device)
     _same_device(G, U, out)
     t = G.dtype
-    _check("ssn_project_grad", lib().ssn_project_grad(
-        _dt_code(t), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2),
-        _dev(out, "out", torch.float32, 2), _stream(stream)))
+    _check("ssn_project_grad_ex", lib().ssn_project_grad_ex(
+        _dt_code(t), _dt_code(z_dtype), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2),
+        _dev(out, "out", z_dtype, 2), _stream(stream)))
     return out
 
 

@@ -229,6 +229,48 @@ def test_codec_shapes(N, d, k, dtype):
     check("expand_grad", host(ssn.expand_grad(dev(Zin, "f32"), U)), O.expand_grad(Zin, Uh), dtype, outkind)
 
 
+BF16_WIRE_SHAPES = [  # (N, d, k): every kernel family with bf16 coordinates
+    (4099, 1024, 96), (300, 5120, 51), (33325, 256, 64), (4500, 2048, 51), (1000, 160, 40),
+    (5000, 1024, 64), (64, 384, 3), (4096, 5120, 51),
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("N,d,k", BF16_WIRE_SHAPES)
+def test_bf16_coordinates(N, d, k, dtype):
+    """Coordinates on the wire in bf16: compress / project_grad store each
+    fp32 result rounded once to nearest even, so they equal the fp32 entry
+    points' outputs rounded by torch bit for bit; decompress / expansion of
+    bf16 coordinates match the oracle fed the same bf16 values."""
+    V = 61
+    seed = 3 * N + 5 * d + k
+    print(f"[case] bf16 coordinates N={N} d={d} k={k} {dtype}", flush=True)
+    r = np.random.default_rng(seed)
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), dtype)
+    Eh = I.store(0.02 * r.standard_normal((V, d)), dtype)
+    Xh = I.store(r.standard_normal((N, d)), dtype)
+    ids_h = r.integers(0, V, size=N).astype(np.int32)
+    X, E, U, ids = dev(Xh, dtype), dev(Eh, dtype), dev(Uh, dtype), dev(ids_h, dtype)
+    Zf = ssn.compress(X, ids, E, U)
+    Zb = ssn.compress(X, ids, E, U, z_dtype=torch.bfloat16)
+    assert Zb.dtype == torch.bfloat16 and torch.equal(Zb, Zf.to(torch.bfloat16))
+    check("compress bf16 Z", host(Zb), O.compress(Xh, ids_h, Eh, Uh), "bf16", "bf16out")
+    Gf = ssn.project_grad(X, U)
+    Gb = ssn.project_grad(X, U, z_dtype=torch.bfloat16)
+    assert torch.equal(Gb, Gf.to(torch.bfloat16))
+    Zin = dev(I.store(rand_coords(N, k, seed), "bf16"), "bf16")
+    Zin_h = host(Zin)
+    outkind = "bf16out" if dtype == "bf16" else "f32out_dec"
+    check("decompress bf16 Z", host(ssn.decompress(Zin, ids, E, U)),
+          O.decompress(Zin_h, ids_h, Eh, Uh), dtype, outkind)
+    check("expand_grad bf16 GZ", host(ssn.expand_grad(Zin, U)), O.expand_grad(Zin_h, Uh), dtype, outkind)
+    # the same values as float32 coordinates take the fp32 path to the same result
+    Zin32 = Zin.float()
+    Yb = ssn.decompress(Zin, ids, E, U)
+    Yf = ssn.decompress(Zin32, ids, E, U)
+    assert torch.equal(Yb, Yf)
+
+
 SPLIT_SHAPES = [  # (N, d, k): few tokens -> the d-split compress kernels (P = 8, 4, 2),
     # ragged token tails, k % 8 != 0, k > 64
     (4096, 5120, 51), (12288, 5120, 51), (20000, 1024, 64), (17, 512, 64), (33, 2048, 40),
