@@ -573,6 +573,42 @@ def main():
         "step_with_projected_compress": {"ms_per_step": round(ms2, 5),
                                          "tokens_per_s": round(N / (ms2 * 1e-3), 1)},
     }
+    # ---------------- variant: coordinates on the wire in bf16 ----------------
+    for s_ in sets:
+        s_["Zin_b"] = s_["Zin"].to(torch.bfloat16)
+        s_["GZin_b"] = s_["GZin"].to(torch.bfloat16)
+        s_["Z_b"] = torch.empty((N, k), dtype=torch.bfloat16, device=dev)
+        s_["GZ_b"] = torch.empty((N, k), dtype=torch.bfloat16, device=dev)
+
+    def step3(s, evs):
+        evs[0].record()
+        ssn.decompress(s["Zin_b"], s["ids"], E, U, out=s["Y"])
+        evs[1].record()
+        ssn.project_grad(s["G"], U, out=s["GZ_b"], z_dtype=torch.bfloat16)
+        evs[2].record()
+        ssn.compress(s["X"], s["ids_c"], E, U, out=s["Z_b"], z_dtype=torch.bfloat16)
+        evs[3].record()
+        ssn.expand_grad(s["GZin_b"], U, out=s["GX"])
+        evs[4].record()
+
+    ev3 = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    for i in range(args.warmup):
+        step3(sets[i % 2], ev3[0])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step3(sets[i % 2], ev3[i])
+    torch.cuda.synchronize()
+    ms3 = (time.perf_counter() - t0) * 1e3 / args.steps
+    st3 = op_stats(ev3, ops)
+    result["variants"]["step_bf16_coordinates"] = {
+        "what": "the same four ops with Z and G_Z in bf16 (half the wire message)",
+        "ms_per_step": round(ms3, 5), "tokens_per_s": round(N / (ms3 * 1e-3), 1),
+        "per_op_ms": {op: round(st3[op][0], 5) for op in ops}}
+    for s_ in sets:
+        for key in ("Zin_b", "GZin_b", "Z_b", "GZ_b"):
+            del s_[key]
+
     gms = time_step_graph(sets, step, args.steps, args.warmup)
     result["variants"]["step_hip_graph"] = {
         "what": "the same four ops captured once per input set as a HIP graph and replayed",
