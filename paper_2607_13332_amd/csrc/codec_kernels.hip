@@ -1117,8 +1117,8 @@ hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, con
 // 8 token tiles (128 tokens) per block, each of the 8 waves sweeping the
 // block's range of d (rotated per block, in steps of one chunk).  When N/128
 // blocks fill the compute units the range is all of d; with fewer tokens a
-// second grid dimension splits d (the smallest divisor of the chunk count
-// that gives one block per compute unit; measured at N = 4096 against blocks
+// second grid dimension splits d (a divisor of the chunk count chosen for
+// block fill, below; measured at N = 4096 against blocks
 // holding two halves of d in 16 waves: expansion 12.0 -> 9.2 us at d = 4096,
 // decompress 13.8 -> 13.2 us).  The gradient expansion (no embedding rows to
 // gather) stores two chunks at a time (256 contiguous bytes per row) when
@@ -1133,10 +1133,24 @@ static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const
   const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
   const int64_t cus = device_cu_count();
   const int chunks = d / kDecompressDC;
+  // with fewer blocks than compute units: the smallest split of d (a divisor
+  // of the chunk count, at least two chunks per block) whose blocks fill at
+  // least 90 % of their last round, else the smallest that reaches one block
+  // per unit (N = 12288, d = 5120, k = 51: 96 blocks in 5 ranges 57.9 us, in
+  // 4 ranges 64.3 us)
   int gy = 1;
-  while (gy < chunks && blocks * gy < cus) {
-    ++gy;
-    while (chunks % gy != 0) ++gy;
+  if (blocks < cus) {
+    int first = 0;
+    for (int g = 2; g <= chunks; ++g) {
+      if (chunks % g != 0 || (blocks * g < cus && g < chunks)) continue;
+      if (first == 0) first = g;
+      const int64_t b = blocks * g, rounds = (b + cus - 1) / cus;
+      if (2 * g <= chunks && 10 * b >= 9 * rounds * cus) {
+        gy = g;
+        break;
+      }
+    }
+    if (gy == 1) gy = first > 0 ? first : 1;
   }
   const dim3 grid((unsigned)blocks, (unsigned)gy);
   if (!HAS_E && (chunks / gy) % 2 == 0)

@@ -196,6 +196,9 @@ CODEC_SHAPES = [  # (N, d, k): tiles, ragged tails, every k bucket, both familie
     (33325, 256, 64), (33325, 384, 32), (20000, 640, 48),
     # few-token projections with two token tiles per wave
     (5000, 1024, 64), (4500, 2048, 51),
+    # few-token decompress / expansion with a fill-chosen split of d (5 and
+    # 16 ranges)
+    (12288, 5120, 51), (6144, 2048, 40),
 ]
 
 
