@@ -125,8 +125,16 @@ def _dt_code(dtype) -> int:
     raise TypeError(f"unsupported storage dtype {dtype}")
 
 
+_raw_current_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream(stream) -> int:
+    """hipStream_t of `stream`, or of the current stream of the current device."""
     if stream is None:
+        if _raw_current_stream is not None:
+            # the raw handle directly (torch.cuda.current_stream() builds a
+            # Stream object per call, a few microseconds)
+            return int(_raw_current_stream(torch.cuda.current_device()))
         stream = torch.cuda.current_stream()
     return int(stream.cuda_stream)
 
