@@ -530,6 +530,39 @@ def test_empty_batch_is_a_no_op():
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("N,d,k,dtype", [(300, 256, 64, "bf16"), (33325, 256, 64, "bf16"),
+                                         (200, 100, 10, "f32")])
+def test_out_of_range_ids_are_clamped(N, d, k, dtype):
+    """Ids outside [0, V) break the caller's contract; every kernel clamps
+    them into range before addressing E, P or a coordinate table, so memory
+    stays in bounds and the other rows are unaffected (the offending rows are
+    those of the clamped id)."""
+    V = 37
+    seed = N + d + k
+    print(f"[case] out-of-range ids N={N} d={d} k={k} {dtype}", flush=True)
+    r = np.random.default_rng(seed)
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), dtype)
+    Eh = I.store(0.02 * r.standard_normal((V, d)), dtype)
+    Xh = I.store(r.standard_normal((N, d)), dtype)
+    ids_h = r.integers(0, V, size=N).astype(np.int32)
+    bad = np.array([0, 1, N // 2, N - 1])
+    ids_h[bad] = np.array([-5, V, V + 1000, -2 ** 31], dtype=np.int32)
+    clamped = np.clip(ids_h.astype(np.int64), 0, V - 1).astype(np.int32)
+    X, E, U, ids = dev(Xh, dtype), dev(Eh, dtype), dev(Uh, dtype), dev(ids_h, dtype)
+    Zin = rand_coords(N, k, seed)
+    outkind = "bf16out" if dtype == "bf16" else "f32out_dec"
+    check("compress", host(ssn.compress(X, ids, E, U)), O.compress(Xh, clamped, Eh, Uh), dtype, "f32out")
+    check("decompress", host(ssn.decompress(dev(Zin, "f32"), ids, E, U)),
+          O.decompress(Zin, clamped, Eh, Uh), dtype, outkind)
+    P = ssn.project_table(E, U)
+    check("compress_projected", host(ssn.compress_projected(X, ids, P, U)),
+          O.compress(Xh, clamped, Eh, Uh), dtype, "f32out")
+    Ef = (0.1 * r.standard_normal((V, k))).astype(np.float32)
+    check("factored embedding", host(ssn.factored_embedding(ids, dev(Ef, "f32"), U)),
+          O.factored_embedding(Ef, clamped, Uh), dtype, outkind)
+    torch.cuda.synchronize()
+
+
 def test_non_default_stream_and_determinism():
     cfg = I.with_tokens(I.MID, 4096)
     h = structured_inputs(cfg)
