@@ -8,6 +8,7 @@
 #include "ssn_device.h"
 #include "ssn_launch.h"
 
+#include <atomic>
 #include <type_traits>
 
 namespace ssn {
@@ -535,17 +536,19 @@ static hipError_t launch_weights_kt(const PanelBatch& pb, int blocks, const void
   return hipGetLastError();
 }
 
+// Cached per device; calls from several host threads may fill an entry
+// concurrently, each with the same value (relaxed atomics).
 int device_cu_count() {
-  static int cus[64] = {0};
+  static std::atomic<int> cus[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] == 0) {
-    int c = 0;
+  int c = cus[dev].load(std::memory_order_relaxed);
+  if (c == 0) {
     if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0)
       c = 256;
-    cus[dev] = c;
+    cus[dev].store(c, std::memory_order_relaxed);
   }
-  return cus[dev];
+  return c;
 }
 
 template <int KT, bool KV>
