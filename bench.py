@@ -83,7 +83,8 @@ def parse_args():
                         "keeps its kernels apart from the codec's in a kernel trace)")
     p.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                    help="before the timed region, run a plain device copy of MIB MiB three times "
-                        "(a known-size kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
+                        "(a known-size kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE); "
+                        "the live device-copy reference rate is then skipped")
     return p.parse_args()
 
 
@@ -525,6 +526,14 @@ def main():
 
     stats = op_stats(events, ops)
     per_op = {op: per_op_entry(op, *stats[op]) for op in ops}
+    # HBM bytes measured by the rocprofv3 counters (when taken on these
+    # sources) over the same mean durations
+    measured = {op: load_traffic(op) for op in ops}
+    for op in ops:
+        if measured[op] is not None:
+            gbs = measured[op] / (stats[op][0] * 1e-3) / 1e9
+            per_op[op]["measured_traffic_GBps"] = round(gbs, 1)
+            per_op[op]["measured_frac_hbm_peak"] = round(gbs / HBM_PEAK_GBS, 4)
     per_op_ms = {op: stats[op][0] for op in ops}
     dom = max(ops, key=lambda o: per_op_ms[o])
     achieved = per_op[dom]["algorithmic_GBps"]
@@ -545,17 +554,22 @@ def main():
                    "storage": "bf16", "coords": "fp32", "parallelism": "none (1 GPU)"},
         "step_algorithmic_GBps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "step_frac_hbm_peak": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "step_measured_frac_hbm_peak": (
+            None if any(v is None for v in measured.values()) else
+            round(sum(measured.values()) / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)),
         "per_op": per_op,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
         "kernel_source_hash": kernel_source_hash(),
     }
-    cp_rate = copy_rate(dev)
-    result["hbm_copy_reference"] = {
-        "what": "torch device copy of 512 MiB on the same GPU, bytes read + written per second",
-        "GBps": round(cp_rate, 1), "frac_hbm_peak": round(cp_rate / HBM_PEAK_GBS, 4),
-        "dominant_kernel_frac_of_copy": round(achieved / cp_rate, 4)}
+    # (not in the counter runs: their copy of known size is the calibration)
+    cp_rate = None if args.copy_calib else copy_rate(dev)
+    if cp_rate is not None:
+        result["hbm_copy_reference"] = {
+            "what": "torch device copy of 512 MiB on the same GPU, bytes read + written per second",
+            "GBps": round(cp_rate, 1), "frac_hbm_peak": round(cp_rate / HBM_PEAK_GBS, 4),
+            "dominant_kernel_frac_of_copy": round(achieved / cp_rate, 4)}
 
     # ---------------- variant: compress against the projected table ----------------
     tev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
