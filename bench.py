@@ -650,7 +650,11 @@ def main():
     gms = time_step_graph(sets, step, args.steps, args.warmup)
     result["variants"]["step_hip_graph"] = {
         "what": "the same four ops captured once per input set as a HIP graph and replayed",
-        "ms_per_step": round(gms, 5), "tokens_per_s": round(N / (gms * 1e-3), 1)}
+        "ms_per_step": round(gms, 5), "tokens_per_s": round(N / (gms * 1e-3), 1),
+        "frac_hbm_peak": round(step_bytes / (gms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "measured_frac_hbm_peak": (
+            None if any(v is None for v in measured.values()) else
+            round(sum(measured.values()) / (gms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))}
     del P
 
     # ---------------- weight re-projection (once per optimizer step) ----------------
