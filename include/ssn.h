@@ -186,6 +186,13 @@ ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t 
 ssn_status_t ssn_compress_projected(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
                                     const void *X, const int32_t *ids, const float *P,
                                     const void *U, float *Z, void *stream);
+/* The same with the coordinate dtype z_dtype (see ssn_compress_ex): the table
+ * P stays float32; with SSN_BF16 each Z value is rounded once after the
+ * subtraction. */
+ssn_status_t ssn_compress_projected_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N,
+                                       int64_t d, int64_t k, int64_t V, const void *X,
+                                       const int32_t *ids, const float *P, const void *U, void *Z,
+                                       void *stream);
 
 /*
  * ssn_project_weights -- original-SSN re-projection after an optimizer step

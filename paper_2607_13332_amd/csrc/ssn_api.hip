@@ -100,24 +100,32 @@ ssn_status_t ssn_compress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, in
   return ssn_compress_ex(dtype, SSN_F32, N, d, k, V, X, ids, E, U, Z, stream);
 }
 
-ssn_status_t ssn_compress_projected(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
-                                    const void* X, const int32_t* ids, const float* P,
-                                    const void* U, float* Z, void* stream) {
-  if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;
+ssn_status_t ssn_compress_projected_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N,
+                                       int64_t d, int64_t k, int64_t V, const void* X,
+                                       const int32_t* ids, const float* P, const void* U, void* Z,
+                                       void* stream) {
+  if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
   if (N < 0 || d < 1 || k < 1 || k > d || V < 1) return SSN_ERR_SHAPE;
   if (!mul_ok(N, d) || !mul_ok(V, k) || !mul_ok(d, k) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
   if (N == 0) return SSN_OK;
   if (!X || !ids || !P || !U || !Z) return SSN_ERR_NULL;
-  const int64_t s = elem_size(dtype);
+  const int64_t s = elem_size(dtype), zs = elem_size(z_dtype);
   if (!aligned_to(X, s) || !aligned_to(P, 4) || !aligned_to(U, s) || !aligned_to(ids, 4) ||
-      !aligned_to(Z, 4))
+      !aligned_to(Z, zs))
     return SSN_ERR_ALIGN;
-  const Span out = span(Z, N * k * 4);
+  const Span out = span(Z, N * k * zs);
   if (overlap(out, span(X, N * d * s)) || overlap(out, span(P, V * k * 4)) ||
       overlap(out, span(U, d * k * s)) || overlap(out, span(ids, N * 4)))
     return SSN_ERR_ALIAS;
-  return launch_status(
-      ssn::launch_compress(dtype, N, d, k, V, X, ids, nullptr, U, Z, P, (hipStream_t)stream));
+  return launch_status(ssn::launch_compress(dtype, N, d, k, V, X, ids, nullptr, U,
+                                            z_f32(z_dtype, Z), P, (hipStream_t)stream,
+                                            z_b16(z_dtype, Z)));
+}
+
+ssn_status_t ssn_compress_projected(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
+                                    const void* X, const int32_t* ids, const float* P,
+                                    const void* U, float* Z, void* stream) {
+  return ssn_compress_projected_ex(dtype, SSN_F32, N, d, k, V, X, ids, P, U, Z, stream);
 }
 
 ssn_status_t ssn_decompress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,

@@ -56,6 +56,9 @@ def _declare(lib):
     lib.ssn_project_grad_ex.restype = ctypes.c_int
     lib.ssn_project_grad_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
                                         _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_compress_projected_ex.restype = ctypes.c_int
+    lib.ssn_compress_projected_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
+                                              _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_project_table.restype = ctypes.c_int
     lib.ssn_project_table.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_compress_projected.restype = ctypes.c_int
@@ -247,21 +250,22 @@ def project_table(E: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] 
 
 
 def compress_projected(X: torch.Tensor, ids: torch.Tensor, P: torch.Tensor, U: torch.Tensor,
-                       out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """Z = X U - P[ids] (float32 [N, k]), with P from project_table(E, U)."""
+                       out: Optional[torch.Tensor] = None, stream=None,
+                       z_dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    """Z = X U - P[ids] ([N, k] in z_dtype), with P from project_table(E, U)."""
     N, d = X.shape
     V, k = P.shape
     if U.shape != (d, k) or ids.shape != (N,):
         raise ValueError(f"shape mismatch X{tuple(X.shape)} ids{tuple(ids.shape)} "
                          f"P{tuple(P.shape)} U{tuple(U.shape)}")
     if out is None:
-        out = torch.empty((N, k), dtype=torch.float32, device=X.device)
+        out = torch.empty((N, k), dtype=z_dtype, device=X.device)
     _same_device(X, ids, P, U, out)
     t = X.dtype
-    _check("ssn_compress_projected", lib().ssn_compress_projected(
-        _dt_code(t), N, d, k, V, _dev(X, "X", t, 2), _dev(ids, "ids", torch.int32, 1),
-        _dev(P, "P", torch.float32, 2), _dev(U, "U", t, 2), _dev(out, "out", torch.float32, 2),
-        _stream(stream)))
+    _check("ssn_compress_projected_ex", lib().ssn_compress_projected_ex(
+        _dt_code(t), _dt_code(z_dtype), N, d, k, V, _dev(X, "X", t, 2),
+        _dev(ids, "ids", torch.int32, 1), _dev(P, "P", torch.float32, 2), _dev(U, "U", t, 2),
+        _dev(out, "out", z_dtype, 2), _stream(stream)))
     return out
 
 

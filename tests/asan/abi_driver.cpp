@@ -64,6 +64,7 @@ int main() {
             ssn_compress_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, X, ids, E, U, Z, nullptr);
             ssn_decompress_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, Z, ids, E, U, Y, nullptr);
             ssn_project_grad_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, X, U, Z, nullptr);
+            ssn_compress_projected_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, X, ids, T, U, Z, nullptr);
           }
         }
   EXPECT(ssn_compress(SSN_BF16, 4096, 4096, 64, 131072, X, ids, E, U, Z, nullptr), SSN_OK);

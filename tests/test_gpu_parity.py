@@ -261,6 +261,10 @@ def test_bf16_coordinates(N, d, k, dtype):
     Gf = ssn.project_grad(X, U)
     Gb = ssn.project_grad(X, U, z_dtype=torch.bfloat16)
     assert torch.equal(Gb, Gf.to(torch.bfloat16))
+    P = ssn.project_table(E, U)
+    Pf = ssn.compress_projected(X, ids, P, U)
+    Pb = ssn.compress_projected(X, ids, P, U, z_dtype=torch.bfloat16)
+    assert torch.equal(Pb, Pf.to(torch.bfloat16))
     Zin = dev(I.store(rand_coords(N, k, seed), "bf16"), "bf16")
     Zin_h = host(Zin)
     outkind = "bf16out" if dtype == "bf16" else "f32out_dec"
