@@ -135,25 +135,36 @@ ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k
                               const void *G, const void *U, float *GZ, void *stream);
 
 /*
- * Coordinate dtype on the wire.  The paper sizes the boundary traffic with
- * activations sent in FP32 (section 3.5.2, its estimate of per-node
- * communication), which the three entry points above keep.  These variants take the dtype of Z (or GZ) as
- * `z_dtype`: SSN_F32 gives exactly the entry points above; SSN_BF16 halves
- * the message.  Compress / project_grad then round each fp32 result once to
- * bf16 (nearest even) as they store it; decompress reads bf16 coordinates,
- * which are exact in its fp32 arithmetic, so decompress_ex(compress_ex(X))
- * differs from the fp32 round trip only by the coordinate rounding.  Z is
- * `void *` [N, k] of z_dtype, aligned to its element size; otherwise the
- * arguments, validation and error codes are those of the entry points above.
+ * Coordinate dtype on the wire, and a padded basis.  The paper sizes the
+ * boundary traffic with activations sent in FP32 (section 3.5.2, its estimate
+ * of per-node communication), which the entry points above keep.  These
+ * variants add two choices:
+ *  - `z_dtype`: the dtype of Z (or GZ), SSN_F32 or SSN_BF16 (half the
+ *    message).  Compress / project_grad round each fp32 result once to bf16
+ *    (nearest even) as they store it; decompress reads bf16 coordinates,
+ *    which are exact in its fp32 arithmetic.
+ *  - `ldu` (>= k): the row stride of U in elements.  U is then [d, ldu] with
+ *    its first k columns the basis and columns k .. ldu-1 ZERO (a padded copy
+ *    made once per basis; the basis is fixed for the run).  With ldu a
+ *    multiple of 8 (16 for the fastest paths) the kernels read U with aligned
+ *    16-byte loads whatever k is, e.g. k = 51 padded to 64; Z keeps k columns.
+ *    ldu == k is the plain layout.
+ * With z_dtype == SSN_F32 and ldu == k these are exactly the entry points
+ * above.  Z is `void *` [N, k] of z_dtype, aligned to its element size;
+ * otherwise the arguments, validation and error codes are those of the entry
+ * points above (ldu < k, or ldu > 2^31, is SSN_ERR_SHAPE; U's span for the
+ * overlap checks is d * ldu elements).
  */
 ssn_status_t ssn_compress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
                              int64_t k, int64_t V, const void *X, const int32_t *ids,
-                             const void *E, const void *U, void *Z, void *stream);
+                             const void *E, const void *U, int64_t ldu, void *Z, void *stream);
 ssn_status_t ssn_decompress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
                                int64_t k, int64_t V, const void *Z, const int32_t *ids,
-                               const void *E, const void *U, void *Xout, void *stream);
+                               const void *E, const void *U, int64_t ldu, void *Xout,
+                               void *stream);
 ssn_status_t ssn_project_grad_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
-                                 int64_t k, const void *G, const void *U, void *GZ, void *stream);
+                                 int64_t k, const void *G, const void *U, int64_t ldu, void *GZ,
+                                 void *stream);
 
 /*
  * ssn_project_table -- the fixed token embedding projected onto the basis,
@@ -186,13 +197,13 @@ ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t 
 ssn_status_t ssn_compress_projected(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
                                     const void *X, const int32_t *ids, const float *P,
                                     const void *U, float *Z, void *stream);
-/* The same with the coordinate dtype z_dtype (see ssn_compress_ex): the table
- * P stays float32; with SSN_BF16 each Z value is rounded once after the
- * subtraction. */
+/* The same with a coordinate dtype and a padded basis (see ssn_compress_ex):
+ * the table P stays float32 [V, k]; with SSN_BF16 each Z value is rounded
+ * once after the subtraction. */
 ssn_status_t ssn_compress_projected_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N,
                                        int64_t d, int64_t k, int64_t V, const void *X,
-                                       const int32_t *ids, const float *P, const void *U, void *Z,
-                                       void *stream);
+                                       const int32_t *ids, const float *P, const void *U,
+                                       int64_t ldu, void *Z, void *stream);
 
 /*
  * ssn_project_weights -- original-SSN re-projection after an optimizer step

@@ -117,7 +117,7 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ P,
-    uint16_t* __restrict__ Zb) {
+    uint16_t* __restrict__ Zb, int kz) {
   static_assert(DEPTH >= 1 && DEPTH <= 4, "one to four chunks of rows in flight");
   static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
   constexpr int KS = 4, DC = 128;
@@ -226,7 +226,11 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     if constexpr (DEPTH > 3) step(i0 + 3, std::integral_constant<int, 3 % DEPTH>{}, L0{});
   }
 
+  // lane (n16, g) holds coordinates col0 .. col0 + KP - 1 of tokens
+  // tok0 + 4g + j; rows of Z (and P) hold kz of the k columns of U
   const int col0 = n16 * KP;
+  bool whole = false;                           // whole 16-byte row pieces
+  if constexpr (KFULL && KP % 4 == 0) whole = (kz == k);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int64_t tj = tok0 + 4 * g + j;
@@ -235,40 +239,49 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
 #pragma unroll
       for (int i = 0; i < KP; ++i) v[i] = HAS_E ? accX[i][j] - accE[i][j] : accX[i][j];
       if constexpr (HAS_P) {
-        const float* pp = P + clamp_id(ids[tj], V) * k + col0;
+        const float* pp = P + clamp_id(ids[tj], V) * kz + col0;
         if constexpr (KFULL && KP % 4 == 0) {
+          if (whole) {
 #pragma unroll
-          for (int i = 0; i < KP; i += 4) {
-            const f32x4 q = *(const f32x4*)(pp + i);
-            v[i] -= q[0]; v[i + 1] -= q[1]; v[i + 2] -= q[2]; v[i + 3] -= q[3];
+            for (int i = 0; i < KP; i += 4) {
+              const f32x4 q = *(const f32x4*)(pp + i);
+              v[i] -= q[0]; v[i + 1] -= q[1]; v[i + 2] -= q[2]; v[i + 3] -= q[3];
+            }
           }
-        } else {
+        }
+        if (!whole) {
 #pragma unroll
           for (int i = 0; i < KP; ++i)
-            if (col0 + i < k) v[i] -= pp[i];
+            if (col0 + i < kz) v[i] -= pp[i];
         }
       }
       if (Zb) {
         // bf16 coordinates: rounded once, to nearest even
-        uint16_t* zb = Zb + tj * k + col0;
+        uint16_t* zb = Zb + tj * kz + col0;
         if constexpr (KFULL && KP % 4 == 0) {
+          if (whole) {
 #pragma unroll
-          for (int i = 0; i < KP; i += 4)
-            *(u32x2*)(zb + i) = u32x2{pack_bf16x2(v[i], v[i + 1]), pack_bf16x2(v[i + 2], v[i + 3])};
-        } else {
+            for (int i = 0; i < KP; i += 4)
+              *(u32x2*)(zb + i) = u32x2{pack_bf16x2(v[i], v[i + 1]), pack_bf16x2(v[i + 2], v[i + 3])};
+          }
+        }
+        if (!whole) {
 #pragma unroll
           for (int i = 0; i < KP; ++i)
-            if (col0 + i < k) zb[i] = (uint16_t)f32_to_bf16(v[i]);
+            if (col0 + i < kz) zb[i] = (uint16_t)f32_to_bf16(v[i]);
         }
       } else {
-        float* zp = Z + tj * k + col0;
+        float* zp = Z + tj * kz + col0;
         if constexpr (KFULL && KP % 4 == 0) {
+          if (whole) {
 #pragma unroll
-          for (int i = 0; i < KP; i += 4) *(f32x4*)(zp + i) = f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
-        } else {
+            for (int i = 0; i < KP; i += 4) *(f32x4*)(zp + i) = f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
+          }
+        }
+        if (!whole) {
 #pragma unroll
           for (int i = 0; i < KP; ++i)
-            if (col0 + i < k) zp[i] = v[i];
+            if (col0 + i < kz) zp[i] = v[i];
         }
       }
     }
@@ -305,7 +318,7 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
     const uint16_t* __restrict__ X, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     float* __restrict__ Z, int64_t N, int d, int k, int64_t V, const float* __restrict__ Pt,
-    uint16_t* __restrict__ Zb) {
+    uint16_t* __restrict__ Zb, int kz) {
   static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
   static_assert(UM >= 0 && UM <= 2, "U staging mode");
   constexpr bool KV = (UM == 0);
@@ -333,7 +346,7 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
   // Z + y * N * k (summed by a second kernel)
   const int nchp = d / (DC * P * (int)gridDim.y);   // chunks of this wave
   const int c0 = ((int)blockIdx.y * P + wave) * nchp;
-  if constexpr (!HAS_E && !HAS_P) Z += (int64_t)blockIdx.y * N * k;
+  if constexpr (!HAS_E && !HAS_P) Z += (int64_t)blockIdx.y * N * kz;
   u32x4* const xtw = (u32x4*)(smem + wave * WAVE_BYTES);           // [X/E][row * 8 + cell']
   uint16_t* const utw = (uint16_t*)(smem + wave * WAVE_BYTES + XT_BYTES);
 
@@ -482,17 +495,17 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
     for (int w = 1; w < P; ++w) sum += red[(w * TTW * KP + ti) * 64 + l];
     // lane l of tile (tt, i) holds Z[tok0 + 16 tt + 4 (l/16) + e][16 i + l % 16]
     const int col = 16 * i + (l & 15);
-    if (col < k) {
+    if (col < kz) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int64_t t = tok0 + 16 * tt + 4 * (l >> 4) + e;
         if (t < N) {
           float v = sum[e];
-          if constexpr (HAS_P) v -= Pt[clamp_id(ids[t], V) * k + col];
+          if constexpr (HAS_P) v -= Pt[clamp_id(ids[t], V) * kz + col];
           if (Zb)
-            Zb[t * k + col] = (uint16_t)f32_to_bf16(v);
+            Zb[t * kz + col] = (uint16_t)f32_to_bf16(v);
           else
-            Z[t * k + col] = v;
+            Z[t * kz + col] = v;
         }
       }
     }
@@ -533,7 +546,7 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids,
     const uint16_t* __restrict__ E, const uint16_t* __restrict__ U,
     uint16_t* __restrict__ Y, int64_t N, int d, int k, int64_t V,
-    const uint16_t* __restrict__ Zb) {
+    const uint16_t* __restrict__ Zb, int kz) {
   static_assert(DC == 64 || DC == 128, "chunk of 64 or 128 d");
   static_assert(KM >= 0 && KM <= 2, "k layout mode");
   static_assert(!(HAS_E && GZ), "gathered coordinates carry no additive embedding");
@@ -559,21 +572,22 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
   {
     int64_t t = tok0 + n16;
     t = t < N ? t : N - 1;
-    const int64_t zrow = (GZ ? clamp_id(ids[t], V) : t) * k;
+    // Z rows hold kz coordinates (for the first kz of the k columns of U)
+    const int64_t zrow = (GZ ? clamp_id(ids[t], V) : t) * kz;
     // bf16 coordinates when Zb is non-NULL (exact in the hi part; the lo
-    // part is zero), else float32 ones from Zc
+    // part is zero), else float32 ones from Zc.  Groups of 8 within kz
+    // travel as 16-byte loads when the rows are 16-byte aligned, the rest
+    // element by element (zero past kz).
     const bool zb16 = Zb != nullptr;
+    const bool zvec = KM != 2 && (zb16 ? kz % 8 == 0 : kz % 4 == 0);
     const float* zp = zb16 ? nullptr : Zc + zrow;
     const uint16_t* zq = zb16 ? Zb + zrow : nullptr;
 #pragma unroll
     for (int s = 0; s < KS2; ++s) {
       const int c0 = 32 * s + 8 * g;
       float v[8];
-      if (zb16) {
-        if constexpr (KM == 2) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = (c0 + e < k) ? bf16_to_f32(zq[c0 + e]) : 0.f;
-        } else if (KFULL32 || c0 + 8 <= k) {
+      if (zvec && c0 + 8 <= kz) {
+        if (zb16) {
           const u32x4 a = *(const u32x4*)(zq + c0);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -581,20 +595,18 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
             v[2 * e + 1] = bf16_to_f32(a[e] >> 16);
           }
         } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = 0.f;
+          const f32x4 a = *(const f32x4*)(zp + c0);
+          const f32x4 b = *(const f32x4*)(zp + c0 + 4);
+          v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
+          v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
         }
-      } else if constexpr (KM == 2) {
+      } else if (c0 < kz) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = (c0 + e < k) ? zp[c0 + e] : 0.f;
-      } else if (KFULL32 || c0 + 8 <= k) {
-        const f32x4 a = *(const f32x4*)(zp + c0);
-        const f32x4 b = *(const f32x4*)(zp + c0 + 4);
-        v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
-        v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
+        for (int e = 0; e < 8; ++e)
+          v[e] = (c0 + e < kz) ? (zb16 ? bf16_to_f32(zq[c0 + e]) : zp[c0 + e]) : 0.f;
       } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = 0.f;   // the whole group lies past k
+        for (int e = 0; e < 8; ++e) v[e] = 0.f;   // the whole group lies past kz
       }
       split_bf16x8(v, zhi[s], zlo[s]);
     }
@@ -801,13 +813,14 @@ template <typename T, bool HAS_E, bool HAS_P = false>
 __global__ __launch_bounds__(256) void compress_generic(
     const T* __restrict__ X, const int32_t* __restrict__ ids, const T* __restrict__ E,
     const T* __restrict__ U, float* __restrict__ Z, int64_t N, int64_t d, int64_t k, int64_t V,
-    const float* __restrict__ P, uint16_t* __restrict__ Zb) {
+    const float* __restrict__ P, uint16_t* __restrict__ Zb, int64_t kz) {
   const int lane = threadIdx.x & 63;
   const int64_t nw = (int64_t)gridDim.x * 4;
   for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < N; t += nw) {
     const T* xr = X + t * d;
     const T* er = HAS_E ? E + clamp_id(ids[t], V) * d : nullptr;
-    for (int64_t kc = 0; kc < k; kc += 16) {
+    // coordinates kc .. kc + 15 of the kz (U rows are k wide)
+    for (int64_t kc = 0; kc < kz; kc += 16) {
       float acc[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[i] = 0.f;
@@ -816,7 +829,7 @@ __global__ __launch_bounds__(256) void compress_generic(
         const T* ur = U + j * k + kc;
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          if (kc + i < k) acc[i] = fmaf(x, load_as_f32(ur + i), acc[i]);
+          if (kc + i < kz) acc[i] = fmaf(x, load_as_f32(ur + i), acc[i]);
       }
       float mine = 0.f;
 #pragma unroll
@@ -824,12 +837,12 @@ __global__ __launch_bounds__(256) void compress_generic(
         const float s = wave_sum(acc[i]);
         if (lane == i) mine = s;
       }
-      if (lane < 16 && kc + lane < k) {
-        if constexpr (HAS_P) mine -= P[clamp_id(ids[t], V) * k + kc + lane];
+      if (lane < 16 && kc + lane < kz) {
+        if constexpr (HAS_P) mine -= P[clamp_id(ids[t], V) * kz + kc + lane];
         if (Zb)
-          Zb[t * k + kc + lane] = (uint16_t)f32_to_bf16(mine);
+          Zb[t * kz + kc + lane] = (uint16_t)f32_to_bf16(mine);
         else
-          Z[t * k + kc + lane] = mine;
+          Z[t * kz + kc + lane] = mine;
       }
     }
   }
@@ -839,11 +852,11 @@ template <typename T, bool HAS_E, bool GZ = false>
 __global__ __launch_bounds__(256) void decompress_generic(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids, const T* __restrict__ E,
     const T* __restrict__ U, T* __restrict__ Y, int64_t N, int64_t d, int64_t k, int64_t V,
-    const uint16_t* __restrict__ Zb) {
+    const uint16_t* __restrict__ Zb, int64_t kz) {
   const int lane = threadIdx.x & 63;
   const int64_t nw = (int64_t)gridDim.x * 4;
   for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < N; t += nw) {
-    const int64_t zrow = (GZ ? clamp_id(ids[t], V) : t) * k;
+    const int64_t zrow = (GZ ? clamp_id(ids[t], V) : t) * kz;
     const float* zr = Zb ? nullptr : Zc + zrow;
     const uint16_t* zq = Zb ? Zb + zrow : nullptr;
     const T* er = HAS_E ? E + clamp_id(ids[t], V) * d : nullptr;
@@ -851,9 +864,9 @@ __global__ __launch_bounds__(256) void decompress_generic(
       float acc = HAS_E ? load_as_f32(er + j) : 0.f;
       const T* ur = U + j * k;
       if (Zb)
-        for (int64_t c = 0; c < k; ++c) acc = fmaf(bf16_to_f32(zq[c]), load_as_f32(ur + c), acc);
+        for (int64_t c = 0; c < kz; ++c) acc = fmaf(bf16_to_f32(zq[c]), load_as_f32(ur + c), acc);
       else
-        for (int64_t c = 0; c < k; ++c) acc = fmaf(zr[c], load_as_f32(ur + c), acc);
+        for (int64_t c = 0; c < kz; ++c) acc = fmaf(zr[c], load_as_f32(ur + c), acc);
       store_from_f32(Y + t * d + j, acc);
     }
   }
@@ -882,17 +895,17 @@ bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) {
 template <int KP, bool HAS_E, bool KFULL, bool HAS_P>
 static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const void* X,
                                        const int32_t* ids, const void* E, const void* U, float* Z,
-                                       const float* P, hipStream_t st, uint16_t* Zb) {
+                                       const float* P, hipStream_t st, uint16_t* Zb, int kz) {
   if ((N + 127) / 128 >= device_cu_count()) {
     const int64_t blocks = (N + 127) / 128;
     hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 8, 1, true, false, true, 4, HAS_P>),
                        dim3((unsigned)blocks), dim3(512), 0, st, (const uint16_t*)X, ids,
-                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P, Zb);
+                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P, Zb, kz);
   } else {
     const int64_t blocks = (N + 63) / 64;
     hipLaunchKernelGGL((compress_rows_bf16<KP, HAS_E, KFULL, 4, 1, true, false, false, 1, HAS_P>),
                        dim3((unsigned)blocks), dim3(256), 0, st, (const uint16_t*)X, ids,
-                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P, Zb);
+                       (const uint16_t*)E, (const uint16_t*)U, Z, N, d, k, V, P, Zb, kz);
   }
   return hipGetLastError();
 }
@@ -902,25 +915,25 @@ static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const
 template <int KP, bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_kp(int64_t N, int d, int k, int64_t V, const void* X,
                                      const int32_t* ids, const void* E, const void* U, float* Z,
-                                     const float* P, hipStream_t st, uint16_t* Zb) {
+                                     const float* P, hipStream_t st, uint16_t* Zb, int kz) {
   return k == 16 * KP
-             ? launch_compress_rows<KP, HAS_E, true, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb)
-             : launch_compress_rows<KP, HAS_E, false, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+             ? launch_compress_rows<KP, HAS_E, true, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz)
+             : launch_compress_rows<KP, HAS_E, false, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz);
 }
 
 template <bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_mfma(int64_t N, int d, int k, int64_t V, const void* X,
                                        const int32_t* ids, const void* E, const void* U, float* Z,
-                                       const float* P, hipStream_t st, uint16_t* Zb) {
+                                       const float* P, hipStream_t st, uint16_t* Zb, int kz) {
   switch ((k + 15) / 16) {
-    case 1: return launch_compress_kp<1, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-    case 2: return launch_compress_kp<2, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-    case 3: return launch_compress_kp<3, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-    case 4: return launch_compress_kp<4, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-    case 5: return launch_compress_kp<5, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-    case 6: return launch_compress_kp<6, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-    case 7: return launch_compress_kp<7, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-    default: return launch_compress_kp<8, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    case 1: return launch_compress_kp<1, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz);
+    case 2: return launch_compress_kp<2, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz);
+    case 3: return launch_compress_kp<3, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz);
+    case 4: return launch_compress_kp<4, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz);
+    case 5: return launch_compress_kp<5, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz);
+    case 6: return launch_compress_kp<6, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz);
+    case 7: return launch_compress_kp<7, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz);
+    default: return launch_compress_kp<8, HAS_E, HAS_P>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz);
   }
 }
 
@@ -934,12 +947,12 @@ static unsigned generic_blocks(int64_t N) {
 template <int KP, bool HAS_E, bool HAS_P, int P, int TTW>
 static hipError_t launch_split_t(int64_t N, int d, int k, int64_t V, const void* X,
                                  const int32_t* ids, const void* E, const void* U, float* Z,
-                                 const float* Pt, hipStream_t st, int S, uint16_t* Zb) {
+                                 const float* Pt, hipStream_t st, int S, uint16_t* Zb, int kz) {
   const dim3 grid((unsigned)((N + 16 * TTW - 1) / (16 * TTW)), (unsigned)S);
 #define SSN_SPLIT(UM)                                                                           \
   hipLaunchKernelGGL((compress_split_bf16<KP, HAS_E, HAS_P, UM, P, TTW>), grid, dim3(64 * P), 0, \
                      st, (const uint16_t*)X, ids, (const uint16_t*)E, (const uint16_t*)U, Z, N, d, \
-                     k, V, Pt, Zb)
+                     k, V, Pt, Zb, kz)
   // odd k (measured at d = 5120 and 18432, k = 51): the shuffled windows win
   // when two token tiles share each U chunk, or with eight waves and d up to
   // 8192; otherwise the span scatter, except for compress with eight waves,
@@ -957,17 +970,17 @@ static hipError_t launch_split_t(int64_t N, int d, int k, int64_t V, const void*
 template <int KP, bool HAS_E, bool HAS_P>
 static hipError_t launch_split_kp(int P, int TTW, int64_t N, int d, int k, int64_t V, const void* X,
                                   const int32_t* ids, const void* E, const void* U, float* Z,
-                                  const float* Pt, hipStream_t st, int S, uint16_t* Zb) {
+                                  const float* Pt, hipStream_t st, int S, uint16_t* Zb, int kz) {
   if constexpr (KP <= 4) {
     if constexpr (!HAS_E)
       if (P == 8 && TTW == 2)
-        return launch_split_t<KP, HAS_E, HAS_P, 8, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
-    if (P == 8) return launch_split_t<KP, HAS_E, HAS_P, 8, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
+        return launch_split_t<KP, HAS_E, HAS_P, 8, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb, kz);
+    if (P == 8) return launch_split_t<KP, HAS_E, HAS_P, 8, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb, kz);
     if (P == 4 && TTW == 2)
-      return launch_split_t<KP, HAS_E, HAS_P, 4, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
+      return launch_split_t<KP, HAS_E, HAS_P, 4, 2>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb, kz);
   }
-  if (P >= 4) return launch_split_t<KP, HAS_E, HAS_P, 4, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
-  return launch_split_t<KP, HAS_E, HAS_P, 2, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb);
+  if (P >= 4) return launch_split_t<KP, HAS_E, HAS_P, 4, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb, kz);
+  return launch_split_t<KP, HAS_E, HAS_P, 2, 1>(N, d, k, V, X, ids, E, U, Z, Pt, st, S, Zb, kz);
 }
 
 // When the d-split kernel runs (measured on MI355X at d = 4096 and 5120):
@@ -978,6 +991,18 @@ static hipError_t launch_split_kp(int P, int TTW, int64_t N, int d, int k, int64
 static bool compress_uses_split(int64_t N, int64_t d, int64_t k, bool has_e) {
   if (d % 128 != 0) return false;
   if (k % 8 != 0) return true;
+  // The token-parallel kernel stages U in 16-byte row pieces only for k = 32,
+  // 64 and 128; for other k it moves a few elements per row and the d-split
+  // kernel wins (N = 12288 .. 32768, d = 4096 and 5120: compress 116 -> 61
+  // us at k = 40, N = 12288; project_grad 107 -> 57 us at k = 56, N = 32768).
+  // For k > 64 it does so only below about 24576 tokens and for an odd
+  // number of 16-column tiles (k = 72 and 112: 177 -> 98 us and 217 -> 100
+  // us at N = 12288; at k = 96 the token-parallel kernel stays ahead, 67
+  // against 99 us, and at 32768 tokens the d-split kernel's four-wave blocks
+  // fall behind).
+  const int kp = (int)((k + 15) / 16);
+  const bool wide = k == 16 * kp && (kp == 2 || kp == 4 || kp == 8);
+  if (!wide && (k <= 64 || (kp % 2 == 1 && N <= 24576))) return true;
   return N <= (has_e ? 8192 : 16384);
 }
 
@@ -1037,12 +1062,12 @@ static SplitPlan split_plan(int64_t N, int d, int k, bool has_e, int smax) {
 template <bool HAS_E, bool HAS_P>
 static hipError_t launch_split(int64_t N, int d, int k, int64_t V, const void* X, const int32_t* ids,
                                const void* E, const void* U, float* Z, const float* Pt,
-                               hipStream_t st, const SplitPlan& p, uint16_t* Zb = nullptr) {
+                               hipStream_t st, const SplitPlan& p, uint16_t* Zb, int kz) {
   if (k <= 32)
-    return launch_split_kp<2, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb);
+    return launch_split_kp<2, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb, kz);
   if (k <= 64)
-    return launch_split_kp<4, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb);
-  return launch_split_kp<8, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb);
+    return launch_split_kp<4, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb, kz);
+  return launch_split_kp<8, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb, kz);
 }
 
 // Sum of S partial results [S][n], in range order (deterministic).
@@ -1059,9 +1084,10 @@ __global__ __launch_bounds__(256) void sum_partials(const float* __restrict__ ws
 template <typename T, bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_generic(int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                                           const int32_t* ids, const void* E, const void* U,
-                                          float* Z, const float* P, hipStream_t st, uint16_t* Zb) {
+                                          float* Z, const float* P, hipStream_t st, uint16_t* Zb,
+                                          int64_t kz) {
   hipLaunchKernelGGL((compress_generic<T, HAS_E, HAS_P>), dim3(generic_blocks(N)), dim3(256), 0, st,
-                     (const T*)X, ids, (const T*)E, (const T*)U, Z, N, d, k, V, P, Zb);
+                     (const T*)X, ids, (const T*)E, (const T*)U, Z, N, d, k, V, P, Zb, kz);
   return hipGetLastError();
 }
 
@@ -1069,29 +1095,31 @@ static hipError_t launch_compress_generic(int64_t N, int64_t d, int64_t k, int64
 // Zb non-NULL: the coordinates go to Zb in bf16 (Z unused).
 hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                            const int32_t* ids, const void* E, const void* U, float* Z,
-                           const float* P, hipStream_t st, uint16_t* Zb) {
+                           const float* P, hipStream_t st, uint16_t* Zb, int kzarg) {
+  const int64_t kz64 = (kzarg <= 0 || kzarg > k) ? k : kzarg;
+  const int kz = (int)(kz64 < 128 ? kz64 : 128);   // the MFMA paths take k <= 128
   const bool has_e = (E != nullptr), has_p = (P != nullptr);
   const void* zout = Zb ? (const void*)Zb : (const void*)Z;
   if (compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(zout) && (!has_e || al16(E)) &&
       (!has_p || al16(P))) {
     if (compress_uses_split(N, d, k, has_e)) {
       const SplitPlan sp = split_plan(N, (int)d, (int)k, has_e, 1);
-      if (has_e) return launch_split<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp, Zb);
-      if (has_p) return launch_split<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp, Zb);
-      return launch_split<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp, Zb);
+      if (has_e) return launch_split<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp, Zb, kz);
+      if (has_p) return launch_split<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp, Zb, kz);
+      return launch_split<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, sp, Zb, kz);
     }
-    if (has_e) return launch_compress_mfma<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, Zb);
-    if (has_p) return launch_compress_mfma<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, Zb);
-    return launch_compress_mfma<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, Zb);
+    if (has_e) return launch_compress_mfma<true, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, Zb, kz);
+    if (has_p) return launch_compress_mfma<false, true>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, Zb, kz);
+    return launch_compress_mfma<false, false>(N, (int)d, (int)k, V, X, ids, E, U, Z, P, st, Zb, kz);
   }
   if (dtype == kF32) {
-    if (has_e) return launch_compress_generic<float, true, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-    if (has_p) return launch_compress_generic<float, false, true>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-    return launch_compress_generic<float, false, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+    if (has_e) return launch_compress_generic<float, true, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz64);
+    if (has_p) return launch_compress_generic<float, false, true>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz64);
+    return launch_compress_generic<float, false, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz64);
   }
-  if (has_e) return launch_compress_generic<uint16_t, true, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-  if (has_p) return launch_compress_generic<uint16_t, false, true>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
-  return launch_compress_generic<uint16_t, false, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb);
+  if (has_e) return launch_compress_generic<uint16_t, true, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz64);
+  if (has_p) return launch_compress_generic<uint16_t, false, true>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz64);
+  return launch_compress_generic<uint16_t, false, false>(N, d, k, V, X, ids, E, U, Z, P, st, Zb, kz64);
 }
 
 // Z = X.U; with few tokens the few-token kernel may split d into up to
@@ -1103,7 +1131,7 @@ hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, con
     const SplitPlan sp = split_plan(N, (int)d, (int)k, false, smax);
     if (sp.S > 1) {
       hipError_t e = launch_split<false, false>(N, (int)d, (int)k, 1, X, nullptr, nullptr, U, ws,
-                                                nullptr, st, sp);
+                                                nullptr, st, sp, nullptr, (int)k);
       if (e != hipSuccess) return e;
       const int64_t n = N * k;
       const int64_t blocks = (n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048;
@@ -1111,7 +1139,7 @@ hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, con
       return hipGetLastError();
     }
   }
-  return launch_compress(dtype, N, d, k, 1, X, nullptr, nullptr, U, Z, nullptr, st, nullptr);
+  return launch_compress(dtype, N, d, k, 1, X, nullptr, nullptr, U, Z, nullptr, st, nullptr, 0);
 }
 
 // 8 token tiles (128 tokens) per block, each of the 8 waves sweeping the
@@ -1128,7 +1156,7 @@ hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, con
 template <int KS2, bool HAS_E, int KM, bool GZ>
 static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
-                                       hipStream_t st, const uint16_t* Zb) {
+                                       hipStream_t st, const uint16_t* Zb, int kz) {
   constexpr int TW = 8;
   const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
   const int64_t cus = device_cu_count();
@@ -1157,32 +1185,32 @@ static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const
     hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ, false,
                                              1, 2>),
                        grid, dim3(64 * TW), 0, st, Zc, ids, (const uint16_t*)E, (const uint16_t*)U,
-                       (uint16_t*)Y, N, d, k, V, Zb);
+                       (uint16_t*)Y, N, d, k, V, Zb, kz);
   else
     hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ>), grid,
                        dim3(64 * TW), 0, st, Zc, ids, (const uint16_t*)E, (const uint16_t*)U,
-                       (uint16_t*)Y, N, d, k, V, Zb);
+                       (uint16_t*)Y, N, d, k, V, Zb, kz);
   return hipGetLastError();
 }
 
 template <int KS2, bool HAS_E, bool GZ>
 static hipError_t launch_decompress_ks(int64_t N, int d, int k, int64_t V, const float* Zc,
                                        const int32_t* ids, const void* E, const void* U, void* Y,
-                                       hipStream_t st, const uint16_t* Zb) {
-  if (k == 32 * KS2) return launch_decompress_km<KS2, HAS_E, 0, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
-  if (k % 8 == 0) return launch_decompress_km<KS2, HAS_E, 1, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
-  return launch_decompress_km<KS2, HAS_E, 2, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+                                       hipStream_t st, const uint16_t* Zb, int kz) {
+  if (k == 32 * KS2) return launch_decompress_km<KS2, HAS_E, 0, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz);
+  if (k % 8 == 0) return launch_decompress_km<KS2, HAS_E, 1, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz);
+  return launch_decompress_km<KS2, HAS_E, 2, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz);
 }
 
 template <bool HAS_E, bool GZ>
 static hipError_t launch_decompress_mfma(int64_t N, int d, int k, int64_t V, const float* Zc,
                                          const int32_t* ids, const void* E, const void* U, void* Y,
-                                         hipStream_t st, const uint16_t* Zb) {
+                                         hipStream_t st, const uint16_t* Zb, int kz) {
   switch ((k + 31) / 32) {
-    case 1: return launch_decompress_ks<1, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
-    case 2: return launch_decompress_ks<2, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
-    case 3: return launch_decompress_ks<3, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
-    default: return launch_decompress_ks<4, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+    case 1: return launch_decompress_ks<1, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz);
+    case 2: return launch_decompress_ks<2, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz);
+    case 3: return launch_decompress_ks<3, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz);
+    default: return launch_decompress_ks<4, HAS_E, GZ>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz);
   }
 }
 
@@ -1190,30 +1218,32 @@ template <typename T, bool HAS_E, bool GZ>
 static hipError_t launch_decompress_generic(int64_t N, int64_t d, int64_t k, int64_t V,
                                             const float* Zc, const int32_t* ids, const void* E,
                                             const void* U, void* Y, hipStream_t st,
-                                            const uint16_t* Zb) {
+                                            const uint16_t* Zb, int64_t kz) {
   hipLaunchKernelGGL((decompress_generic<T, HAS_E, GZ>), dim3(generic_blocks(N)), dim3(256), 0, st, Zc,
-                     ids, (const T*)E, (const T*)U, (T*)Y, N, d, k, V, Zb);
+                     ids, (const T*)E, (const T*)U, (T*)Y, N, d, k, V, Zb, kz);
   return hipGetLastError();
 }
 
 hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const float* Zc,
                              const int32_t* ids, const void* E, const void* U, void* Y,
-                             bool gather_z, hipStream_t st, const uint16_t* Zb) {
+                             bool gather_z, hipStream_t st, const uint16_t* Zb, int kzarg) {
+  const int64_t kz64 = (kzarg <= 0 || kzarg > k || gather_z) ? k : kzarg;
+  const int kz = (int)(kz64 < 128 ? kz64 : 128);   // the MFMA paths take k <= 128
   const bool has_e = (E != nullptr);
   const void* zin = Zb ? (const void*)Zb : (const void*)Zc;
   if (decompress_uses_mfma(dtype, d, k) && al16(zin) && al16(U) && al16(Y) && (!has_e || al16(E))) {
-    if (has_e) return launch_decompress_mfma<true, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb);
-    if (gather_z) return launch_decompress_mfma<false, true>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb);
-    return launch_decompress_mfma<false, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb);
+    if (has_e) return launch_decompress_mfma<true, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb, kz);
+    if (gather_z) return launch_decompress_mfma<false, true>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb, kz);
+    return launch_decompress_mfma<false, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb, kz);
   }
   if (dtype == kF32) {
-    if (has_e) return launch_decompress_generic<float, true, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
-    if (gather_z) return launch_decompress_generic<float, false, true>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
-    return launch_decompress_generic<float, false, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+    if (has_e) return launch_decompress_generic<float, true, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz64);
+    if (gather_z) return launch_decompress_generic<float, false, true>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz64);
+    return launch_decompress_generic<float, false, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz64);
   }
-  if (has_e) return launch_decompress_generic<uint16_t, true, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
-  if (gather_z) return launch_decompress_generic<uint16_t, false, true>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
-  return launch_decompress_generic<uint16_t, false, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb);
+  if (has_e) return launch_decompress_generic<uint16_t, true, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz64);
+  if (gather_z) return launch_decompress_generic<uint16_t, false, true>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz64);
+  return launch_decompress_generic<uint16_t, false, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz64);
 }
 
 }  // namespace ssn

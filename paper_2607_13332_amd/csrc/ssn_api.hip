@@ -74,12 +74,18 @@ static uint16_t* z_b16(ssn_dtype_t z_dtype, void* Z) {
   return z_dtype == SSN_BF16 ? (uint16_t*)Z : nullptr;
 }
 
+// A basis stored with rows of ldu >= k elements (a zero-padded copy: with
+// ldu a multiple of 8 the kernels take their aligned U paths for any k); the
+// launchers take the U row width as their k and the coordinate count as kz.
+static bool ldu_ok(int64_t k, int64_t ldu) { return ldu >= k && ldu <= (int64_t)1 << 31; }
+static int kz_of(int64_t k, int64_t ldu) { return ldu == k ? 0 : (int)k; }
+
 ssn_status_t ssn_compress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
                              int64_t k, int64_t V, const void* X, const int32_t* ids,
-                             const void* E, const void* U, void* Z, void* stream) {
+                             const void* E, const void* U, int64_t ldu, void* Z, void* stream) {
   if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
-  if (N < 0 || d < 1 || k < 1 || k > d || V < 1) return SSN_ERR_SHAPE;
-  if (!mul_ok(N, d) || !mul_ok(V, d) || !mul_ok(d, k) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
+  if (N < 0 || d < 1 || k < 1 || k > d || V < 1 || !ldu_ok(k, ldu)) return SSN_ERR_SHAPE;
+  if (!mul_ok(N, d) || !mul_ok(V, d) || !mul_ok(d, ldu) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
   if (N == 0) return SSN_OK;
   if (!X || !ids || !E || !U || !Z) return SSN_ERR_NULL;
   const int64_t s = elem_size(dtype), zs = elem_size(z_dtype);
@@ -88,25 +94,26 @@ ssn_status_t ssn_compress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, 
     return SSN_ERR_ALIGN;
   const Span out = span(Z, N * k * zs);
   if (overlap(out, span(X, N * d * s)) || overlap(out, span(E, V * d * s)) ||
-      overlap(out, span(U, d * k * s)) || overlap(out, span(ids, N * 4)))
+      overlap(out, span(U, d * ldu * s)) || overlap(out, span(ids, N * 4)))
     return SSN_ERR_ALIAS;
-  return launch_status(ssn::launch_compress(dtype, N, d, k, V, X, ids, E, U, z_f32(z_dtype, Z),
-                                            nullptr, (hipStream_t)stream, z_b16(z_dtype, Z)));
+  return launch_status(ssn::launch_compress(dtype, N, d, ldu, V, X, ids, E, U, z_f32(z_dtype, Z),
+                                            nullptr, (hipStream_t)stream, z_b16(z_dtype, Z),
+                                            kz_of(k, ldu)));
 }
 
 ssn_status_t ssn_compress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
                           const void* X, const int32_t* ids, const void* E, const void* U,
                           float* Z, void* stream) {
-  return ssn_compress_ex(dtype, SSN_F32, N, d, k, V, X, ids, E, U, Z, stream);
+  return ssn_compress_ex(dtype, SSN_F32, N, d, k, V, X, ids, E, U, k, Z, stream);
 }
 
 ssn_status_t ssn_compress_projected_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N,
                                        int64_t d, int64_t k, int64_t V, const void* X,
-                                       const int32_t* ids, const float* P, const void* U, void* Z,
-                                       void* stream) {
+                                       const int32_t* ids, const float* P, const void* U,
+                                       int64_t ldu, void* Z, void* stream) {
   if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
-  if (N < 0 || d < 1 || k < 1 || k > d || V < 1) return SSN_ERR_SHAPE;
-  if (!mul_ok(N, d) || !mul_ok(V, k) || !mul_ok(d, k) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
+  if (N < 0 || d < 1 || k < 1 || k > d || V < 1 || !ldu_ok(k, ldu)) return SSN_ERR_SHAPE;
+  if (!mul_ok(N, d) || !mul_ok(V, k) || !mul_ok(d, ldu) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
   if (N == 0) return SSN_OK;
   if (!X || !ids || !P || !U || !Z) return SSN_ERR_NULL;
   const int64_t s = elem_size(dtype), zs = elem_size(z_dtype);
@@ -115,26 +122,27 @@ ssn_status_t ssn_compress_projected_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, i
     return SSN_ERR_ALIGN;
   const Span out = span(Z, N * k * zs);
   if (overlap(out, span(X, N * d * s)) || overlap(out, span(P, V * k * 4)) ||
-      overlap(out, span(U, d * k * s)) || overlap(out, span(ids, N * 4)))
+      overlap(out, span(U, d * ldu * s)) || overlap(out, span(ids, N * 4)))
     return SSN_ERR_ALIAS;
-  return launch_status(ssn::launch_compress(dtype, N, d, k, V, X, ids, nullptr, U,
+  return launch_status(ssn::launch_compress(dtype, N, d, ldu, V, X, ids, nullptr, U,
                                             z_f32(z_dtype, Z), P, (hipStream_t)stream,
-                                            z_b16(z_dtype, Z)));
+                                            z_b16(z_dtype, Z), kz_of(k, ldu)));
 }
 
 ssn_status_t ssn_compress_projected(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
                                     const void* X, const int32_t* ids, const float* P,
                                     const void* U, float* Z, void* stream) {
-  return ssn_compress_projected_ex(dtype, SSN_F32, N, d, k, V, X, ids, P, U, Z, stream);
+  return ssn_compress_projected_ex(dtype, SSN_F32, N, d, k, V, X, ids, P, U, k, Z, stream);
 }
 
 ssn_status_t ssn_decompress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
                                int64_t k, int64_t V, const void* Z, const int32_t* ids,
-                               const void* E, const void* U, void* Xout, void* stream) {
+                               const void* E, const void* U, int64_t ldu, void* Xout,
+                               void* stream) {
   if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
   const bool has_e = (E != nullptr);
-  if (N < 0 || d < 1 || k < 1 || k > d || (has_e && V < 1)) return SSN_ERR_SHAPE;
-  if (!mul_ok(N, d) || !mul_ok(d, k) || !mul_ok(N, k) || (has_e && !mul_ok(V, d)))
+  if (N < 0 || d < 1 || k < 1 || k > d || (has_e && V < 1) || !ldu_ok(k, ldu)) return SSN_ERR_SHAPE;
+  if (!mul_ok(N, d) || !mul_ok(d, ldu) || !mul_ok(N, k) || (has_e && !mul_ok(V, d)))
     return SSN_ERR_SHAPE;
   if (N == 0) return SSN_OK;
   if ((E == nullptr) != (ids == nullptr)) return SSN_ERR_NULL;
@@ -144,40 +152,41 @@ ssn_status_t ssn_decompress_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N
       (has_e && (!aligned_to(E, s) || !aligned_to(ids, 4))))
     return SSN_ERR_ALIGN;
   const Span out = span(Xout, N * d * s);
-  if (overlap(out, span(Z, N * k * zs)) || overlap(out, span(U, d * k * s)) ||
+  if (overlap(out, span(Z, N * k * zs)) || overlap(out, span(U, d * ldu * s)) ||
       (has_e && (overlap(out, span(E, V * d * s)) || overlap(out, span(ids, N * 4)))))
     return SSN_ERR_ALIAS;
   void* zm = const_cast<void*>(Z);
-  return launch_status(ssn::launch_decompress(dtype, N, d, k, has_e ? V : 1, z_f32(z_dtype, zm),
+  return launch_status(ssn::launch_decompress(dtype, N, d, ldu, has_e ? V : 1, z_f32(z_dtype, zm),
                                               ids, E, U, Xout, false, (hipStream_t)stream,
-                                              z_b16(z_dtype, zm)));
+                                              z_b16(z_dtype, zm), kz_of(k, ldu)));
 }
 
 ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
                             const float* Z, const int32_t* ids, const void* E, const void* U,
                             void* Xout, void* stream) {
-  return ssn_decompress_ex(dtype, SSN_F32, N, d, k, V, Z, ids, E, U, Xout, stream);
+  return ssn_decompress_ex(dtype, SSN_F32, N, d, k, V, Z, ids, E, U, k, Xout, stream);
 }
 
 ssn_status_t ssn_project_grad_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
-                                 int64_t k, const void* G, const void* U, void* GZ, void* stream) {
+                                 int64_t k, const void* G, const void* U, int64_t ldu, void* GZ,
+                                 void* stream) {
   if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
-  if (N < 0 || d < 1 || k < 1 || k > d) return SSN_ERR_SHAPE;
-  if (!mul_ok(N, d) || !mul_ok(d, k) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
+  if (N < 0 || d < 1 || k < 1 || k > d || !ldu_ok(k, ldu)) return SSN_ERR_SHAPE;
+  if (!mul_ok(N, d) || !mul_ok(d, ldu) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
   if (N == 0) return SSN_OK;
   if (!G || !U || !GZ) return SSN_ERR_NULL;
   const int64_t s = elem_size(dtype), zs = elem_size(z_dtype);
   if (!aligned_to(G, s) || !aligned_to(U, s) || !aligned_to(GZ, zs)) return SSN_ERR_ALIGN;
   const Span out = span(GZ, N * k * zs);
-  if (overlap(out, span(G, N * d * s)) || overlap(out, span(U, d * k * s))) return SSN_ERR_ALIAS;
-  return launch_status(ssn::launch_compress(dtype, N, d, k, 1, G, nullptr, nullptr, U,
+  if (overlap(out, span(G, N * d * s)) || overlap(out, span(U, d * ldu * s))) return SSN_ERR_ALIAS;
+  return launch_status(ssn::launch_compress(dtype, N, d, ldu, 1, G, nullptr, nullptr, U,
                                             z_f32(z_dtype, GZ), nullptr, (hipStream_t)stream,
-                                            z_b16(z_dtype, GZ)));
+                                            z_b16(z_dtype, GZ), kz_of(k, ldu)));
 }
 
 ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, const void* G,
                               const void* U, float* GZ, void* stream) {
-  return ssn_project_grad_ex(dtype, SSN_F32, N, d, k, G, U, GZ, stream);
+  return ssn_project_grad_ex(dtype, SSN_F32, N, d, k, G, U, k, GZ, stream);
 }
 
 ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t k, const void* E,

@@ -21,10 +21,12 @@ bool weights_use_mfma(int dtype, int64_t d, int64_t k);
 
 // E non-NULL: Z = (X - E[ids]).U; P non-NULL: Z = X.U - P[ids]; neither: Z = X.U.
 // Zb non-NULL: the coordinates are written to Zb in bf16 (rounded to nearest
-// even) and Z is unused.
+// even) and Z is unused.  0 < kz < k: U rows are k wide but only their first
+// kz columns are coordinates (a zero-padded basis); Z and P rows hold kz
+// values.  kz <= 0: kz = k.
 hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                            const int32_t* ids, const void* E, const void* U, float* Z,
-                           const float* P, hipStream_t st, uint16_t* Zb = nullptr);
+                           const float* P, hipStream_t st, uint16_t* Zb = nullptr, int kz = 0);
 // Z = X.U (no E, no P).  With few tokens it may split d into up to smax
 // ranges whose partial products go to ws [S][N][k] (float32, S <= smax,
 // written before Z) and are summed into Z; ws NULL or smax <= 1: one launch.
@@ -32,9 +34,12 @@ hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, con
                                  const void* U, float* Z, float* ws, int smax, hipStream_t st);
 // E non-NULL: Y = E[ids] + Z U^T; gather_z: Y = Z[ids] U^T; else Y = Z U^T.
 // Zb non-NULL: the coordinates are read from Zb in bf16 and Z is unused.
+// 0 < kz < k: Z rows hold kz coordinates for the first kz of the k columns
+// of U (the rest must be zero); kz <= 0 (and gather_z): kz = k.
 hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V, const float* Z,
                              const int32_t* ids, const void* E, const void* U, void* Y,
-                             bool gather_z, hipStream_t st, const uint16_t* Zb = nullptr);
+                             bool gather_z, hipStream_t st, const uint16_t* Zb = nullptr,
+                             int kz = 0);
 // dZp[din, k] = H[N, din]^T . GT[N, k] (float32 GT and dZp); `ws` holds the
 // partial sums of the token splits (factor_grad_workspace_bytes).
 size_t factor_grad_workspace_bytes(int dtype, int64_t N, int64_t din, int64_t k);

@@ -49,16 +49,16 @@ def _declare(lib):
     lib.ssn_project_grad.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_compress_ex.restype = ctypes.c_int
     lib.ssn_compress_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
-                                    _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
+                                    _c_p, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]
     lib.ssn_decompress_ex.restype = ctypes.c_int
     lib.ssn_decompress_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
-                                      _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
+                                      _c_p, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]
     lib.ssn_project_grad_ex.restype = ctypes.c_int
     lib.ssn_project_grad_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
-                                        _c_p, _c_p, _c_p, _c_p]
+                                        _c_p, _c_p, _c_i64, _c_p, _c_p]
     lib.ssn_compress_projected_ex.restype = ctypes.c_int
     lib.ssn_compress_projected_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
-                                              _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
+                                              _c_i64, _c_p, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]
     lib.ssn_project_table.restype = ctypes.c_int
     lib.ssn_project_table.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_compress_projected.restype = ctypes.c_int
@@ -164,10 +164,12 @@ def _same_device(*ts):
 
 def compress(X: torch.Tensor, ids: torch.Tensor, E: torch.Tensor, U: torch.Tensor,
              out: Optional[torch.Tensor] = None, stream=None,
-             z_dtype: torch.dtype = torch.float32) -> torch.Tensor:
-    """Z = (X - E[ids]) U  ([N, k] in z_dtype: float32, or bfloat16 rounded once)."""
+             z_dtype: torch.dtype = torch.float32, k: Optional[int] = None) -> torch.Tensor:
+    """Z = (X - E[ids]) U  ([N, k] in z_dtype: float32, or bfloat16 rounded once).
+    k < U.shape[1]: U is a zero-padded basis whose first k columns are used."""
     N, d = X.shape
-    V, k = E.shape[0], U.shape[1]
+    V, ldu = E.shape[0], U.shape[1]
+    k = ldu if k is None else int(k)
     if E.shape[1] != d or U.shape[0] != d or ids.shape != (N,):
         raise ValueError(f"shape mismatch X{tuple(X.shape)} ids{tuple(ids.shape)} "
                          f"E{tuple(E.shape)} U{tuple(U.shape)}")
@@ -177,7 +179,7 @@ def compress(X: torch.Tensor, ids: torch.Tensor, E: torch.Tensor, U: torch.Tenso
     t = X.dtype
     _check("ssn_compress_ex", lib().ssn_compress_ex(
         _dt_code(t), _dt_code(z_dtype), N, d, k, V, _dev(X, "X", t, 2),
-        _dev(ids, "ids", torch.int32, 1), _dev(E, "E", t, 2), _dev(U, "U", t, 2),
+        _dev(ids, "ids", torch.int32, 1), _dev(E, "E", t, 2), _dev(U, "U", t, 2), ldu,
         _dev(out, "out", z_dtype, 2), _stream(stream)))
     return out
 
@@ -185,10 +187,11 @@ def compress(X: torch.Tensor, ids: torch.Tensor, E: torch.Tensor, U: torch.Tenso
 def decompress(Z: torch.Tensor, ids: Optional[torch.Tensor], E: Optional[torch.Tensor],
                U: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """X' = E[ids] + Z U^T (storage dtype of U); with ids = E = None, Z U^T.
-    Z is float32 or bfloat16 (the coordinate dtype on the wire)."""
+    Z is float32 or bfloat16 (the coordinate dtype on the wire); U may be a
+    zero-padded basis with more columns than Z."""
     N, k = Z.shape
-    d = U.shape[0]
-    if U.shape[1] != k:
+    d, ldu = U.shape
+    if ldu < k:
         raise ValueError(f"shape mismatch Z{tuple(Z.shape)} U{tuple(U.shape)}")
     if (E is None) != (ids is None):
         raise ValueError("pass both ids and E, or neither")
@@ -204,7 +207,7 @@ def decompress(Z: torch.Tensor, ids: Optional[torch.Tensor], E: Optional[torch.T
     _check("ssn_decompress_ex", lib().ssn_decompress_ex(
         _dt_code(t), _dt_code(Z.dtype), N, d, k, V, _dev(Z, "Z", Z.dtype, 2),
         None if ids is None else _dev(ids, "ids", torch.int32, 1),
-        None if E is None else _dev(E, "E", t, 2), _dev(U, "U", t, 2),
+        None if E is None else _dev(E, "E", t, 2), _dev(U, "U", t, 2), ldu,
         _dev(out, "out", t, 2), _stream(stream)))
     return out
 
@@ -216,10 +219,13 @@ def expand_grad(GZ: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] =
 
 
 def project_grad(G: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] = None,
-                 stream=None, z_dtype: torch.dtype = torch.float32) -> torch.Tensor:
-    """G_Z = G U ([N, k] in z_dtype: float32, or bfloat16 rounded once)."""
+                 stream=None, z_dtype: torch.dtype = torch.float32,
+                 k: Optional[int] = None) -> torch.Tensor:
+    """G_Z = G U ([N, k] in z_dtype: float32, or bfloat16 rounded once).
+    k < U.shape[1]: U is a zero-padded basis whose first k columns are used."""
     N, d = G.shape
-    k = U.shape[1]
+    ldu = U.shape[1]
+    k = ldu if k is None else int(k)
     if U.shape[0] != d:
         raise ValueError(f"shape mismatch G{tuple(G.shape)} U{tuple(U.shape)}")
     if out is None:
@@ -227,7 +233,7 @@ def project_grad(G: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] =
     _same_device(G, U, out)
     t = G.dtype
     _check("ssn_project_grad_ex", lib().ssn_project_grad_ex(
-        _dt_code(t), _dt_code(z_dtype), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2),
+        _dt_code(t), _dt_code(z_dtype), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2), ldu,
         _dev(out, "out", z_dtype, 2), _stream(stream)))
     return out
 
@@ -255,7 +261,8 @@ def compress_projected(X: torch.Tensor, ids: torch.Tensor, P: torch.Tensor, U: t
     """Z = X U - P[ids] ([N, k] in z_dtype), with P from project_table(E, U)."""
     N, d = X.shape
     V, k = P.shape
-    if U.shape != (d, k) or ids.shape != (N,):
+    ldu = U.shape[1]
+    if U.shape[0] != d or ldu < k or ids.shape != (N,):
         raise ValueError(f"shape mismatch X{tuple(X.shape)} ids{tuple(ids.shape)} "
                          f"P{tuple(P.shape)} U{tuple(U.shape)}")
     if out is None:
@@ -265,7 +272,7 @@ def compress_projected(X: torch.Tensor, ids: torch.Tensor, P: torch.Tensor, U: t
     _check("ssn_compress_projected_ex", lib().ssn_compress_projected_ex(
         _dt_code(t), _dt_code(z_dtype), N, d, k, V, _dev(X, "X", t, 2),
         _dev(ids, "ids", torch.int32, 1), _dev(P, "P", torch.float32, 2), _dev(U, "U", t, 2),
-        _dev(out, "out", z_dtype, 2), _stream(stream)))
+        ldu, _dev(out, "out", z_dtype, 2), _stream(stream)))
     return out
 
 

@@ -61,10 +61,11 @@ int main() {
           ssn_compress_projected((ssn_dtype_t)dt, N, d, k, 100, X, ids, T, U, Z, nullptr);
           ssn_factored_embedding((ssn_dtype_t)dt, N, d, k, 100, ids, T, U, Y, nullptr);
           for (int zt : {(int)SSN_F32, (int)SSN_BF16, 7}) {
-            ssn_compress_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, X, ids, E, U, Z, nullptr);
-            ssn_decompress_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, Z, ids, E, U, Y, nullptr);
-            ssn_project_grad_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, X, U, Z, nullptr);
-            ssn_compress_projected_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, X, ids, T, U, Z, nullptr);
+            ssn_compress_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, X, ids, E, U, k, Z, nullptr);
+            ssn_compress_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, X, ids, E, U, 64, Z, nullptr);
+            ssn_decompress_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, Z, ids, E, U, 64, Y, nullptr);
+            ssn_project_grad_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, X, U, BIG, Z, nullptr);
+            ssn_compress_projected_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, X, ids, T, U, k < BIG - 8 ? k + 5 : k, Z, nullptr);
           }
         }
   EXPECT(ssn_compress(SSN_BF16, 4096, 4096, 64, 131072, X, ids, E, U, Z, nullptr), SSN_OK);
@@ -78,13 +79,16 @@ int main() {
   EXPECT(ssn_decompress(SSN_BF16, 10, 4096, 64, 100, Z, ids, nullptr, U, Y, nullptr), SSN_ERR_NULL);
   EXPECT(ssn_decompress(SSN_BF16, 10, 4096, 64, 100, Z, nullptr, nullptr, U, Y, nullptr), SSN_OK);
   // bf16 coordinates: 2-byte alignment suffices, the span is N * k * 2 bytes
-  EXPECT(ssn_compress_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, 100, X, ids, E, U, (char*)Z + 2, nullptr), SSN_OK);
-  EXPECT(ssn_compress_ex(SSN_BF16, SSN_F32, 10, 4096, 64, 100, X, ids, E, U, (char*)Z + 2, nullptr), SSN_ERR_ALIGN);
-  EXPECT(ssn_compress_ex(SSN_BF16, (ssn_dtype_t)5, 10, 4096, 64, 100, X, ids, E, U, Z, nullptr), SSN_ERR_DTYPE);
-  EXPECT(ssn_decompress_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, 100, (char*)Y - 10 * 64 * 2, ids, E, U, Y, nullptr), SSN_OK);
-  EXPECT(ssn_decompress_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, 100, (char*)Y - 10 * 64 * 2 + 2, ids, E, U, Y, nullptr), SSN_ERR_ALIAS);
-  EXPECT(ssn_project_grad_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, X, U, (char*)X - 10 * 64 * 2, nullptr), SSN_OK);
-  EXPECT(ssn_project_grad_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, X, U, (char*)X - 10 * 64 * 2 + 2, nullptr), SSN_ERR_ALIAS);
+  EXPECT(ssn_compress_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, 100, X, ids, E, U, 64, (char*)Z + 2, nullptr), SSN_OK);
+  EXPECT(ssn_compress_ex(SSN_BF16, SSN_F32, 10, 4096, 51, 100, X, ids, E, U, 64, Z, nullptr), SSN_OK);
+  EXPECT(ssn_compress_ex(SSN_BF16, SSN_F32, 10, 4096, 51, 100, X, ids, E, U, 50, Z, nullptr), SSN_ERR_SHAPE);
+  EXPECT(ssn_compress_ex(SSN_BF16, SSN_F32, 10, 4096, 51, 100, X, ids, E, U, BIG, Z, nullptr), SSN_ERR_SHAPE);
+  EXPECT(ssn_compress_ex(SSN_BF16, SSN_F32, 10, 4096, 64, 100, X, ids, E, U, 64, (char*)Z + 2, nullptr), SSN_ERR_ALIGN);
+  EXPECT(ssn_compress_ex(SSN_BF16, (ssn_dtype_t)5, 10, 4096, 64, 100, X, ids, E, U, 64, Z, nullptr), SSN_ERR_DTYPE);
+  EXPECT(ssn_decompress_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, 100, (char*)Y - 10 * 64 * 2, ids, E, U, 64, Y, nullptr), SSN_OK);
+  EXPECT(ssn_decompress_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, 100, (char*)Y - 10 * 64 * 2 + 2, ids, E, U, 64, Y, nullptr), SSN_ERR_ALIAS);
+  EXPECT(ssn_project_grad_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, X, U, 64, (char*)X - 10 * 64 * 2, nullptr), SSN_OK);
+  EXPECT(ssn_project_grad_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, X, U, 64, (char*)X - 10 * 64 * 2 + 2, nullptr), SSN_ERR_ALIAS);
 
   // ---- weight re-projection: host arrays of every legal and illegal count ----
   for (int64_t count = -1; count <= SSN_MAX_BATCH + 2; ++count) {

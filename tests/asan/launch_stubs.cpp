@@ -17,12 +17,12 @@ bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) { return dtype == kBF
 bool weights_use_mfma(int dtype, int64_t d, int64_t k) { return dtype == kBF16 && d % 32 == 0 && k <= 128; }
 
 hipError_t launch_compress(int, int64_t, int64_t, int64_t, int64_t, const void*, const int32_t*,
-                           const void*, const void*, float*, const float*, hipStream_t, uint16_t*) {
+                           const void*, const void*, float*, const float*, hipStream_t, uint16_t*, int) {
   ++g_launches;
   return hipSuccess;
 }
 hipError_t launch_decompress(int, int64_t, int64_t, int64_t, int64_t, const float*, const int32_t*,
-                             const void*, const void*, void*, bool, hipStream_t, const uint16_t*) {
+                             const void*, const void*, void*, bool, hipStream_t, const uint16_t*, int) {
   ++g_launches;
   return hipSuccess;
 }

@@ -199,6 +199,9 @@ CODEC_SHAPES = [  # (N, d, k): tiles, ragged tails, every k bucket, both familie
     # few-token decompress / expansion with a fill-chosen split of d (5 and
     # 16 ranges)
     (12288, 5120, 51), (6144, 2048, 40),
+    # k % 8 == 0 without 16-byte U row pieces in the token-parallel kernel:
+    # the d-split kernel at many tokens (k = 56; k = 72, 112 below 24576)
+    (33325, 256, 56), (20000, 256, 72), (3000, 512, 112),
 ]
 
 
@@ -276,6 +279,49 @@ def test_bf16_coordinates(N, d, k, dtype):
     Yb = ssn.decompress(Zin, ids, E, U)
     Yf = ssn.decompress(Zin32, ids, E, U)
     assert torch.equal(Yb, Yf)
+
+
+PADDED_BASIS_SHAPES = [  # (N, d, k, ldu, dtype): a zero-padded basis, every kernel family
+    (4096, 5120, 51, 64, "bf16"), (12288, 5120, 51, 64, "bf16"), (2048, 2048, 40, 48, "bf16"),
+    (33325, 256, 51, 56, "bf16"), (300, 512, 17, 32, "bf16"), (1000, 4096, 100, 128, "bf16"),
+    (777, 384, 51, 64, "f32"), (200, 100, 10, 16, "bf16"),
+]
+
+
+@pytest.mark.parametrize("N,d,k,ldu,dtype", PADDED_BASIS_SHAPES)
+def test_padded_basis(N, d, k, ldu, dtype):
+    """U stored with rows of ldu >= k elements, columns k.. zero (a padded
+    copy of the fixed basis): every op matches the oracle run on the k-column
+    basis, and Z keeps k columns."""
+    V = 53
+    seed = N + 7 * d + k + ldu
+    print(f"[case] padded basis N={N} d={d} k={k} ldu={ldu} {dtype}", flush=True)
+    r = np.random.default_rng(seed)
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), dtype)
+    Eh = I.store(0.02 * r.standard_normal((V, d)), dtype)
+    Xh = I.store(r.standard_normal((N, d)), dtype)
+    ids_h = r.integers(0, V, size=N).astype(np.int32)
+    X, E, U, ids = dev(Xh, dtype), dev(Eh, dtype), dev(Uh, dtype), dev(ids_h, dtype)
+    Up = torch.zeros((d, ldu), dtype=U.dtype, device=DEV)
+    Up[:, :k] = U
+    outkind = "bf16out" if dtype == "bf16" else "f32out_dec"
+    Z = ssn.compress(X, ids, E, Up, k=k)
+    assert Z.shape == (N, k)
+    check("compress", host(Z), O.compress(Xh, ids_h, Eh, Uh), dtype, "f32out")
+    check("project_grad", host(ssn.project_grad(X, Up, k=k)), O.project_grad(Xh, Uh), dtype, "f32out")
+    P = ssn.project_table(E, U)
+    check("compress_projected", host(ssn.compress_projected(X, ids, P, Up)),
+          O.compress(Xh, ids_h, Eh, Uh), dtype, "f32out")
+    Zin = rand_coords(N, k, seed)
+    check("decompress", host(ssn.decompress(dev(Zin, "f32"), ids, E, Up)),
+          O.decompress(Zin, ids_h, Eh, Uh), dtype, outkind)
+    check("expand_grad", host(ssn.expand_grad(dev(Zin, "f32"), Up)), O.expand_grad(Zin, Uh), dtype, outkind)
+    # bf16 coordinates through the padded basis: the rounding of the fp32 result
+    Zb = ssn.compress(X, ids, E, Up, k=k, z_dtype=torch.bfloat16)
+    assert torch.equal(Zb, Z.to(torch.bfloat16))
+    Zbh = host(Zb)
+    check("decompress bf16 Z", host(ssn.decompress(Zb, ids, E, Up)), O.decompress(Zbh, ids_h, Eh, Uh),
+          dtype, outkind)
 
 
 SPLIT_SHAPES = [  # (N, d, k): few tokens -> the d-split compress kernels (P = 8, 4, 2),
