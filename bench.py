@@ -341,19 +341,20 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         sets.append(inp)
     ops = ["decompress", "project_grad", "compress", "expand_grad"]
 
-    def step(s, evs):
+    def step(s, evs, Ub=None):
+        Ub = U if Ub is None else Ub
         if evs:
             evs[0].record()
-        ssn.decompress(s["Zin"], s["ids"], E, U, out=s["Y"])
+        ssn.decompress(s["Zin"], s["ids"], E, Ub, out=s["Y"])
         if evs:
             evs[1].record()
-        ssn.project_grad(s["G"], U, out=s["GZ"])
+        ssn.project_grad(s["G"], Ub, out=s["GZ"], k=k)
         if evs:
             evs[2].record()
-        ssn.compress(s["X"], s["ids_c"], E, U, out=s["Z"])
+        ssn.compress(s["X"], s["ids_c"], E, Ub, out=s["Z"], k=k)
         if evs:
             evs[3].record()
-        ssn.expand_grad(s["GZin"], U, out=s["GX"])
+        ssn.expand_grad(s["GZin"], Ub, out=s["GX"])
         if evs:
             evs[4].record()
 
@@ -382,6 +383,29 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
            "ms_per_step_hip_graph": round(gms, 5),
            "tokens_per_s_hip_graph": round(N / (gms * 1e-3), 1),
            "per_op": per_op}
+    if k % 16 != 0:
+        # the same step with U zero-padded to whole 16-column tiles (a copy
+        # made once per basis), so that every kernel reads aligned U rows
+        ldu = 16 * ((k + 15) // 16)
+        Up = torch.zeros((d, ldu), dtype=U.dtype, device=dev)
+        Up[:, :k] = U
+        for i in range(warmup):
+            step(sets[i % 2], evs[0], Up)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            step(sets[i % 2], evs[i], Up)
+        torch.cuda.synchronize()
+        pms = (time.perf_counter() - t0) * 1e3 / steps
+        pgms = time_step_graph(sets, lambda s: step(s, None, Up), steps, warmup)
+        out["padded_basis"] = {
+            "what": f"U stored zero-padded to {ldu} columns (Z keeps k={k})",
+            "ms_per_step": round(pms, 5), "tokens_per_s": round(N / (pms * 1e-3), 1),
+            "ms_per_step_hip_graph": round(pgms, 5),
+            "tokens_per_s_hip_graph": round(N / (pgms * 1e-3), 1),
+            "per_op_ms": {op: round(float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])), 5)
+                          for j, op in enumerate(ops)}}
+        del Up
     del sets, base, U, E
     torch.cuda.empty_cache()
     return out
