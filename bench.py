@@ -183,14 +183,34 @@ def time_weights(wc, steps: int, dev):
     }
     if wc.name == I.WEIGHTS.name:
         out["traffic"] = load_traffic("project_weights")
+    if wc.k % 16 != 0:
+        # U stored with zero columns up to whole 16-column tiles: the same
+        # projection (the padding rows of U^T W are zero), aligned U paths
+        kp = 16 * ((wc.k + 15) // 16)
+        Up = torch.zeros((wc.d, kp), dtype=Uw.dtype, device=dev)
+        Up[:, :wc.k] = Uw
+        for _ in range(5):
+            ssn.project_weights_batched(Ws, Up)
+        ev[0].record()
+        for r in range(reps):
+            ssn.project_weights_batched(Ws, Up)
+            ev[r + 1].record()
+        torch.cuda.synchronize()
+        pms = sum(ev[r].elapsed_time(ev[r + 1]) for r in range(reps)) / reps
+        out["padded_basis"] = {"what": f"U stored zero-padded to {kp} columns", "ms": round(pms, 5),
+                               "frac_hbm_peak": round(wbytes / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        del Up
     del Ws
     torch.cuda.empty_cache()
     return out
 
 
-def time_reparam(N: int, din: int, d: int, k: int, steps: int, dev, seed: int = 1040):
+def time_reparam(N: int, din: int, d: int, k: int, steps: int, dev, seed: int = 1040,
+                 pad_to: int = 0):
     """Reparameterized-SSN projection of one layer: forward (H Zp) U^T and the
-    backward (G U, (G U) Zp^T, H^T (G U)), bf16 storage."""
+    backward (G U, (G U) Zp^T, H^T (G U)), bf16 storage.  pad_to > k: Zp and U
+    stored with zero columns up to pad_to (the same layer: the padding columns
+    of T, G U and the factor gradient stay zero)."""
     import numpy as np
     import torch
     from paper_2607_13332_amd import inputs as I
@@ -200,6 +220,13 @@ def time_reparam(N: int, din: int, d: int, k: int, steps: int, dev, seed: int = 
     G = torch.randn((N, d), generator=g, device=dev).to(torch.bfloat16)
     Zp = (0.02 * torch.randn((din, k), generator=g, device=dev)).to(torch.bfloat16)
     U = I.to_device(I.store(I.gaussian_orthonormal_basis(d, k, seed), "bf16"), "bf16", dev)
+    kalg = k
+    if pad_to > k:
+        Zq = torch.zeros((din, pad_to), dtype=torch.bfloat16, device=dev)
+        Uq = torch.zeros((d, pad_to), dtype=torch.bfloat16, device=dev)
+        Zq[:, :k] = Zp
+        Uq[:, :k] = U
+        Zp, U, k = Zq, Uq, pad_to
     T = torch.empty((N, k), dtype=torch.float32, device=dev)
     Y = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
     GT = torch.empty((N, k), dtype=torch.float32, device=dev)
@@ -221,9 +248,11 @@ def time_reparam(N: int, din: int, d: int, k: int, steps: int, dev, seed: int = 
     torch.cuda.synchronize()
     fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
     bwd = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
-    fb = 2.0 * N * din + 2.0 * N * d + 8.0 * N * k + 2.0 * (din + d) * k
-    bb = 2.0 * N * d + 4.0 * N * din + 12.0 * N * k + 2.0 * (din + d) * k + 4.0 * din * k
-    out = {"workload": f"one projection layer: H [{N}, {din}], Zp [{din}, {k}], U [{d}, {k}], bf16",
+    fb = 2.0 * N * din + 2.0 * N * d + 8.0 * N * kalg + 2.0 * (din + d) * kalg
+    bb = 2.0 * N * d + 4.0 * N * din + 12.0 * N * kalg + 2.0 * (din + d) * kalg + 4.0 * din * kalg
+    pad = f", stored zero-padded to {k} columns" if k != kalg else ""
+    out = {"workload": f"one projection layer: H [{N}, {din}], Zp [{din}, {kalg}], "
+                       f"U [{d}, {kalg}]{pad}, bf16",
            "forward_ms": round(fwd, 5),
            "forward_frac_hbm_peak": round(fb / (fwd * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "backward_ms": round(bwd, 5),
@@ -447,6 +476,8 @@ def run_section(name: str, args, dev):
     if name == "reparam":
         return {
             "paper8b_mlp_out": time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2), dev),
+            "paper8b_mlp_out_padded64": time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2),
+                                                     dev, pad_to=64),
             "stage8b_mlp_out": time_reparam(32768, 14336, 4096, 64, max(10, args.steps // 2), dev),
         }
     return time_sparta(I.SPARTA_BLOCK8B, args.steps, dev)
