@@ -56,6 +56,46 @@ def test_codec_step_replays_match_eager(N, d, k):
             assert torch.equal(got[key], ref[key]), f"replay {rep}: {key} differs from eager"
 
 
+def test_wire_formats_capture():
+    """bf16 coordinates and a zero-padded basis (the _ex entry points) capture
+    and replay like the plain step."""
+    N, d, k, V, ldu = 4096, 5120, 51, 4096, 64
+    print(f"[graph] bf16 coordinates, padded basis N={N} d={d} k={k} ldu={ldu}", flush=True)
+    static = _codec_inputs(N, d, k, V, 7200)
+    Up = torch.zeros((d, ldu), dtype=torch.bfloat16, device=DEV)
+    Zb = static["Zin"].to(torch.bfloat16)
+    outs = {"Y": torch.empty((N, d), dtype=torch.bfloat16, device=DEV),
+            "GZ": torch.empty((N, k), dtype=torch.bfloat16, device=DEV),
+            "Z": torch.empty((N, k), dtype=torch.bfloat16, device=DEV),
+            "GX": torch.empty((N, d), dtype=torch.bfloat16, device=DEV)}
+
+    def step(o):
+        ssn.decompress(Zb, static["ids"], static["E"], Up, out=o["Y"])
+        ssn.project_grad(static["G"], Up, out=o["GZ"], z_dtype=torch.bfloat16, k=k)
+        ssn.compress(static["X"], static["ids"], static["E"], Up, out=o["Z"], z_dtype=torch.bfloat16, k=k)
+        ssn.expand_grad(Zb, Up, out=o["GX"])
+
+    Up[:, :k] = static["U"]
+    step(outs)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(outs)
+    for rep in range(3):
+        fresh = _codec_inputs(N, d, k, V, 7300 + rep)
+        for key in ("X", "G", "E", "ids"):
+            static[key].copy_(fresh[key])
+        Up[:, :k] = fresh["U"]
+        Zb.copy_(fresh["Zin"].to(torch.bfloat16))
+        g.replay()
+        got = {key: v.clone() for key, v in outs.items()}
+        ref = {key: torch.empty_like(v) for key, v in outs.items()}
+        step(ref)
+        torch.cuda.synchronize()
+        for key in outs:
+            assert torch.equal(got[key], ref[key]), f"replay {rep}: {key} differs from eager"
+
+
 def test_reparam_and_averaging_capture():
     """The reparameterized layer (forward + backward with its workspace) and
     a delta-rule round in one graph."""
