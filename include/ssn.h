@@ -239,6 +239,11 @@ ssn_status_t ssn_project_weights_batched(ssn_dtype_t dtype, int64_t count, int64
  *   U  [d, k]   dtype   the shared basis
  * Shape rules: 1 <= k <= d, k <= din; N == 0 is a no-op (backward: GZp = 0).
  * All intermediate products accumulate in fp32; bf16 outputs are rounded once.
+ * Zp and U may be stored with zero columns appended up to a whole number of
+ * 16-column tiles (pass the padded width as k): that is the same layer, the
+ * padding columns of T, GT and GZp stay zero, and the kernels take their
+ * aligned paths (k = 51 padded to 64 at din = 18432, d = 5120, N = 4096:
+ * forward and backward 175 -> 155 us on MI355X).
  */
 
 /*
