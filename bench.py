@@ -65,6 +65,10 @@ def parse_args():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=200,
                    help="untimed steps first (the GPU's clocks settle after ~30 ms of sustained load)")
+    p.add_argument("--settle-seconds", type=float, default=3.0,
+                   help="before the warmup steps, untimed steps for this long: the first GPU "
+                        "process on an idle box runs at lower clocks for a while (the headline "
+                        "step measured 336 us cold against 301 us in the next process)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-weights", action="store_true")
     p.add_argument("--no-sweep", action="store_true",
@@ -141,9 +145,27 @@ def cpu_baseline(sample, cfg, seconds: float):
         el = time.perf_counter() - t0
         if el >= seconds:
             break
-    return {"value": done / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n} of the {cfg.N} tokens of one microbatch (d={cfg.d}, k={cfg.k}), "
-                      f"all four codec ops in float64, repeated {done // n}x over {el:.1f} s"}
+    out = {"value": done / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+           "sample": f"{n} of the {cfg.N} tokens of one microbatch (d={cfg.d}, k={cfg.k}), "
+                     f"all four codec ops in float64, repeated {done // n}x over {el:.1f} s"}
+    try:
+        # the same oracle on one core, over a quarter of the time
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            done1, t1 = 0, time.perf_counter()
+            while True:
+                O.decompress(sample["Zin"], sample["ids"], sample["E"], sample["U"])
+                O.project_grad(sample["G"], sample["U"])
+                O.compress(sample["X"], sample["ids"], sample["E"], sample["U"])
+                O.expand_grad(sample["GZin"], sample["U"])
+                done1 += n
+                el1 = time.perf_counter() - t1
+                if el1 >= seconds / 4:
+                    break
+        out["single_core_value"] = done1 / el1
+    except Exception:
+        pass
+    return out
 
 
 def time_weights(wc, steps: int, dev):
@@ -549,6 +571,12 @@ def main():
     if args.copy_calib:
         copy_calibration(args.copy_calib, dev)
 
+    # untimed: the clock ramp of an idle GPU, then the warmup steps
+    t_settle = time.perf_counter() + max(0.0, args.settle_seconds)
+    while time.perf_counter() < t_settle:
+        for i in range(64):
+            step(sets[i % 2])
+        torch.cuda.synchronize()
     for i in range(args.warmup):
         step(sets[i % 2])
     torch.cuda.synchronize()
