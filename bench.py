@@ -21,7 +21,7 @@ embedding table (Z = X U - (E U)[ids], table formed once outside the timed
 region) is timed separately and reported under "variants"; the headline value
 is the step with compress as written in Eq. (2).  The same step at the
 paper's own stage shapes (Pluralis-8B d=5120, k=51, V=128,256, S=4096; the 1B
-ablation model d=2048, k=40, S=2048; b = 1 and 3 coalesced sequences) and the
+ablation model d=2048, k=40, S=2048; b = 1, 2 and 3 coalesced sequences) and the
 weight re-projection at those shapes are reported under "paper_shapes", and
 the k=64 points of the sweep (d=4096, N=4096..131072, Zipf(1.1) ids) under
 "sweep_k64".
@@ -82,9 +82,11 @@ def parse_args():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle baseline sample")
     p.add_argument("--tokens", type=int, default=0, help="override N (testing only)")
-    p.add_argument("--only", choices=("reparam", "sparta"), default=None,
+    p.add_argument("--only", choices=("reparam", "sparta", "sweep", "paper", "weights"), default=None,
                    help="profiling aid: run only this section and print its JSON (no headline; "
                         "keeps its kernels apart from the codec's in a kernel trace)")
+    p.add_argument("--sweep-tokens", type=str, default="",
+                   help="with --only sweep / paper: comma-separated token counts to keep")
     p.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                    help="before the timed region, run a plain device copy of MIB MiB three times "
                         "(a known-size kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE); "
@@ -126,45 +128,56 @@ def load_traffic(kernel_key: str):
     return None if ent is None else ent.get("bytes_per_launch")
 
 
-def cpu_baseline(sample, cfg, seconds: float):
-    """The float64 oracle on a bounded token sample, on this host's cores."""
-    from oracle import ssn_oracle as O
+def cpu_model() -> str:
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
-    n = sample["X"].shape[0]
-    done, t0 = 0, time.perf_counter()
-    while True:
-        O.decompress(sample["Zin"], sample["ids"], sample["E"], sample["U"])
-        O.project_grad(sample["G"], sample["U"])
-        O.compress(sample["X"], sample["ids"], sample["E"], sample["U"])
-        O.expand_grad(sample["GZin"], sample["U"])
-        done += n
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    out = {"value": done / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-           "sample": f"{n} of the {cfg.N} tokens of one microbatch (d={cfg.d}, k={cfg.k}), "
-                     f"all four codec ops in float64, repeated {done // n}x over {el:.1f} s"}
-    try:
-        # the same oracle on one core, over a quarter of the time
-        from threadpoolctl import threadpool_limits
-        with threadpool_limits(limits=1):
-            done1, t1 = 0, time.perf_counter()
-            while True:
-                O.decompress(sample["Zin"], sample["ids"], sample["E"], sample["U"])
-                O.project_grad(sample["G"], sample["U"])
-                O.compress(sample["X"], sample["ids"], sample["E"], sample["U"])
-                O.expand_grad(sample["GZin"], sample["U"])
-                done1 += n
-                el1 = time.perf_counter() - t1
-                if el1 >= seconds / 4:
-                    break
-        out["single_core_value"] = done1 / el1
-    except Exception:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
         pass
+    return "unknown"
+
+
+def cpu_baseline(sample, cfg, seconds: float):
+    """The float64 oracle on a bounded token sample, on this host's cores:
+    BLAS threads set to the cores this process may run on."""
+    from oracle import ssn_oracle as O
+    cores = len(os.sched_getaffinity(0))
+
+    def run(budget):
+        n = sample["X"].shape[0]
+        done, t0 = 0, time.perf_counter()
+        while True:
+            O.decompress(sample["Zin"], sample["ids"], sample["E"], sample["U"])
+            O.project_grad(sample["G"], sample["U"])
+            O.compress(sample["X"], sample["ids"], sample["E"], sample["U"])
+            O.expand_grad(sample["GZin"], sample["U"])
+            done += n
+            el = time.perf_counter() - t0
+            if el >= budget:
+                return done, el
+
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:
+        threadpool_limits = None
+    n = sample["X"].shape[0]
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=cores):
+            done, el = run(seconds)
+    else:
+        done, el = run(seconds)
+    out = {"value": done / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+           "cpu_model": cpu_model(),
+           "sample": f"{n} of the {cfg.N} tokens of one microbatch (d={cfg.d}, k={cfg.k}), "
+                     f"all four codec ops in float64 with BLAS on {cores} threads, "
+                     f"repeated {done // n}x over {el:.1f} s"}
+    if threadpool_limits is not None:
+        # the same oracle on one core, over a quarter of the time
+        with threadpool_limits(limits=1):
+            done1, el1 = run(seconds / 4)
+        out["single_core_value"] = done1 / el1
     return out
 
 
@@ -495,6 +508,14 @@ def copy_rate(dev, mib: int = 512, reps: int = 20) -> float:
 
 def run_section(name: str, args, dev):
     from paper_2607_13332_amd import inputs as I
+    keep = {int(x) for x in args.sweep_tokens.split(",") if x.strip()}
+    if name in ("sweep", "paper"):
+        cfgs = ([c for c in I.sweep_configs() if c.k == 64] if name == "sweep" else I.paper_configs())
+        return {c.name: time_codec_config(c, max(10, args.steps // 2), args.warmup, dev)
+                for c in cfgs if not keep or c.N in keep}
+    if name == "weights":
+        return {wc.name: time_weights(wc, args.steps, dev)
+                for wc in (I.WEIGHTS, I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B)}
     if name == "reparam":
         return {
             "paper8b_mlp_out": time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2), dev),
@@ -753,8 +774,7 @@ def main():
     if not args.no_paper_shapes:
         shapes = {}
         for pc in I.paper_configs():
-            if pc.B in (1, 3):
-                shapes[pc.name] = time_codec_config(pc, max(10, args.steps // 2), args.warmup, dev)
+            shapes[pc.name] = time_codec_config(pc, max(10, args.steps // 2), args.warmup, dev)
         for wc in (I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B):
             shapes[wc.name] = time_weights(wc, args.steps, dev)
         result["paper_shapes"] = shapes

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define SSN_ABI_VERSION 1
+#define SSN_ABI_VERSION 2
 /* Largest matrix count accepted by ssn_project_weights_batched. */
 #define SSN_MAX_BATCH 16
 /* Largest sender count accepted by ssn_sparta_average. */
@@ -213,9 +213,19 @@ ssn_status_t ssn_compress_projected_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, i
  *   W <- U . (U^T . W)        in place, W [d, n] dtype, U [d, k] dtype
  * U^T W is accumulated in fp32 and never leaves the chip; W is read once and
  * written once.  Requires 1 <= k <= d.  k > 1024 is SSN_ERR_UNSUPPORTED.
+ * `workspace` (device, caller-owned) holds at least
+ * ssn_project_weights_workspace_bytes(d, n, k) bytes, else SSN_ERR_SHAPE; it
+ * may be NULL when that size is 0.  The kernels keep the k x n partial
+ * product U^T W in registers and LDS of the compute unit that owns those
+ * columns (each block reads its whole column strip of W before writing it
+ * back), so the size is 0 for every shape today; the argument keeps room for
+ * a split of d across blocks, which would stage U^T W in device memory.
+ * Matrices wider than 2^31 - 1 columns run the generic kernel.
  */
+size_t ssn_project_weights_workspace_bytes(int64_t d, int64_t n, int64_t k);
 ssn_status_t ssn_project_weights(ssn_dtype_t dtype, int64_t d, int64_t n, int64_t k,
-                                 void *W, const void *U, void *stream);
+                                 void *W, const void *U, void *workspace, size_t workspace_bytes,
+                                 void *stream);
 
 /*
  * ssn_project_weights_batched -- the same re-projection for `count` matrices
@@ -312,6 +322,20 @@ ssn_status_t ssn_factored_embedding(ssn_dtype_t dtype, int64_t N, int64_t d, int
  * All arithmetic is float32; m == 0 is a no-op.  Segment calls whose pointers
  * are 16-byte aligned (and m % 4 == 0) use 16-byte accesses.
  */
+
+/*
+ * ssn_sparta_segment -- the segment averaged in round r: the run shares
+ * p = 1/segments of the parameters per round, and consecutive rounds cover
+ * every parameter once per `segments` rounds (p = 5 %, 20 rounds in the
+ * paper).  Segment s = [floor(s n / S), floor((s + 1) n / S)) for
+ * S = segments, and round r averages segment r mod S: the S segments tile
+ * [0, n) in order and their sizes differ by at most one.  Host function (no
+ * HIP call): writes *first and *m, the arguments of the segment form above.
+ * Requires n >= 0, r >= 0, 1 <= segments <= 2^20 (else SSN_ERR_SHAPE) and
+ * non-NULL outputs (SSN_ERR_NULL).
+ */
+ssn_status_t ssn_sparta_segment(int64_t n, int64_t r, int64_t segments, int64_t *first,
+                                int64_t *m);
 
 /*
  * ssn_sparta_snapshot -- snap[i] = theta[P_i], the copy each replica takes at

@@ -177,6 +177,20 @@ def sparta_indices(n: int, m: int, I=None, first: int = 0) -> np.ndarray:
     return np.arange(first, first + m, dtype=np.int64)
 
 
+def sparta_segment(n: int, r: int, segments: int = 20):
+    """(first, m) of the segment averaged in round r.  The run shares a 1/20
+    share of the parameters per round and consecutive rounds cover every
+    parameter once per 20 rounds (sections 3.3.1 and 5.2); read here as
+    `segments` contiguous segments, segment s = [floor(s n / S), floor((s+1) n / S)),
+    visited in order, round r taking segment r mod S."""
+    if n < 0 or r < 0 or segments < 1:
+        raise ValueError("n >= 0, r >= 0 and segments >= 1")
+    s = r % segments
+    lo = (s * n) // segments
+    hi = ((s + 1) * n) // segments
+    return lo, hi - lo
+
+
 def sparta_snapshot(theta, idx) -> np.ndarray:
     """snap = theta[P]."""
     return f64(theta)[np.asarray(idx, dtype=np.int64)]
@@ -199,15 +213,27 @@ def delta_rule(theta, idx, avg, snap, lam: float = 1.0) -> np.ndarray:
     return out
 
 
-def rel_frobenius(got, ref) -> float:
-    """||got - ref||_F / ||ref||_F in float64 (the parity metric)."""
+def rel_frobenius(got, ref, scale=None) -> float:
+    """The parity metric: ||got - ref||_F / ||ref||_F in float64, got widened
+    exactly from its stored dtype (bf16 bit patterns included).
+
+    When the reference is all zero there is no relative error to take; the
+    bar is then an absolute one, ||got||_F <= tol * ||inputs||_F, so this
+    returns ||got||_F / scale with `scale` the Frobenius norm of the inputs
+    that produced the output.  Without a scale a zero reference is met only
+    by an exactly zero output (0.0), anything else is infinitely far (inf).
+    """
     g = f64(got) if np.asarray(got).dtype == np.uint16 else np.asarray(got, dtype=np.float64)
     r = np.asarray(ref, dtype=np.float64)
+    if g.shape != r.shape:
+        raise ValueError(f"shape mismatch {g.shape} vs {r.shape}")
     den = np.linalg.norm(r)
-    num = np.linalg.norm(g - r)
-    if den == 0.0:
-        return float(num)
-    return float(num / den)
+    if den > 0.0:
+        return float(np.linalg.norm(g - r) / den)
+    num = np.linalg.norm(g)
+    if scale is not None and scale > 0.0:
+        return float(num / scale)
+    return 0.0 if num == 0.0 else float("inf")
 
 
 # --------------------------------------------------------------------------
@@ -221,7 +247,9 @@ def boundary_bits(n_tokens: int, width: float, bits_per_value: int = 32) -> floa
 
 def bandwidth_floor_bits_per_s(a_f: float, a_b: float, seq_len: int, width: float,
                                ar_bits: int, ar_payload_params: float, ar_time_s: float) -> float:
-    """Per-contributor bandwidth estimate of section 3.5: forward + backward
-    activation payloads in FP32 at the given wire width, plus one all-reduce
-    burst of `ar_payload_params` values of `ar_bits` bits every `ar_time_s`."""
+    """Per-contributor bandwidth estimate of section 3.5.2 (estimated
+    communication): a_f forward and a_b backward activation payloads per
+    second, each seq_len x width values in FP32, plus one all-reduce of
+    `ar_payload_params` values of `ar_bits` bits every `ar_time_s` seconds
+    (with SPARTA the payload is the sparse share of the stage's parameters)."""
     return 32.0 * (a_f + a_b) * seq_len * width + ar_bits * ar_payload_params / ar_time_s

@@ -332,14 +332,38 @@ ssn_status_t ssn_project_weights_batched(ssn_dtype_t dtype, int64_t count, int64
                                                    (hipStream_t)stream));
 }
 
+size_t ssn_project_weights_workspace_bytes(int64_t d, int64_t n, int64_t k) {
+  (void)d;
+  (void)n;
+  (void)k;
+  return 0;   // U^T W stays on the compute unit that owns its columns
+}
+
 ssn_status_t ssn_project_weights(ssn_dtype_t dtype, int64_t d, int64_t n, int64_t k, void* W,
-                                 const void* U, void* stream) {
+                                 const void* U, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
   void* w[1] = {W};
   const int64_t nn[1] = {n};
   if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;
-  if (n == 0 && d >= 1 && k >= 1 && k <= d) return SSN_OK;
-  if (n > 0 && !W) return SSN_ERR_NULL;
+  if (d < 1 || k < 1 || k > d || n < 0) return SSN_ERR_SHAPE;
+  const size_t need = ssn_project_weights_workspace_bytes(d, n, k);
+  if (workspace_bytes < need || (need > 0 && !workspace)) return SSN_ERR_SHAPE;
+  if (n == 0) return SSN_OK;
+  if (!W) return SSN_ERR_NULL;
   return ssn_project_weights_batched(dtype, 1, d, nn, k, w, U, stream);
+}
+
+ssn_status_t ssn_sparta_segment(int64_t n, int64_t r, int64_t segments, int64_t* first,
+                                int64_t* m) {
+  if (n < 0 || r < 0 || segments < 1 || segments > ((int64_t)1 << 20)) return SSN_ERR_SHAPE;
+  if (!first || !m) return SSN_ERR_NULL;
+  // floor(s n / S) without forming s n: n = q S + rem, so s n / S = s q + s rem / S
+  const int64_t s = r % segments, q = n / segments, rem = n % segments;
+  const int64_t lo = s * q + (s * rem) / segments;
+  const int64_t hi = (s + 1) * q + ((s + 1) * rem) / segments;
+  *first = lo;
+  *m = hi - lo;
+  return SSN_OK;
 }
 
 // Index set of a sparse-averaging round: the list form needs n >= 1, the

@@ -599,14 +599,19 @@ hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t
                                   void* const* W, const void* U, hipStream_t st) {
   bool aligned = (((uintptr_t)U & 15u) == 0);
   bool cols8 = true;
+  // the MFMA kernels keep each matrix's row stride n in 32 bits; wider
+  // matrices take the generic kernel, whose indexing is 64-bit throughout
+  bool n32 = true;
   int64_t panels = 0, tiles = 0;
   for (int b = 0; b < count; ++b) {
     aligned = aligned && (((uintptr_t)W[b] & 15u) == 0);
     cols8 = cols8 && (n[b] % 8 == 0);
+    n32 = n32 && n[b] <= INT32_MAX;
     panels += (n[b] + 63) / 64;
     tiles += (n[b] + 15) / 16;
   }
-  if (weights_use_mfma(dtype, d, k) && aligned && cols8 && tiles <= INT32_MAX / 2) {
+  const bool mfma = weights_use_mfma(dtype, d, k) && aligned && n32;
+  if (mfma && cols8 && tiles <= INT32_MAX / 2) {
     ColumnBatch cb{};
     int nb = 0;
     int32_t acc = 0;
@@ -629,7 +634,7 @@ hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t
     return launch_cols<8>(cb, cus, U, (int)d, (int)k, st);
   }
   // the 64-column panel kernel reads U rows as 16-byte pieces: k % 8 == 0
-  if (weights_use_mfma(dtype, d, k) && k % 8 == 0 && aligned && panels <= INT32_MAX) {
+  if (mfma && k % 8 == 0 && panels <= INT32_MAX) {
     PanelBatch pb{};
     int nb = 0;
     int32_t acc = 0;

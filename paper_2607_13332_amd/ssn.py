@@ -76,8 +76,14 @@ def _declare(lib):
     lib.ssn_factored_embedding.restype = ctypes.c_int
     lib.ssn_factored_embedding.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
                                            _c_p, _c_p, _c_p, _c_p, _c_p]
+    lib.ssn_project_weights_workspace_bytes.restype = ctypes.c_size_t
+    lib.ssn_project_weights_workspace_bytes.argtypes = [_c_i64, _c_i64, _c_i64]
     lib.ssn_project_weights.restype = ctypes.c_int
-    lib.ssn_project_weights.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]
+    lib.ssn_project_weights.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p,
+                                        ctypes.c_size_t, _c_p]
+    lib.ssn_sparta_segment.restype = ctypes.c_int
+    lib.ssn_sparta_segment.argtypes = [_c_i64, _c_i64, _c_i64, ctypes.POINTER(_c_i64),
+                                       ctypes.POINTER(_c_i64)]
     lib.ssn_sparta_snapshot.restype = ctypes.c_int
     lib.ssn_sparta_snapshot.argtypes = [_c_i64, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_p]
     lib.ssn_sparta_average.restype = ctypes.c_int
@@ -347,15 +353,29 @@ def factored_embedding(ids: torch.Tensor, E: torch.Tensor, U: torch.Tensor,
     return out
 
 
-def project_weights(W: torch.Tensor, U: torch.Tensor, stream=None) -> torch.Tensor:
-    """In place: W <- U (U^T W) for W [d, n]."""
+def project_weights_workspace_bytes(d: int, n: int, k: int) -> int:
+    return int(lib().ssn_project_weights_workspace_bytes(d, n, k))
+
+
+def project_weights(W: torch.Tensor, U: torch.Tensor, workspace: Optional[torch.Tensor] = None,
+                    stream=None) -> torch.Tensor:
+    """In place: W <- U (U^T W) for W [d, n].  `workspace` (device memory of at
+    least project_weights_workspace_bytes(d, n, k) bytes) is allocated here
+    when it is needed and not given."""
     d, n = W.shape
+    k = U.shape[1]
     if U.shape[0] != d:
         raise ValueError(f"shape mismatch W{tuple(W.shape)} U{tuple(U.shape)}")
-    _same_device(W, U)
+    need = project_weights_workspace_bytes(d, n, k)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=W.device)
+    _same_device(W, U, workspace)
     t = W.dtype
+    wptr = None if workspace is None else _dev(workspace, "workspace")
+    wbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check("ssn_project_weights", lib().ssn_project_weights(
-        _dt_code(t), d, n, U.shape[1], _dev(W, "W", t, 2), _dev(U, "U", t, 2), _stream(stream)))
+        _dt_code(t), d, n, k, _dev(W, "W", t, 2), _dev(U, "U", t, 2), wptr, wbytes,
+        _stream(stream)))
     return W
 
 
@@ -387,14 +407,11 @@ SPARTA_SEGMENTS = 20
 
 
 def sparta_segment(n: int, r: int, segments: int = SPARTA_SEGMENTS):
-    """(first, m) of the segment averaged in round r: `segments` contiguous
-    segments tile [0, n) (sizes differ by at most one) and rounds rotate
-    through them in order."""
-    if n < 0 or segments < 1:
-        raise ValueError("n >= 0 and segments >= 1")
-    s = r % segments
-    first = s * n // segments
-    return first, (s + 1) * n // segments - first
+    """(first, m) of the segment averaged in round r (ssn_sparta_segment)."""
+    first, m = _c_i64(), _c_i64()
+    _check("ssn_sparta_segment", lib().ssn_sparta_segment(n, r, segments, ctypes.byref(first),
+                                                          ctypes.byref(m)))
+    return first.value, m.value
 
 
 def _positions(I, m, first):

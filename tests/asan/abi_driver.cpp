@@ -110,8 +110,24 @@ int main() {
     void* V2[2] = {P(0x800000000000), P(0x800000000000 + 64)};   // overlapping
     EXPECT(ssn_project_weights_batched(SSN_BF16, 2, 4096, m, 64, V2, U, nullptr), SSN_ERR_ALIAS);
   }
-  EXPECT(ssn_project_weights(SSN_BF16, 4096, 14336, 64, X, U, nullptr), SSN_OK);
-  EXPECT(ssn_project_weights(SSN_BF16, BIG, 14336, 64, X, U, nullptr), SSN_ERR_SHAPE);
+  EXPECT(ssn_project_weights_workspace_bytes(4096, 14336, 64), (size_t)0);
+  EXPECT(ssn_project_weights(SSN_BF16, 4096, 14336, 64, X, U, nullptr, 0, nullptr), SSN_OK);
+  EXPECT(ssn_project_weights(SSN_BF16, 4096, 14336, 64, X, U, Z, 64, nullptr), SSN_OK);
+  EXPECT(ssn_project_weights(SSN_BF16, BIG, 14336, 64, X, U, nullptr, 0, nullptr), SSN_ERR_SHAPE);
+  EXPECT(ssn_project_weights(SSN_BF16, 4096, -1, 64, X, U, nullptr, 0, nullptr), SSN_ERR_SHAPE);
+  EXPECT(ssn_project_weights(SSN_BF16, 4096, 0, 64, nullptr, nullptr, nullptr, 0, nullptr), SSN_OK);
+  {
+    int64_t f = -1, m = -1;
+    EXPECT(ssn_sparta_segment(10, 1, 4, &f, &m), SSN_OK);
+    EXPECT(f, (int64_t)2);
+    EXPECT(m, (int64_t)3);
+    EXPECT(ssn_sparta_segment(((int64_t)1 << 56) - 1, ((int64_t)1 << 62), 1 << 20, &f, &m), SSN_OK);
+    EXPECT(ssn_sparta_segment(-1, 0, 20, &f, &m), SSN_ERR_SHAPE);
+    EXPECT(ssn_sparta_segment(10, -1, 20, &f, &m), SSN_ERR_SHAPE);
+    EXPECT(ssn_sparta_segment(10, 0, 0, &f, &m), SSN_ERR_SHAPE);
+    EXPECT(ssn_sparta_segment(10, 0, (1 << 20) + 1, &f, &m), SSN_ERR_SHAPE);
+    EXPECT(ssn_sparta_segment(10, 0, 20, nullptr, &m), SSN_ERR_NULL);
+  }
 
   // ---- reparameterized layer ----
   for (int64_t N : {(int64_t)0, (int64_t)1, (int64_t)4096, BIG})

@@ -48,7 +48,7 @@ def test_every_declared_symbol_is_exported(ssn):
 
 def test_version_and_status_strings(ssn):
     L = ssn.lib()
-    assert L.ssn_abi_version() == 1
+    assert L.ssn_abi_version() == 2
     assert L.ssn_status_string(OK) == b"ok"
     assert L.ssn_status_string(ERR_ALIAS) == b"output overlaps an input"
     assert L.ssn_status_string(99) == b"unknown status"
@@ -175,12 +175,16 @@ def test_reparam_validation(ssn):
 def test_project_weights_validation(ssn):
     L = ssn.lib()
     f = L.ssn_project_weights
-    assert f(1, 64, 0, 8, None, None, None) == OK
-    assert f(1, 64, 10, 8, None, D, None) == ERR_NULL
-    assert f(1, 64, 10, 0, A, D, None) == ERR_SHAPE
-    assert f(1, 4096, 10, 2048, A, D, None) == ERR_UNSUPPORTED          # k > 1024
-    assert f(1, 64, 10, 8, A, A + 64, None) == ERR_ALIAS                # W overlaps U
-    assert f(1, 64, 10, 8, A + 1, D, None) == ERR_ALIGN
+    assert L.ssn_project_weights_workspace_bytes(4096, 14336, 64) == 0   # U^T W stays on chip
+    assert ssn.project_weights_workspace_bytes(5120, 18432, 51) == 0
+    assert f(1, 64, 0, 8, None, None, None, 0, None) == OK
+    assert f(1, 64, 10, 8, None, D, None, 0, None) == ERR_NULL
+    assert f(1, 64, 10, 0, A, D, None, 0, None) == ERR_SHAPE
+    assert f(1, 64, -1, 8, A, D, None, 0, None) == ERR_SHAPE
+    assert f(1, 4096, 10, 2048, A, D, None, 0, None) == ERR_UNSUPPORTED    # k > 1024
+    assert f(1, 64, 10, 8, A, A + 64, None, 0, None) == ERR_ALIAS          # W overlaps U
+    assert f(1, 64, 10, 8, A + 1, D, None, 0, None) == ERR_ALIGN
+    assert f(7, 64, 10, 8, A, D, None, 0, None) == ERR_DTYPE
     g = L.ssn_project_weights_batched
     n = (ctypes.c_int64 * 2)(16, 16)
     w = (ctypes.c_void_p * 2)(A, A + 64)                                  # overlapping matrices
@@ -232,19 +236,30 @@ def test_sparta_validation(ssn):
 
 
 def test_sparta_segments_tile_and_rotate(ssn):
-    """Host logic of the rotation: 20 contiguous segments tile [0, n) for any
-    n, sizes differ by at most one, and round r takes segment r mod 20."""
-    for n in (0, 1, 19, 20, 21, 1000, 320_000_003):
+    """Host logic of the rotation (ssn_sparta_segment) against the oracle's
+    schedule: 20 contiguous segments tile [0, n) for any n, sizes differ by
+    at most one, and round r takes segment r mod 20."""
+    from oracle import ssn_oracle as O
+    for n in (0, 1, 19, 20, 21, 1000, 320_000_003, (1 << 56) - 5):
         seen = 0
         sizes = []
         for r in range(ssn.SPARTA_SEGMENTS):
             first, m = ssn.sparta_segment(n, r)
+            assert (first, m) == O.sparta_segment(n, r, ssn.SPARTA_SEGMENTS)
             assert first == seen
             seen += m
             sizes.append(m)
             assert ssn.sparta_segment(n, r + 3 * ssn.SPARTA_SEGMENTS) == (first, m)
         assert seen == n
         assert max(sizes) - min(sizes) <= 1
+    for n, r, S in [(10, 3, 4), (999, 7, 7), (12345, 11, 1000)]:
+        assert ssn.sparta_segment(n, r, S) == O.sparta_segment(n, r, S)
+    L = ssn.lib()
+    f, m = ctypes.c_int64(), ctypes.c_int64()
+    assert L.ssn_sparta_segment(-1, 0, 20, ctypes.byref(f), ctypes.byref(m)) == ERR_SHAPE
+    assert L.ssn_sparta_segment(10, -1, 20, ctypes.byref(f), ctypes.byref(m)) == ERR_SHAPE
+    assert L.ssn_sparta_segment(10, 0, 0, ctypes.byref(f), ctypes.byref(m)) == ERR_SHAPE
+    assert L.ssn_sparta_segment(10, 0, 20, None, ctypes.byref(m)) == ERR_NULL
 
 
 def test_binding_refuses_cpu_tensors_and_missing_library(ssn, monkeypatch):

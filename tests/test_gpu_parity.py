@@ -10,7 +10,9 @@ import numpy as np
 import pytest
 import torch
 
-from helpers import DESIGN, TOL, rand_coords, rel, sample_rows, structured_inputs
+from helpers import (DESIGN, TOL, check_elementwise, mag_compress, mag_decompress, mag_project,
+                     mag_reparam_forward, mag_reparam_grad_factor, mag_reparam_grad_input,
+                     mag_weights, rand_coords, rel, sample_rows, structured_inputs)
 from oracle import ssn_oracle as O
 from paper_2607_13332_amd import inputs as I
 from paper_2607_13332_amd import ssn
@@ -28,9 +30,18 @@ def host(t):
     return I.to_host(t)
 
 
-def check(name, got, ref, dtype, kind):
+def check(name, got, ref, dtype, kind, mag=None):
+    """Relative Frobenius error against the parity bar and the design bound;
+    with `mag` = (M, L, split) also every element against its own bound
+    (helpers.elementwise_bound), so that one wrong element cannot hide in
+    the norm of a large output."""
     err = rel(got, ref)
-    print(f"[parity] {name}: rel={err:.3e}", flush=True)
+    q = None
+    if mag is not None:
+        M, L, split = mag
+        q = check_elementwise(name, got, ref, M, L, split, out_bf16=(kind == "bf16out"))
+    print(f"[parity] {name}: rel={err:.3e}" + ("" if q is None else f" max|err|/bound={q:.3f}"),
+          flush=True)
     assert err <= TOL[dtype], f"{name}: rel {err:.3e} above the parity bar {TOL[dtype]}"
     assert err <= DESIGN[(dtype, kind)], f"{name}: rel {err:.3e} above design bound"
     return err
@@ -50,17 +61,21 @@ def test_structured_config_all_ops(cfg):
     h = structured_inputs(cfg)
     X, ids, E, U, G = dev(h["X"], t), dev(h["ids"], t), dev(h["E"], t), dev(h["U"], t), dev(h["G"], t)
     Z = ssn.compress(X, ids, E, U)
-    check(f"{cfg.name} compress", host(Z), O.compress(h["X"], h["ids"], h["E"], h["U"]), t, "f32out")
+    check(f"{cfg.name} compress", host(Z), O.compress(h["X"], h["ids"], h["E"], h["U"]), t, "f32out",
+          mag_compress(h["X"], h["ids"], h["E"], h["U"]))
     # the structured activation gives back its coordinates up to noise/rounding
     assert rel(host(Z), h["Z0"]) < 0.05
     Zin = rand_coords(cfg.N, cfg.k, cfg.seed + 1)
     Y = ssn.decompress(dev(Zin, "f32"), ids, E, U)
     kind = "bf16out" if t == "bf16" else "f32out_dec"
-    check(f"{cfg.name} decompress", host(Y), O.decompress(Zin, h["ids"], h["E"], h["U"]), t, kind)
+    check(f"{cfg.name} decompress", host(Y), O.decompress(Zin, h["ids"], h["E"], h["U"]), t, kind,
+          mag_decompress(Zin, h["ids"], h["E"], h["U"]))
     GZ = ssn.project_grad(G, U)
-    check(f"{cfg.name} project_grad", host(GZ), O.project_grad(h["G"], h["U"]), t, "f32out")
+    check(f"{cfg.name} project_grad", host(GZ), O.project_grad(h["G"], h["U"]), t, "f32out",
+          mag_project(h["G"], h["U"]))
     GX = ssn.expand_grad(dev(Zin, "f32"), U)
-    check(f"{cfg.name} expand_grad", host(GX), O.expand_grad(Zin, h["U"]), t, kind)
+    check(f"{cfg.name} expand_grad", host(GX), O.expand_grad(Zin, h["U"]), t, kind,
+          mag_decompress(Zin, None, None, h["U"]))
     torch.cuda.synchronize()
 
 
@@ -110,36 +125,63 @@ def test_compress_projected_stage8b_sampled():
 
 
 # ---------------------------------------------------------------- full-size codec
-def _sampled_codec_check(cfg, nsample=384):
+def _codec_outputs(cfg):
     t = cfg.dtype
     print(f"[case] {cfg.name} N={cfg.N} d={cfg.d} k={cfg.k} V={cfg.V}", flush=True)
     inp = I.codec_inputs_device(cfg, DEV)
     X, ids, E, U, G = inp["X"], inp["ids"], inp["E"], inp["U"], inp["G"]
     Zin = I.coords_device(cfg.N, cfg.k, cfg.seed, DEV)
-    Z = ssn.compress(X, ids, E, U)
-    Y = ssn.decompress(Zin, ids, E, U)
-    GZ = ssn.project_grad(G, U)
-    GX = ssn.expand_grad(Zin, U)
+    out = {"Z": ssn.compress(X, ids, E, U), "Y": ssn.decompress(Zin, ids, E, U),
+           "GZ": ssn.project_grad(G, U), "GX": ssn.expand_grad(Zin, U)}
     torch.cuda.synchronize()
-    rows = sample_rows(cfg.N, nsample, cfg.seed)
-    r = torch.from_numpy(rows).to(DEV)
-    Xs, Gs, ids_s = host(X[r]), host(G[r]), host(ids[r])
-    Es = host(E.index_select(0, ids[r].long()))
-    Us, Zs = host(U), host(Zin[r])
-    loc = np.arange(len(rows), dtype=np.int32)
-    check(f"{cfg.name} compress", host(Z[r]), O.compress(Xs, loc, Es, Us), t, "f32out")
-    check(f"{cfg.name} decompress", host(Y[r]), O.decompress(Zs, loc, Es, Us), t, "bf16out")
-    check(f"{cfg.name} project_grad", host(GZ[r]), O.project_grad(Gs, Us), t, "f32out")
-    check(f"{cfg.name} expand_grad", host(GX[r]), O.expand_grad(Zs, Us), t, "bf16out")
     # every row was written (no NaN / untouched garbage anywhere)
-    assert torch.isfinite(Z).all() and torch.isfinite(Y.float()).all()
-    assert torch.isfinite(GZ).all() and torch.isfinite(GX.float()).all()
-    del inp, X, E, G, Z, Y, GZ, GX
+    for key in ("Z", "GZ"):
+        assert torch.isfinite(out[key]).all()
+    for key in ("Y", "GX"):
+        assert torch.isfinite(out[key].float()).all()
+    inp["Zin"] = Zin
+    return inp, out
+
+
+def _check_codec_rows(cfg, inp, out, rows, label):
+    """The four ops on the given rows against the oracle, with per-element
+    bounds; the embedding rows are gathered on the device by id."""
+    t = cfg.dtype
+    r = torch.from_numpy(rows).to(DEV)
+    ids = inp["ids"]
+    Xs, Gs = host(inp["X"][r]), host(inp["G"][r])
+    Es = host(inp["E"].index_select(0, ids[r].long()))
+    Us, Zs = host(inp["U"]), host(inp["Zin"][r])
+    loc = np.arange(len(rows), dtype=np.int32)
+    check(f"{cfg.name} compress{label}", host(out["Z"][r]), O.compress(Xs, loc, Es, Us), t, "f32out",
+          mag_compress(Xs, loc, Es, Us))
+    check(f"{cfg.name} decompress{label}", host(out["Y"][r]), O.decompress(Zs, loc, Es, Us), t, "bf16out",
+          mag_decompress(Zs, loc, Es, Us))
+    check(f"{cfg.name} project_grad{label}", host(out["GZ"][r]), O.project_grad(Gs, Us), t, "f32out",
+          mag_project(Gs, Us))
+    check(f"{cfg.name} expand_grad{label}", host(out["GX"][r]), O.expand_grad(Zs, Us), t, "bf16out",
+          mag_decompress(Zs, None, None, Us))
+
+
+def _sampled_codec_check(cfg, nsample=384):
+    inp, out = _codec_outputs(cfg)
+    _check_codec_rows(cfg, inp, out, sample_rows(cfg.N, nsample, cfg.seed), " (sampled rows)")
+    del inp, out
     torch.cuda.empty_cache()
 
 
-def test_stage8b_full_size_sampled():
-    _sampled_codec_check(I.STAGE8B)
+@pytest.mark.timeout(600)
+def test_stage8b_full_size_all_rows():
+    """The 8B-stage workload at full size, every one of the 32768 rows of
+    every op against the oracle, in blocks of 4096 rows (the oracle's own
+    row block), each element within its own bound."""
+    cfg = I.STAGE8B
+    inp, out = _codec_outputs(cfg)
+    for r0 in range(0, cfg.N, O.ROW_BLOCK):
+        rows = np.arange(r0, min(cfg.N, r0 + O.ROW_BLOCK), dtype=np.int64)
+        _check_codec_rows(cfg, inp, out, rows, f" rows {r0}..{rows[-1]}")
+    del inp, out
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("cfg", I.sweep_configs(), ids=lambda c: c.name)
@@ -147,7 +189,7 @@ def test_sweep_full_size_sampled(cfg):
     _sampled_codec_check(cfg, nsample=256)
 
 
-@pytest.mark.parametrize("cfg", [c for c in I.paper_configs() if c.B in (1, 3)], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", I.paper_configs(), ids=lambda c: c.name)
 def test_paper_shapes_full_size_sampled(cfg):
     _sampled_codec_check(cfg, nsample=256)
 
@@ -173,7 +215,8 @@ def test_weight_reprojection_stage_sampled(wc):
     Uh = host(U)
     for b, W in enumerate(Ws):
         got = host(W[:, torch.from_numpy(cols[b]).to(DEV)])
-        check(f"{wc.name} matrix {b} {tuple(W.shape)}", got, O.project_weights(before[b], Uh), "bf16", "bf16out")
+        check(f"{wc.name} matrix {b} {tuple(W.shape)}", got, O.project_weights(before[b], Uh), "bf16", "bf16out",
+              mag_weights(before[b], Uh))
     # one launch for the batch gives the same bits as one launch per matrix
     for b in range(2):
         assert torch.equal(Ws[b], ref_single[b])
@@ -223,16 +266,21 @@ def test_codec_shapes(N, d, k, dtype):
     Zin = rand_coords(N, k, seed)
     X, E, U, ids = dev(Xh, dtype), dev(Eh, dtype), dev(Uh, dtype), dev(ids_h, dtype)
     outkind = "bf16out" if dtype == "bf16" else "f32out_dec"
-    check("compress", host(ssn.compress(X, ids, E, U)), O.compress(Xh, ids_h, Eh, Uh), dtype, "f32out")
+    mc = mag_compress(Xh, ids_h, Eh, Uh)
+    check("compress", host(ssn.compress(X, ids, E, U)), O.compress(Xh, ids_h, Eh, Uh), dtype, "f32out", mc)
     P = ssn.project_table(E, U)
+    # the table's rows carry their own accumulation (of length d): the bound
+    # of compress with that term counted once more
     check("compress_projected", host(ssn.compress_projected(X, ids, P, U)),
-          O.compress(Xh, ids_h, Eh, Uh), dtype, "f32out")
+          O.compress(Xh, ids_h, Eh, Uh), dtype, "f32out", (mc[0], 2 * d, False))
     Ze = ssn.compress_projected(E[ids.long()].contiguous(), ids, P, U)
     assert Ze.abs().max().item() <= 1e-5 * P.abs().max().item()
-    check("project_grad", host(ssn.project_grad(X, U)), O.project_grad(Xh, Uh), dtype, "f32out")
+    check("project_grad", host(ssn.project_grad(X, U)), O.project_grad(Xh, Uh), dtype, "f32out",
+          mag_project(Xh, Uh))
     check("decompress", host(ssn.decompress(dev(Zin, "f32"), ids, E, U)),
-          O.decompress(Zin, ids_h, Eh, Uh), dtype, outkind)
-    check("expand_grad", host(ssn.expand_grad(dev(Zin, "f32"), U)), O.expand_grad(Zin, Uh), dtype, outkind)
+          O.decompress(Zin, ids_h, Eh, Uh), dtype, outkind, mag_decompress(Zin, ids_h, Eh, Uh))
+    check("expand_grad", host(ssn.expand_grad(dev(Zin, "f32"), U)), O.expand_grad(Zin, Uh), dtype, outkind,
+          mag_decompress(Zin, None, None, Uh))
 
 
 BF16_WIRE_SHAPES = [  # (N, d, k): every kernel family with bf16 coordinates
@@ -374,7 +422,7 @@ def test_weight_shapes(d, n, k, dtype):
     W = dev(Wh, dtype)
     ssn.project_weights(W, dev(Uh, dtype))
     check("project_weights", host(W), O.project_weights(Wh, Uh), dtype,
-          "bf16out" if dtype == "bf16" else "f32out")
+          "bf16out" if dtype == "bf16" else "f32out", mag_weights(Wh, Uh))
 
 
 BATCHES = [  # (d, k, [n...]): several matrices per launch; 16-column tiles that
@@ -408,7 +456,8 @@ def test_weight_batches(d, k, ns):
     for b, (W, Wh) in enumerate(zip(Ws, Whs)):
         cols = sample_rows(Wh.shape[1], 512, b)
         got = host(W)[:, cols]
-        check(f"batched matrix {b} n={Wh.shape[1]}", got, O.project_weights(Wh[:, cols], Uh), "bf16", "bf16out")
+        check(f"batched matrix {b} n={Wh.shape[1]}", got, O.project_weights(Wh[:, cols], Uh), "bf16", "bf16out",
+              mag_weights(Wh[:, cols], Uh))
         # the column partition differs between the two launches; the bits do not
         assert torch.equal(W, singles[b])
 
@@ -445,12 +494,15 @@ def test_reparam_shapes(N, din, d, k, dtype):
     H, Zp, U, G = dev(Hh, dtype), dev(Zh, dtype), dev(Uh, dtype), dev(Gh, dtype)
     outk = "bf16out" if dtype == "bf16" else "f32out_dec"
     T, Y = ssn.reparam_forward(H, Zp, U)
-    check("T = H Zp", host(T), O.project_grad(Hh, Zh), dtype, "f32out")
-    check("Y = (H Zp) U^T", host(Y), O.reparam_forward(Hh, Zh, Uh), dtype, outk)
+    check("T = H Zp", host(T), O.project_grad(Hh, Zh), dtype, "f32out", mag_project(Hh, Zh))
+    check("Y = (H Zp) U^T", host(Y), O.reparam_forward(Hh, Zh, Uh), dtype, outk,
+          mag_reparam_forward(Hh, Zh, Uh))
     GT, GH, GZ = ssn.reparam_backward(H, Zp, U, G)
-    check("GT = G U", host(GT), O.project_grad(Gh, Uh), dtype, "f32out")
-    check("dL/dH", host(GH), O.reparam_grad_input(Gh, Zh, Uh), dtype, outk)
-    check("dL/dZp", host(GZ), O.reparam_grad_factor(Hh, Gh, Uh), dtype, "f32out")
+    check("GT = G U", host(GT), O.project_grad(Gh, Uh), dtype, "f32out", mag_project(Gh, Uh))
+    check("dL/dH", host(GH), O.reparam_grad_input(Gh, Zh, Uh), dtype, outk,
+          mag_reparam_grad_input(Gh, Zh, Uh))
+    check("dL/dZp", host(GZ), O.reparam_grad_factor(Hh, Gh, Uh), dtype, "f32out",
+          mag_reparam_grad_factor(Hh, Gh, Uh))
     # the split reduction is deterministic
     _, _, GZ2 = ssn.reparam_backward(H, Zp, U, G)
     assert torch.equal(GZ, GZ2)
@@ -510,11 +562,14 @@ def test_reparam_paper_shape_sampled(N, din, d, k):
     rows = torch.from_numpy(sample_rows(N, 128, 1)).to(DEV)
     cols = torch.from_numpy(sample_rows(din, 128, 2)).to(DEV)
     Hs, Gs, Zh, Uh = host(H[rows]), host(G[rows]), host(Zp), host(U)
-    check("paper Y", host(Y[rows]), O.reparam_forward(Hs, Zh, Uh), "bf16", "bf16out")
-    check("paper dL/dH", host(GH[rows]), O.reparam_grad_input(Gs, Zh, Uh), "bf16", "bf16out")
+    check("paper Y", host(Y[rows]), O.reparam_forward(Hs, Zh, Uh), "bf16", "bf16out",
+          mag_reparam_forward(Hs, Zh, Uh))
+    check("paper dL/dH", host(GH[rows]), O.reparam_grad_input(Gs, Zh, Uh), "bf16", "bf16out",
+          mag_reparam_grad_input(Gs, Zh, Uh))
     # factor gradient rows need every token: the oracle takes H's sampled columns
-    check("paper dL/dZp", host(GZ[cols]), O.reparam_grad_factor(host(H[:, cols].contiguous()), host(G), Uh),
-          "bf16", "f32out")
+    Hc, Gall = host(H[:, cols].contiguous()), host(G)
+    check("paper dL/dZp", host(GZ[cols]), O.reparam_grad_factor(Hc, Gall, Uh), "bf16", "f32out",
+          mag_reparam_grad_factor(Hc, Gall, Uh))
     del H, G, T, Y, GT, GH, GZ
     torch.cuda.empty_cache()
 

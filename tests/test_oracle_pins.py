@@ -324,3 +324,81 @@ def test_sparta_weighted_average_and_segments():
     cover = np.concatenate([O.sparta_indices(n, n // segs, first=j * (n // segs)) for j in range(segs)])
     assert np.array_equal(np.sort(cover), np.arange(n))
 
+
+
+def test_sparta_segment_schedule_by_hand():
+    """Segments of n = 10 in S = 4 by hand: [0,2) [2,5) [5,7) [7,10); the
+    schedule repeats every S rounds; for any n the segments tile [0, n)
+    in order with sizes that differ by at most one."""
+    assert [O.sparta_segment(10, r, 4) for r in range(4)] == [(0, 2), (2, 3), (5, 2), (7, 3)]
+    assert O.sparta_segment(10, 5, 4) == O.sparta_segment(10, 1, 4)
+    for n, S in [(1000, 20), (7, 20), (0, 3), (320_000_003, 20)]:
+        segs = [O.sparta_segment(n, r, S) for r in range(S)]
+        ends = [f + m for f, m in segs]
+        assert segs[0][0] == 0 and ends[-1] == n
+        assert all(segs[j + 1][0] == ends[j] for j in range(S - 1))
+        sizes = [m for _, m in segs]
+        assert max(sizes) - min(sizes) <= 1
+    with pytest.raises(ValueError):
+        O.sparta_segment(10, -1, 4)
+
+
+# ---------------------------------------------------------------- parity metric
+def test_rel_frobenius_by_hand():
+    """The parity metric on values worked by hand: ||got - ref|| / ||ref||
+    with ref = diag(3, 4) (norm 5), the argument order matters, bf16 bit
+    patterns are widened before the difference, and a zero reference takes
+    the absolute bar ||got|| / ||inputs|| (exactly 0 or inf without one)."""
+    ref = np.array([[3.0, 0.0], [0.0, 4.0]])
+    got = np.array([[3.0, 1.0], [0.0, 4.0]])
+    assert O.rel_frobenius(got, ref) == pytest.approx(1.0 / 5.0, rel=1e-15)
+    # swapped: the difference has norm 1 and the new reference sqrt(26)
+    assert O.rel_frobenius(ref, got) == pytest.approx(1.0 / np.sqrt(26.0), rel=1e-15)
+    # a 3-4-5 error: ||(0.3, 0.4)|| = 0.5 against ||(6, 8)|| = 10
+    assert O.rel_frobenius(np.array([6.3, 8.4]), np.array([6.0, 8.0])) == pytest.approx(0.05, rel=1e-13)
+    # bf16 0x3F80 is 1.0; against 1 + 2^-7 the error is 2^-7 / (1 + 2^-7)
+    b = np.array([0x3F80], dtype=np.uint16)
+    assert O.rel_frobenius(b, np.array([1.0 + 2 ** -7])) == pytest.approx(2 ** -7 / (1 + 2 ** -7), rel=1e-15)
+    assert O.rel_frobenius(b, np.array([1.0])) == 0.0
+    # zero reference: ||(3, 4)|| = 5 against inputs of norm 50 -> 0.1
+    z = np.zeros(2)
+    assert O.rel_frobenius(np.array([3.0, 4.0]), z, scale=50.0) == pytest.approx(0.1, rel=1e-15)
+    assert O.rel_frobenius(np.zeros(2), z) == 0.0
+    assert O.rel_frobenius(np.array([0.0, 1e-30]), z) == float("inf")
+    with pytest.raises(ValueError):
+        O.rel_frobenius(np.zeros(3), np.zeros(2))
+
+
+# ---------------------------------------------------------------- bandwidth estimate
+def _body_stage_trainable_params(m, rank):
+    """Trainable parameters of one body stage of the reparameterized model
+    (section 5.2 model card; section 4.1: the attention and MLP output
+    projections are trained as factors of din x k, every other projection is
+    full): per layer Wq d x (heads * hd), Wk and Wv d x (kv * hd), the output
+    factor (heads * hd) x k, gate and up d x ffn, the down factor ffn x k.
+    Normalisation scales (a few thousand values) are left out."""
+    d, hd = m["d"], m["head_dim"]
+    ffn = int(np.ceil(m["ffn_multiplier"] * (8 * d / 3) / m["ffn_round"]) * m["ffn_round"])
+    attn = d * m["heads"] * hd + 2 * d * m["kv_heads"] * hd + m["heads"] * hd * rank
+    mlp = 2 * d * ffn + ffn * rank
+    return m["body_layers"] * (attn + mlp)
+
+
+def test_bandwidth_floor_matches_the_paper():
+    """Section 3.5.2: about 113 Mbit/s (BF16 all-reduce) and 186 Mbit/s (FP32)
+    per contributor, from a_f = a_b = 3, FP32 activations of 4096 tokens at
+    the compressed width d / 100 = 51.2, and 5 % of a body stage's trainable
+    parameters every 10 s.  Both figures are reproduced to 1 Mbit/s."""
+    with open(os.path.join(GOLDEN, "paper_figures.json")) as f:
+        fig = json.load(f)
+    m, bw, c8 = fig["model_8b"], fig["bandwidth_floor"], fig["compression_8b"]
+    params = _body_stage_trainable_params(m, fig["rank_8b"]["rank"])
+    assert 900e6 < params < 915e6          # 4 x 226.6M
+    payload = m["sparse_share"] * params
+    for bits, want in ((16, bw["mbit_per_s_bf16"]), (32, bw["mbit_per_s_fp32"])):
+        got = O.bandwidth_floor_bits_per_s(bw["a_f"], bw["a_b"], m["seq_len"], c8["wire_width"],
+                                           bits, payload, bw["ar_time_s"]) / 1e6
+        assert abs(got - want) <= 1.0, (bits, got, want)
+    # the activation share alone: 32 x 6 x 4096 x 51.2 bits/s = 40.3 Mbit/s
+    act = O.bandwidth_floor_bits_per_s(3, 3, 4096, 51.2, 16, 0.0, 10.0)
+    assert act == pytest.approx(40_265_318.4, rel=1e-12)
