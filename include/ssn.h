@@ -296,6 +296,31 @@ ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int
                                   size_t workspace_bytes, void *stream);
 
 /*
+ * ssn_reparam_backward_noalloc -- ssn_reparam_backward for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): the same kernels and results, with
+ * the factor gradient's partial sums in the library's own scratch array of
+ * SSN_NOALLOC_SCRATCH_BYTES per device instead of a caller workspace.  The
+ * caller still passes every input and output.  Arguments and errors are those
+ * of ssn_reparam_backward; a shape whose ssn_reparam_workspace_bytes exceeds
+ * SSN_NOALLOC_SCRATCH_BYTES is SSN_ERR_UNSUPPORTED; none is: the token
+ * splits times din never exceed 256 column blocks of 512 (k <= 64) or 256
+ * (64 < k <= 128), so the partial sums take at most 32 MiB, and k > 128
+ * needs no workspace.  Allocates nothing: the array is part of the library's device
+ * code, held by every GPU the library runs on until the process ends; its
+ * address is looked up on the first call on each device.  All calls on one
+ * GPU share that GPU's array, so calls that overlap in time on one GPU (on
+ * different streams, or from several host threads) race and must be ordered
+ * by the caller; each call writes every scratch value it reads, so nothing
+ * carries over from the previous call.
+ */
+#define SSN_NOALLOC_SCRATCH_BYTES (32u << 20)
+ssn_status_t ssn_reparam_backward_noalloc(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d,
+                                          int64_t k, const void *H, const void *Zp,
+                                          const void *U, const void *G, float *GT, void *GH,
+                                          float *GZp, void *stream);
+
+/*
  * ssn_factored_embedding -- the trainable embedding factored through the
  * basis, T_S = E U^T (section 4.1), looked up by token id:
  *   X0[i, :] = E[ids[i], :] . U^T

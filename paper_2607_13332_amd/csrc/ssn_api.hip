@@ -8,6 +8,7 @@
 #include <stdint.h>
 
 #include "ssn_launch.h"
+#include "ssn_checks.h"
 
 namespace {
 
@@ -243,16 +244,21 @@ size_t ssn_reparam_workspace_bytes(ssn_dtype_t dtype, int64_t N, int64_t din, in
   return ssn::factor_grad_workspace_bytes(dtype, N, din, k);
 }
 
-ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,
-                                  const void* H, const void* Zp, const void* U, const void* G,
-                                  float* GT, void* GH, float* GZp, void* workspace,
-                                  size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+// Arguments of ssn_reparam_backward; with check_ws false the workspace is the
+// caller's business (the library's own scratch) and is not examined.
+ssn_status_t ssn::reparam_backward_args(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d,
+                                        int64_t k, const void* H, const void* Zp, const void* U,
+                                        const void* G, const float* GT, const void* GH,
+                                        const float* GZp, const void* workspace,
+                                        size_t workspace_bytes, bool check_ws) {
   const ssn_status_t sh = reparam_shape(dtype, N, din, d, k);
   if (sh != SSN_OK) return sh;
   if (!GZp) return SSN_ERR_NULL;
   const int64_t s = elem_size(dtype);
   if (!aligned_to(GZp, 4)) return SSN_ERR_ALIGN;
-  const size_t need = ssn::factor_grad_workspace_bytes(dtype, N, din, k);
+  const size_t need = check_ws ? ssn::factor_grad_workspace_bytes(dtype, N, din, k) : 0;
   if (N > 0) {
     if (!H || !Zp || !U || !G || !GT || !GH) return SSN_ERR_NULL;
     if (!aligned_to(H, s) || !aligned_to(Zp, s) || !aligned_to(U, s) || !aligned_to(G, s) ||
@@ -271,6 +277,19 @@ ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int
         if (overlap(outs[a], outs[b])) return SSN_ERR_ALIAS;
     }
   }
+  return SSN_OK;
+}
+
+extern "C" {
+
+ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int64_t d, int64_t k,
+                                  const void* H, const void* Zp, const void* U, const void* G,
+                                  float* GT, void* GH, float* GZp, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  const ssn_status_t chk = ssn::reparam_backward_args(dtype, N, din, d, k, H, Zp, U, G, GT, GH, GZp,
+                                                      workspace, workspace_bytes, true);
+  if (chk != SSN_OK) return chk;
+  const int64_t s = elem_size(dtype);
   hipStream_t st = (hipStream_t)stream;
   if (N == 0)   // no tokens: the factor-gradient kernel writes zeros (no memset, capture-safe)
     return launch_status(ssn::launch_factor_grad(dtype, 0, din, k, H, GT, GZp, (float*)workspace, st));

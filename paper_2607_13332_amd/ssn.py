@@ -20,6 +20,7 @@ SSN_F32, SSN_BF16 = 0, 1
 OPS = {"compress": 0, "decompress": 1, "project_grad": 2, "project_weights": 3,
        "compress_projected": 4}
 MAX_BATCH = 16
+NOALLOC_SCRATCH_BYTES = 32 << 20
 SPARTA_MAX_SENDERS = 64
 
 _c_i64 = ctypes.c_int64
@@ -73,6 +74,9 @@ def _declare(lib):
     lib.ssn_reparam_backward.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
                                          _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
                                          ctypes.c_size_t, _c_p]
+    lib.ssn_reparam_backward_noalloc.restype = ctypes.c_int
+    lib.ssn_reparam_backward_noalloc.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
+                                                 _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_factored_embedding.restype = ctypes.c_int
     lib.ssn_factored_embedding.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64,
                                            _c_p, _c_p, _c_p, _c_p, _c_p]
@@ -332,6 +336,26 @@ def reparam_backward(H: torch.Tensor, Zp: torch.Tensor, U: torch.Tensor, G: torc
         _dev(G, "G", t, 2), _dev(GT, "GT", torch.float32, 2), _dev(GH, "GH", t, 2),
         _dev(GZp, "GZp", torch.float32, 2), _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+    return GT, GH, GZp
+
+
+def reparam_backward_noalloc(H: torch.Tensor, Zp: torch.Tensor, U: torch.Tensor, G: torch.Tensor,
+                             GT: torch.Tensor, GH: torch.Tensor, GZp: torch.Tensor, stream=None):
+    """reparam_backward with the library's own scratch memory: the caller
+    passes every output, and the call allocates nothing on the device."""
+    N, din = H.shape
+    d, k = U.shape
+    if Zp.shape != (din, k) or G.shape != (N, d) or GT.shape != (N, k) or GH.shape != (N, din) \
+            or GZp.shape != (din, k):
+        raise ValueError(f"shape mismatch H{tuple(H.shape)} Zp{tuple(Zp.shape)} U{tuple(U.shape)} "
+                         f"G{tuple(G.shape)} GT{tuple(GT.shape)} GH{tuple(GH.shape)} "
+                         f"GZp{tuple(GZp.shape)}")
+    t = H.dtype
+    _same_device(H, Zp, U, G, GT, GH, GZp)
+    _check("ssn_reparam_backward_noalloc", lib().ssn_reparam_backward_noalloc(
+        _dt_code(t), N, din, d, k, _dev(H, "H", t, 2), _dev(Zp, "Zp", t, 2), _dev(U, "U", t, 2),
+        _dev(G, "G", t, 2), _dev(GT, "GT", torch.float32, 2), _dev(GH, "GH", t, 2),
+        _dev(GZp, "GZp", torch.float32, 2), _stream(stream)))
     return GT, GH, GZp
 
 
