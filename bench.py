@@ -380,7 +380,11 @@ def time_step_graph(sets, step_fn, steps: int, warmup: int) -> float:
 
 def time_codec_config(cfg, steps: int, warmup: int, dev):
     """The four codec ops of one microbatch on a workload other than the
-    headline one (two alternating input sets, HIP events per op)."""
+    headline one (two alternating input sets).  The step is timed with no
+    event inside it; a second pass with HIP events around each op gives the
+    per-op times.  For k % 16 != 0 the basis is the zero-padded copy made
+    once by ssn_pad_basis (the library's layout for such ranks); the same
+    step on the unpadded basis is reported beside it."""
     import numpy as np
     import torch
     from paper_2607_13332_amd import inputs as I
@@ -405,8 +409,7 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         sets.append(inp)
     ops = ["decompress", "project_grad", "compress", "expand_grad"]
 
-    def step(s, evs, Ub=None):
-        Ub = U if Ub is None else Ub
+    def step(s, Ub, evs=None):
         if evs:
             evs[0].record()
         ssn.decompress(s["Zin"], s["ids"], E, Ub, out=s["Y"])
@@ -422,55 +425,60 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         if evs:
             evs[4].record()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
-    for i in range(warmup):
-        step(sets[i % 2], evs[0])
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(steps):
-        step(sets[i % 2], evs[i])
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / steps
+    def measure(Ub):
+        """(ms per step, per-op mean ms) on basis Ub."""
+        for i in range(warmup):
+            step(sets[i % 2], Ub)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            step(sets[i % 2], Ub)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+        for i in range(steps):
+            step(sets[i % 2], Ub, evs[i])
+        torch.cuda.synchronize()
+        op_ms = {op: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, op in enumerate(ops)}
+        return ms, op_ms
+
+    Ub, ldu, pad_ms = U, k, None
+    if k % 16 != 0:
+        ldu = 16 * ((k + 15) // 16)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        Ub = ssn.pad_basis(U, ldu)
+        e1.record()
+        torch.cuda.synchronize()
+        pad_ms = e0.elapsed_time(e1)
+    ms, op_ms = measure(Ub)
     per_op = {}
     step_bytes = 0
-    for j, op in enumerate(ops):
-        t = float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs]))
+    for op in ops:
+        t = op_ms[op]
         byts = float(np.mean([algorithmic_bytes(op, N, d, k, op_u(op, s)) for s in sets]))
         step_bytes += byts
         per_op[op] = {"ms": round(t, 5), "algorithmic_GBps": round(byts / (t * 1e-3) / 1e9, 1),
                       "frac_hbm_peak": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-    gms = time_step_graph(sets, lambda s: step(s, None), steps, warmup)
+    gms = time_step_graph(sets, lambda s: step(s, Ub), steps, warmup)
+    basis = f"U [{d}, {k}] stored zero-padded to {ldu} columns (ssn_pad_basis, once per basis)" \
+        if ldu != k else f"U [{d}, {k}]"
     out = {"workload": f"N={N} (B={cfg.B} x S={cfg.S}), d={d}, k={k}, V={cfg.V}, bf16, "
                        f"{cfg.ids_dist} ids",
+           "basis": basis,
            "ms_per_step": round(ms, 5), "tokens_per_s": round(N / (ms * 1e-3), 1),
            "step_frac_hbm_peak": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "ms_per_step_hip_graph": round(gms, 5),
            "tokens_per_s_hip_graph": round(N / (gms * 1e-3), 1),
            "per_op": per_op}
-    if k % 16 != 0:
-        # the same step with U zero-padded to whole 16-column tiles (a copy
-        # made once per basis), so that every kernel reads aligned U rows
-        ldu = 16 * ((k + 15) // 16)
-        Up = torch.zeros((d, ldu), dtype=U.dtype, device=dev)
-        Up[:, :k] = U
-        for i in range(warmup):
-            step(sets[i % 2], evs[0], Up)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(steps):
-            step(sets[i % 2], evs[i], Up)
-        torch.cuda.synchronize()
-        pms = (time.perf_counter() - t0) * 1e3 / steps
-        pgms = time_step_graph(sets, lambda s: step(s, None, Up), steps, warmup)
-        out["padded_basis"] = {
-            "what": f"U stored zero-padded to {ldu} columns (Z keeps k={k})",
-            "ms_per_step": round(pms, 5), "tokens_per_s": round(N / (pms * 1e-3), 1),
-            "ms_per_step_hip_graph": round(pgms, 5),
-            "tokens_per_s_hip_graph": round(N / (pgms * 1e-3), 1),
-            "per_op_ms": {op: round(float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])), 5)
-                          for j, op in enumerate(ops)}}
-        del Up
-    del sets, base, U, E
+    if pad_ms is not None:
+        out["pad_basis_ms"] = round(pad_ms, 5)
+        ums, uop = measure(U)
+        out["unpadded_basis"] = {
+            "what": f"the same step on U [{d}, {k}] as stored (k % 16 != 0: odd-width U rows)",
+            "ms_per_step": round(ums, 5), "tokens_per_s": round(N / (ums * 1e-3), 1),
+            "per_op_ms": {op: round(v, 5) for op, v in uop.items()}}
+    del sets, base, U, E, Ub
     torch.cuda.empty_cache()
     return out
 
@@ -602,16 +610,6 @@ def main():
         step(sets[i % 2])
     torch.cuda.synchronize()
 
-    # ---------------- timed region ----------------
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(sets[i % 2], events[i])
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-
     def op_stats(evs, names):
         out = {}
         for j, op in enumerate(names):
@@ -628,7 +626,42 @@ def main():
                 "frac_hbm_peak": round(byts / (mean_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                 "bytes_per_launch": int(byts)}
 
+    # per-op breakdown: a pass with HIP events around every op (events
+    # between kernels cost the step time, so this pass is not the timed one)
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(sets[i % 2], events[i])
+    torch.cuda.synchronize()
     stats = op_stats(events, ops)
+    dom = max(ops, key=lambda o: stats[o][0])
+
+    # ---------------- timed region ----------------
+    # the step as a caller runs it; the only events are the pair around the
+    # dominant kernel, on the stream it is launched on, for the roofline
+    dom_j = ops.index(dom)
+    dev_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+
+    def timed_step(s, ev):
+        for j, fn in enumerate((lambda: ssn.decompress(s["Zin"], s["ids"], E, U, out=s["Y"]),
+                                lambda: ssn.project_grad(s["G"], U, out=s["GZ"]),
+                                lambda: ssn.compress(s["X"], s["ids_c"], E, U, out=s["Z"]),
+                                lambda: ssn.expand_grad(s["GZin"], U, out=s["GX"]))):
+            if j == dom_j:
+                ev[0].record()
+                fn()
+                ev[1].record()
+            else:
+                fn()
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        timed_step(sets[i % 2], dev_ev[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    dom_ts = np.array([e[0].elapsed_time(e[1]) for e in dev_ev])
+
     per_op = {op: per_op_entry(op, *stats[op]) for op in ops}
     # HBM bytes measured by the rocprofv3 counters (when taken on these
     # sources) over the same mean durations
@@ -638,9 +671,9 @@ def main():
             gbs = measured[op] / (stats[op][0] * 1e-3) / 1e9
             per_op[op]["measured_traffic_GBps"] = round(gbs, 1)
             per_op[op]["measured_frac_hbm_peak"] = round(gbs / HBM_PEAK_GBS, 4)
-    per_op_ms = {op: stats[op][0] for op in ops}
-    dom = max(ops, key=lambda o: per_op_ms[o])
-    achieved = per_op[dom]["algorithmic_GBps"]
+    # the roofline's duration: the dominant kernel inside the timed region
+    dom_entry = per_op_entry(dom, float(dom_ts.mean()), np.percentile(dom_ts, [10, 50, 90]))
+    achieved = dom_entry["algorithmic_GBps"]
     traffic = load_traffic(dom)
     step_bytes = sum(per_op[o]["bytes_per_launch"] for o in ops)
 
@@ -664,7 +697,9 @@ def main():
         "per_op": per_op,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic},
+                     "traffic": traffic, "ms": dom_entry["ms"],
+                     "ms_p10_p50_p90": dom_entry["ms_p10_p50_p90"],
+                     "bytes_per_launch": dom_entry["bytes_per_launch"]},
         "kernel_source_hash": kernel_source_hash(),
     }
     # (not in the counter runs: their copy of known size is the calibration)
@@ -674,6 +709,27 @@ def main():
             "what": "torch device copy of 512 MiB on the same GPU, bytes read + written per second",
             "GBps": round(cp_rate, 1), "frac_hbm_peak": round(cp_rate / HBM_PEAK_GBS, 4),
             "dominant_kernel_frac_of_copy": round(achieved / cp_rate, 4)}
+
+    def time_variant(fn):
+        """ms per step with no event inside the step, then per-op stats from
+        a pass with events around every op."""
+        for i in range(args.warmup):
+            fn(sets[i % 2], None)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            fn(sets[i % 2], None)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            fn(sets[i % 2], evs[i])
+        torch.cuda.synchronize()
+        return ms, evs
+
+    def rec(evs, j):
+        if evs is not None:
+            evs[j].record()
 
     # ---------------- variant: compress against the projected table ----------------
     tev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -685,25 +741,17 @@ def main():
     ops2 = ["decompress", "project_grad", "compress_projected", "expand_grad"]
 
     def step2(s, evs):
-        evs[0].record()
+        rec(evs, 0)
         ssn.decompress(s["Zin"], s["ids"], E, U, out=s["Y"])
-        evs[1].record()
+        rec(evs, 1)
         ssn.project_grad(s["G"], U, out=s["GZ"])
-        evs[2].record()
+        rec(evs, 2)
         ssn.compress_projected(s["X"], s["ids_c"], P, U, out=s["Z"])
-        evs[3].record()
+        rec(evs, 3)
         ssn.expand_grad(s["GZin"], U, out=s["GX"])
-        evs[4].record()
+        rec(evs, 4)
 
-    ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    for i in range(args.warmup):
-        step2(sets[i % 2], ev2[0])
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step2(sets[i % 2], ev2[i])
-    torch.cuda.synchronize()
-    ms2 = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms2, ev2 = time_variant(step2)
     st2 = op_stats(ev2, ops2)
     cp = per_op_entry("compress_projected", *st2["compress_projected"])
     cp["traffic"] = load_traffic("compress_projected")
@@ -723,25 +771,17 @@ def main():
         s_["GZ_b"] = torch.empty((N, k), dtype=torch.bfloat16, device=dev)
 
     def step3(s, evs):
-        evs[0].record()
+        rec(evs, 0)
         ssn.decompress(s["Zin_b"], s["ids"], E, U, out=s["Y"])
-        evs[1].record()
+        rec(evs, 1)
         ssn.project_grad(s["G"], U, out=s["GZ_b"], z_dtype=torch.bfloat16)
-        evs[2].record()
+        rec(evs, 2)
         ssn.compress(s["X"], s["ids_c"], E, U, out=s["Z_b"], z_dtype=torch.bfloat16)
-        evs[3].record()
+        rec(evs, 3)
         ssn.expand_grad(s["GZin_b"], U, out=s["GX"])
-        evs[4].record()
+        rec(evs, 4)
 
-    ev3 = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    for i in range(args.warmup):
-        step3(sets[i % 2], ev3[0])
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step3(sets[i % 2], ev3[i])
-    torch.cuda.synchronize()
-    ms3 = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms3, ev3 = time_variant(step3)
     st3 = op_stats(ev3, ops)
     result["variants"]["step_bf16_coordinates"] = {
         "what": "the same four ops with Z and G_Z in bf16 (half the wire message)",

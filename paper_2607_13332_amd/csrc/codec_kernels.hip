@@ -1081,6 +1081,32 @@ __global__ __launch_bounds__(256) void sum_partials(const float* __restrict__ ws
   }
 }
 
+// Up[i, c] = U[i, c] for c < k, 0 for k <= c < ldu: the basis with zero
+// columns appended, element by element (a once-per-basis copy).
+template <typename T>
+__global__ __launch_bounds__(256) void pad_basis(const T* __restrict__ U, T* __restrict__ Up,
+                                                 int64_t d, int64_t k, int64_t ldu) {
+  const int64_t n = d * ldu;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / ldu, c = i - r * ldu;
+    Up[i] = c < k ? U[r * k + c] : T(0);
+  }
+}
+
+hipError_t launch_pad_basis(int dtype, int64_t d, int64_t k, int64_t ldu, const void* U, void* Up,
+                            hipStream_t st) {
+  const int64_t n = d * ldu;
+  const unsigned blocks = (unsigned)((n + 255) / 256 < 16384 ? (n + 255) / 256 : 16384);
+  if (dtype == kF32)
+    hipLaunchKernelGGL((pad_basis<float>), dim3(blocks), dim3(256), 0, st, (const float*)U,
+                       (float*)Up, d, k, ldu);
+  else
+    hipLaunchKernelGGL((pad_basis<uint16_t>), dim3(blocks), dim3(256), 0, st, (const uint16_t*)U,
+                       (uint16_t*)Up, d, k, ldu);
+  return hipGetLastError();
+}
+
 template <typename T, bool HAS_E, bool HAS_P>
 static hipError_t launch_compress_generic(int64_t N, int64_t d, int64_t k, int64_t V, const void* X,
                                           const int32_t* ids, const void* E, const void* U,

@@ -190,6 +190,17 @@ ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k
   return ssn_project_grad_ex(dtype, SSN_F32, N, d, k, G, U, k, GZ, stream);
 }
 
+ssn_status_t ssn_pad_basis(ssn_dtype_t dtype, int64_t d, int64_t k, int64_t ldu, const void* U,
+                           void* Up, void* stream) {
+  if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;
+  if (d < 1 || k < 1 || k > d || !ldu_ok(k, ldu) || !mul_ok(d, ldu)) return SSN_ERR_SHAPE;
+  if (!U || !Up) return SSN_ERR_NULL;
+  const int64_t s = elem_size(dtype);
+  if (!aligned_to(U, s) || !aligned_to(Up, s)) return SSN_ERR_ALIGN;
+  if (overlap(span(Up, d * ldu * s), span(U, d * k * s))) return SSN_ERR_ALIAS;
+  return launch_status(ssn::launch_pad_basis(dtype, d, k, ldu, U, Up, (hipStream_t)stream));
+}
+
 ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t k, const void* E,
                                const void* U, float* P, void* stream) {
   return ssn_project_grad(dtype, V, d, k, E, U, P, stream);

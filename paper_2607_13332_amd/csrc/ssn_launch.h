@@ -40,6 +40,9 @@ hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t
                              const int32_t* ids, const void* E, const void* U, void* Y,
                              bool gather_z, hipStream_t st, const uint16_t* Zb = nullptr,
                              int kz = 0);
+// Up [d, ldu] = U [d, k] with zero columns k .. ldu - 1.
+hipError_t launch_pad_basis(int dtype, int64_t d, int64_t k, int64_t ldu, const void* U, void* Up,
+                            hipStream_t st);
 // dZp[din, k] = H[N, din]^T . GT[N, k] (float32 GT and dZp); `ws` holds the
 // partial sums of the token splits (factor_grad_workspace_bytes).
 size_t factor_grad_workspace_bytes(int dtype, int64_t N, int64_t din, int64_t k);

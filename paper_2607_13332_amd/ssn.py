@@ -60,6 +60,8 @@ def _declare(lib):
     lib.ssn_compress_projected_ex.restype = ctypes.c_int
     lib.ssn_compress_projected_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
                                               _c_i64, _c_p, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]
+    lib.ssn_pad_basis.restype = ctypes.c_int
+    lib.ssn_pad_basis.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]
     lib.ssn_project_table.restype = ctypes.c_int
     lib.ssn_project_table.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]
     lib.ssn_compress_projected.restype = ctypes.c_int
@@ -245,6 +247,24 @@ def project_grad(G: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] =
     _check("ssn_project_grad_ex", lib().ssn_project_grad_ex(
         _dt_code(t), _dt_code(z_dtype), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2), ldu,
         _dev(out, "out", z_dtype, 2), _stream(stream)))
+    return out
+
+
+def pad_basis(U: torch.Tensor, ldu: Optional[int] = None, out: Optional[torch.Tensor] = None,
+              stream=None) -> torch.Tensor:
+    """U [d, k] with zero columns appended up to ldu (default: the next
+    multiple of 16), the layout the `_ex` entry points read with aligned
+    16-byte pieces; pass it with k= to compress / project_grad."""
+    d, k = U.shape
+    ldu = 16 * ((k + 15) // 16) if ldu is None else int(ldu)
+    if out is None:
+        out = torch.empty((d, ldu), dtype=U.dtype, device=U.device)
+    if out.shape != (d, ldu):
+        raise ValueError(f"out has shape {tuple(out.shape)}, expected ({d}, {ldu})")
+    _same_device(U, out)
+    t = U.dtype
+    _check("ssn_pad_basis", lib().ssn_pad_basis(_dt_code(t), d, k, ldu, _dev(U, "U", t, 2),
+                                                _dev(out, "out", t, 2), _stream(stream)))
     return out
 
 

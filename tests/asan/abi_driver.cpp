@@ -58,6 +58,7 @@ int main() {
           ssn_decompress((ssn_dtype_t)dt, N, d, k, 100, Z, nullptr, nullptr, U, Y, nullptr);
           ssn_project_grad((ssn_dtype_t)dt, N, d, k, X, U, Z, nullptr);
           ssn_project_table((ssn_dtype_t)dt, N, d, k, E, U, Z, nullptr);
+          ssn_pad_basis((ssn_dtype_t)dt, d, k, k < BIG - 16 ? k + 13 : k, U, Y, nullptr);
           ssn_compress_projected((ssn_dtype_t)dt, N, d, k, 100, X, ids, T, U, Z, nullptr);
           ssn_factored_embedding((ssn_dtype_t)dt, N, d, k, 100, ids, T, U, Y, nullptr);
           for (int zt : {(int)SSN_F32, (int)SSN_BF16, 7}) {
@@ -110,6 +111,11 @@ int main() {
     void* V2[2] = {P(0x800000000000), P(0x800000000000 + 64)};   // overlapping
     EXPECT(ssn_project_weights_batched(SSN_BF16, 2, 4096, m, 64, V2, U, nullptr), SSN_ERR_ALIAS);
   }
+  EXPECT(ssn_pad_basis(SSN_BF16, 5120, 51, 64, U, Y, nullptr), SSN_OK);
+  EXPECT(ssn_pad_basis(SSN_BF16, 5120, 51, 50, U, Y, nullptr), SSN_ERR_SHAPE);
+  EXPECT(ssn_pad_basis(SSN_BF16, 5120, 51, 64, U, U, nullptr), SSN_ERR_ALIAS);
+  EXPECT(ssn_pad_basis(SSN_BF16, 5120, 51, 64, nullptr, Y, nullptr), SSN_ERR_NULL);
+  EXPECT(ssn_pad_basis(SSN_BF16, 5120, 51, 64, U, (char*)Y + 1, nullptr), SSN_ERR_ALIGN);
   EXPECT(ssn_project_weights_workspace_bytes(4096, 14336, 64), (size_t)0);
   EXPECT(ssn_project_weights(SSN_BF16, 4096, 14336, 64, X, U, nullptr, 0, nullptr), SSN_OK);
   EXPECT(ssn_project_weights(SSN_BF16, 4096, 14336, 64, X, U, Z, 64, nullptr), SSN_OK);

@@ -33,6 +33,10 @@ hipError_t launch_project_ranges(int dtype, int64_t, int64_t, int64_t, const voi
   g_launches += (dtype == kBF16 && ws && smax >= 2) ? 2 : 1;
   return hipSuccess;
 }
+hipError_t launch_pad_basis(int, int64_t, int64_t, int64_t, const void*, void*, hipStream_t) {
+  ++g_launches;
+  return hipSuccess;
+}
 size_t factor_grad_workspace_bytes(int dtype, int64_t N, int64_t din, int64_t k) {
   return (dtype == kBF16 && N > 0) ? (size_t)(2 * din * k * 4) : 0;
 }

@@ -172,6 +172,16 @@ def test_reparam_validation(ssn):
     assert e(1, 10, 128, 16, 100, A, B, C, B + 64, None) == ERR_ALIAS
 
 
+def test_pad_basis_validation(ssn):
+    f = ssn.lib().ssn_pad_basis
+    assert f(1, 5120, 51, 50, A, B, None) == ERR_SHAPE              # ldu < k
+    assert f(1, 5120, 0, 64, A, B, None) == ERR_SHAPE
+    assert f(1, 5120, 51, 64, None, B, None) == ERR_NULL
+    assert f(1, 5120, 51, 64, A, A + 64, None) == ERR_ALIAS         # the copy on top of U
+    assert f(1, 5120, 51, 64, A, B + 1, None) == ERR_ALIGN
+    assert f(4, 5120, 51, 64, A, B, None) == ERR_DTYPE
+
+
 def test_project_weights_validation(ssn):
     L = ssn.lib()
     f = L.ssn_project_weights

@@ -350,8 +350,10 @@ def test_padded_basis(N, d, k, ldu, dtype):
     Xh = I.store(r.standard_normal((N, d)), dtype)
     ids_h = r.integers(0, V, size=N).astype(np.int32)
     X, E, U, ids = dev(Xh, dtype), dev(Eh, dtype), dev(Uh, dtype), dev(ids_h, dtype)
-    Up = torch.zeros((d, ldu), dtype=U.dtype, device=DEV)
-    Up[:, :k] = U
+    Up = ssn.pad_basis(U, ldu)
+    Uref = torch.zeros((d, ldu), dtype=U.dtype, device=DEV)
+    Uref[:, :k] = U
+    assert torch.equal(Up, Uref)           # the library's padded copy, bit for bit
     outkind = "bf16out" if dtype == "bf16" else "f32out_dec"
     Z = ssn.compress(X, ids, E, Up, k=k)
     assert Z.shape == (N, k)
