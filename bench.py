@@ -435,8 +435,13 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
             step(sets[i % 2], Ub)
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3 / steps
+        # per-op times: each step with its events is queued behind a ~1 ms
+        # spin kernel, so the GPU runs the four kernels back to back instead
+        # of waiting for the host between launches (at these sizes a kernel
+        # takes about as long as its launch from Python)
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
         for i in range(steps):
+            torch.cuda._sleep(2_000_000)
             step(sets[i % 2], Ub, evs[i])
         torch.cuda.synchronize()
         op_ms = {op: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, op in enumerate(ops)}

@@ -141,11 +141,15 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     xr[i] = X + t * d + 8 * lc;
     er[i] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * lc : nullptr;
   }
-  const int nch = d / DC;
+  // blockIdx.y selects one of gridDim.y equal ranges of d (a plain
+  // projection with few tokens: the range's partial product goes to rows
+  // [blockIdx.y * N, (blockIdx.y + 1) * N) of Z, summed afterwards)
+  const int nch = d / DC / (int)gridDim.y;
+  const int cbase = (int)blockIdx.y * nch;
   // rotation in units of ROTG chunks (when they divide nch)
   const int rg = (ROTG > 1 && nch % ROTG == 0) ? ROTG : 1;
   const int rot = ROT ? (int)(blockIdx.x % (unsigned)(nch / rg)) * rg : 0;
-  auto chunk = [&](int i) { const int x = i + rot; return x < nch ? x : x - nch; };
+  auto chunk = [&](int i) { const int x = i + rot; return cbase + (x < nch ? x : x - nch); };
 
   // DEPTH register sets: step i's rows travel in set i % DEPTH
   u32x4 xv[DEPTH][4], ev[DEPTH][4];
@@ -271,7 +275,7 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
             if (col0 + i < kz) zb[i] = (uint16_t)f32_to_bf16(v[i]);
         }
       } else {
-        float* zp = Z + tj * kz + col0;
+        float* zp = Z + ((int64_t)blockIdx.y * N + tj) * kz + col0;
         if constexpr (KFULL && KP % 4 == 0) {
           if (whole) {
 #pragma unroll
@@ -892,6 +896,18 @@ bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) {
 // concurrent requests collide (measured 1.1-1.8x slower at d = 4096).
 // Activation rows are streamed with non-temporal loads; embedding rows keep
 // normal caching (repeated ids hit in L2).
+// Z = X.U with few tokens: 128-token blocks of the row kernel over S ranges
+// of d (grid.y), each writing its partial product to ws [S][N][k].
+template <int KP, bool KFULL>
+static hipError_t launch_rows_ranges(int64_t N, int d, int k, const void* X, const void* U, float* ws,
+                                     int S, hipStream_t st) {
+  const int64_t blocks = (N + 127) / 128;
+  hipLaunchKernelGGL((compress_rows_bf16<KP, false, KFULL, 8, 1, true, false, true, 4, false>),
+                     dim3((unsigned)blocks, (unsigned)S), dim3(512), 0, st, (const uint16_t*)X,
+                     nullptr, nullptr, (const uint16_t*)U, ws, N, d, k, (int64_t)1, nullptr, nullptr, k);
+  return hipGetLastError();
+}
+
 template <int KP, bool HAS_E, bool KFULL, bool HAS_P>
 static hipError_t launch_compress_rows(int64_t N, int d, int k, int64_t V, const void* X,
                                        const int32_t* ids, const void* E, const void* U, float* Z,
@@ -1150,11 +1166,45 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
 
 // Z = X.U; with few tokens the few-token kernel may split d into up to
 // smax ranges whose partial products go to ws [S][N][k] and are then summed.
+// Ranges of d for the row kernel with few tokens: the smallest S <= smax
+// dividing the chunk count for which the 128-token blocks of all ranges
+// reach one block per compute unit, each range keeping at least 8 chunks
+// (0: the token blocks alone fill the chip, or no such S).  Only for the
+// widths whose U the row kernel stages as whole 16-byte row pieces (k = 32,
+// 64, 128).  Measured on MI355X, N = 4096, k = 64: H Zp over din = 18432 in
+// 8 ranges of 18 chunks (forward 60.5 -> 49.4 us with the expansion); G U
+// over d = 5120 in 8 ranges of 5 chunks lost to the d-split kernel, and at
+// k = 51 the element-wise U staging made the forward 68 -> 94 us.
+static int rows_ranges(int64_t N, int64_t d, int64_t k, int smax) {
+  const int64_t blocks = (N + 127) / 128, cus = device_cu_count();
+  const int nch = (int)(d / kCompressDC);
+  const bool wide = k == 32 || k == 64 || k == 128;
+  if (!wide || blocks >= cus || d % kCompressDC != 0) return 0;
+  for (int S = 2; S <= smax && 8 * S <= nch; ++S)
+    if (nch % S == 0 && blocks * S >= cus) return S;
+  return 0;
+}
+
 hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, const void* X,
                                  const void* U, float* Z, float* ws, int smax, hipStream_t st) {
+  const int rs = (smax > 1 && ws && dtype == kBF16 && k <= 128 && al16(X) && al16(U) && al16(ws) &&
+                  d <= INT32_MAX)
+                     ? rows_ranges(N, d, k, smax)
+                     : 0;
+  if (rs > 1) {
+    hipError_t e;
+    if (k == 32) e = launch_rows_ranges<2, true>(N, (int)d, (int)k, X, U, ws, rs, st);
+    else if (k == 64) e = launch_rows_ranges<4, true>(N, (int)d, (int)k, X, U, ws, rs, st);
+    else e = launch_rows_ranges<8, true>(N, (int)d, (int)k, X, U, ws, rs, st);
+    if (e != hipSuccess) return e;
+    const int64_t n = N * k;
+    const int64_t blocks = (n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048;
+    hipLaunchKernelGGL(sum_partials, dim3((unsigned)blocks), dim3(256), 0, st, ws, Z, n, rs);
+    return hipGetLastError();
+  }
   if (smax > 1 && ws && compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(Z) &&
       compress_uses_split(N, d, k, false)) {
-    const SplitPlan sp = split_plan(N, (int)d, (int)k, false, smax);
+    const SplitPlan sp = split_plan(N, (int)d, (int)k, false, smax < 4 ? smax : 4);
     if (sp.S > 1) {
       hipError_t e = launch_split<false, false>(N, (int)d, (int)k, 1, X, nullptr, nullptr, U, ws,
                                                 nullptr, st, sp, nullptr, (int)k);

@@ -14,7 +14,7 @@ namespace {
 
 constexpr int64_t kMaxElems = (int64_t)1 << 56;   // keeps every byte offset in int64
 // ranges of the inner dimension in the reparameterized layer's first projection
-constexpr int kReparamMaxRanges = 4;
+constexpr int kReparamMaxRanges = 16;
 
 inline int64_t elem_size(int dtype) { return dtype == SSN_BF16 ? 2 : 4; }
 

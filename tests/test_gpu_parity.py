@@ -481,6 +481,11 @@ REPARAM_SHAPES = [  # (N, din, d, k, dtype): every kernel family and tail
     # k > 64 with k % 4 != 0: the factor gradient's element-wise G U staging
     # on 256-column blocks
     (500, 1024, 512, 97, "bf16"),
+    # few tokens on the row kernel over ranges of the inner dimension (partial
+    # products staged in the output; forward only: the backward's G U over d
+    # has too few chunks per range and keeps the d-split kernel): k = 64 and
+    # 128 in 8 ranges, k = 32 in 16 ranges
+    (4096, 18432, 2048, 64, "bf16"), (4096, 8192, 2048, 128, "bf16"), (2048, 16384, 1024, 32, "bf16"),
 ]
 
 
