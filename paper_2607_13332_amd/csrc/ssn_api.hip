@@ -307,6 +307,9 @@ ssn_status_t ssn_reparam_backward(ssn_dtype_t dtype, int64_t N, int64_t din, int
   // GH is written only after GT is complete: it holds the partial products
   hipError_t e = project_in_ranges(dtype, N, d, k, G, U, GT, GH, din * s, st);
   if (e != hipSuccess) return SSN_ERR_LAUNCH;
+  if (ssn::reparam_backward_fuses(dtype, N, din, k, H, GT, Zp, GH))
+    return launch_status(ssn::launch_reparam_backward_fused(N, din, k, H, GT, Zp, GH, GZp,
+                                                            (float*)workspace, st));
   e = ssn::launch_decompress(dtype, N, din, k, 1, GT, nullptr, nullptr, Zp, GH, false, st);
   if (e != hipSuccess) return SSN_ERR_LAUNCH;
   return launch_status(ssn::launch_factor_grad(dtype, N, din, k, H, GT, GZp, (float*)workspace, st));

@@ -48,6 +48,15 @@ hipError_t launch_pad_basis(int dtype, int64_t d, int64_t k, int64_t ldu, const 
 size_t factor_grad_workspace_bytes(int dtype, int64_t N, int64_t din, int64_t k);
 hipError_t launch_factor_grad(int dtype, int64_t N, int64_t din, int64_t k, const void* H,
                               const float* GT, float* dZp, float* ws, hipStream_t st);
+// Both [N, din] gradients of the reparameterized layer in one launch (plus
+// the split sum): GH = GT Zp^T and dZp = H^T GT, the same bits as
+// launch_decompress(GT, Zp) and launch_factor_grad; `ws` as for
+// launch_factor_grad.  Only where reparam_backward_fuses() holds.
+bool reparam_backward_fuses(int dtype, int64_t N, int64_t din, int64_t k, const void* H,
+                            const float* GT, const void* Zp, const void* GH);
+hipError_t launch_reparam_backward_fused(int64_t N, int64_t din, int64_t k, const void* H,
+                                         const float* GT, const void* Zp, void* GH, float* dZp,
+                                         float* ws, hipStream_t st);
 // count matrices W[b] [d, n[b]] sharing U [d, k], re-projected in place.
 hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t* n, int64_t k,
                                   void* const* W, const void* U, hipStream_t st);

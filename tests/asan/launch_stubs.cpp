@@ -37,6 +37,15 @@ hipError_t launch_pad_basis(int, int64_t, int64_t, int64_t, const void*, void*, 
   ++g_launches;
   return hipSuccess;
 }
+bool reparam_backward_fuses(int, int64_t, int64_t, int64_t, const void*, const float*, const void*,
+                            const void*) {
+  return false;
+}
+hipError_t launch_reparam_backward_fused(int64_t, int64_t, int64_t, const void*, const float*,
+                                         const void*, void*, float*, float*, hipStream_t) {
+  ++g_launches;
+  return hipSuccess;
+}
 size_t factor_grad_workspace_bytes(int dtype, int64_t N, int64_t din, int64_t k) {
   return (dtype == kBF16 && N > 0) ? (size_t)(2 * din * k * 4) : 0;
 }

@@ -515,6 +515,31 @@ def test_reparam_shapes(N, din, d, k, dtype):
     assert torch.equal(GZ, GZ2)
 
 
+@pytest.mark.parametrize("N,din,d,k", [(4096, 18432, 5120, 64), (2048, 1024, 512, 32),
+                                        (1024, 2048, 1024, 128), (96, 512, 256, 64)])
+def test_reparam_backward_fused_pass(N, din, d, k):
+    """Whole tiles and chunks: one launch writes dL/dH and accumulates dL/dZp
+    from the same chunks of H.  dL/dH is the expansion of G U by Zp^T bit for
+    bit (the same MFMA sequence), and both match the oracle element by
+    element; the factor gradient's split sum is deterministic."""
+    seed = N + din + k
+    print(f"[case] reparam fused backward N={N} din={din} d={d} k={k}", flush=True)
+    r = np.random.default_rng(seed)
+    Hh = I.store(r.standard_normal((N, din)), "bf16")
+    Zh = I.store(0.05 * r.standard_normal((din, k)), "bf16")
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), "bf16")
+    Gh = I.store(r.standard_normal((N, d)), "bf16")
+    H, Zp, U, G = dev(Hh, "bf16"), dev(Zh, "bf16"), dev(Uh, "bf16"), dev(Gh, "bf16")
+    GT, GH, GZ = ssn.reparam_backward(H, Zp, U, G)
+    assert torch.equal(GH, ssn.expand_grad(GT, Zp))
+    check("fused dL/dH", host(GH), O.reparam_grad_input(Gh, Zh, Uh), "bf16", "bf16out",
+          mag_reparam_grad_input(Gh, Zh, Uh))
+    check("fused dL/dZp", host(GZ), O.reparam_grad_factor(Hh, Gh, Uh), "bf16", "f32out",
+          mag_reparam_grad_factor(Hh, Gh, Uh))
+    _, GH2, GZ2 = ssn.reparam_backward(H, Zp, U, G)
+    assert torch.equal(GH, GH2) and torch.equal(GZ, GZ2)
+
+
 def test_reparam_staging_memory_alignment():
     """With few tokens the projections stage partial products over ranges of
     the inner dimension in the output's memory (Y forward, dL/dH backward).
