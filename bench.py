@@ -200,11 +200,22 @@ def time_weights(wc, steps: int, dev):
     reps = 10
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
     ev[0].record()
-    for r in range(reps):
+    for r in range(reps):       # back to back
         ssn.project_weights_batched(Ws, Uw)
         ev[r + 1].record()
     torch.cuda.synchronize()
     wms = sum(ev[r].elapsed_time(ev[r + 1]) for r in range(reps)) / reps
+    # the same call after 20 ms of idle GPU, as once per optimizer step
+    iso = []
+    for r in range(5):
+        time.sleep(0.02)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        ssn.project_weights_batched(Ws, Uw)
+        e1.record()
+        torch.cuda.synchronize()
+        iso.append(e0.elapsed_time(e1))
+    iso_ms = sorted(iso)[len(iso) // 2]
     wbytes = sum(2 * W.numel() * 2 for W in Ws) + wc.d * wc.k * 2
     wflops = sum(4.0 * wc.d * wc.k * W.shape[1] for W in Ws)
     shapes = " + ".join(f"{a}x{b}" for a, b in wc.shapes)
@@ -215,6 +226,9 @@ def time_weights(wc, steps: int, dev):
         "frac_hbm_peak": round(wbytes / (wms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "mfma_TFLOPs": round(wflops / (wms * 1e-3) / 1e12, 2),
         "frac_mfma_peak": round(wflops / (wms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        "isolated_call": {"what": "median of 5 single calls, each after 20 ms of idle GPU",
+                          "ms": round(iso_ms, 5),
+                          "frac_hbm_peak": round(wbytes / (iso_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
     }
     if wc.name == I.WEIGHTS.name:
         out["traffic"] = load_traffic("project_weights")
@@ -435,16 +449,32 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
             step(sets[i % 2], Ub)
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3 / steps
-        # per-op times: each step with its events is queued behind a ~1 ms
-        # spin kernel, so the GPU runs the four kernels back to back instead
-        # of waiting for the host between launches (at these sizes a kernel
-        # takes about as long as its launch from Python)
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
-        for i in range(steps):
-            torch.cuda._sleep(2_000_000)
-            step(sets[i % 2], Ub, evs[i])
-        torch.cuda.synchronize()
-        op_ms = {op: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, op in enumerate(ops)}
+        # per-op times: R back-to-back calls of one op (alternating input
+        # sets) queued behind a ~1 ms spin kernel, one event pair around them,
+        # so the GPU runs them without waiting for the host between launches
+        # (at these sizes a kernel takes about as long as its launch from
+        # Python); the time per call includes the dispatch gap between
+        # dependent kernels
+        R = 20
+        calls = {
+            "decompress": lambda s: ssn.decompress(s["Zin"], s["ids"], E, Ub, out=s["Y"]),
+            "project_grad": lambda s: ssn.project_grad(s["G"], Ub, out=s["GZ"], k=k),
+            "compress": lambda s: ssn.compress(s["X"], s["ids_c"], E, Ub, out=s["Z"], k=k),
+            "expand_grad": lambda s: ssn.expand_grad(s["GZin"], Ub, out=s["GX"]),
+        }
+        op_ms = {}
+        for op in ops:
+            ts = []
+            for rep in range(max(3, steps // 10)):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda._sleep(2_000_000)
+                e0.record()
+                for i in range(R):
+                    calls[op](sets[i % 2])
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) / R)
+            op_ms[op] = float(np.median(ts))
         return ms, op_ms
 
     Ub, ldu, pad_ms = U, k, None

@@ -96,10 +96,13 @@ def test_wire_formats_capture():
             assert torch.equal(got[key], ref[key]), f"replay {rep}: {key} differs from eager"
 
 
-def test_reparam_and_averaging_capture():
+@pytest.mark.parametrize("N,din,d,k", [(1024, 2048, 1024, 51), (2048, 16384, 1024, 32)],
+                         ids=["d_split_kernels", "row_ranges_and_fused_backward"])
+def test_reparam_and_averaging_capture(N, din, d, k):
     """The reparameterized layer (forward + backward with its workspace) and
-    a delta-rule round in one graph."""
-    N, din, d, k = 1024, 2048, 1024, 51
+    a delta-rule round in one graph: the d-split projections with separate
+    backward kernels (k = 51), and the row kernel over ranges of din with the
+    fused backward pass (k = 32, whole tiles)."""
     g0 = torch.Generator(device=DEV).manual_seed(3)
 
     def draw():
