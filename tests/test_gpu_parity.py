@@ -3,8 +3,10 @@ float64 oracle on the same seeded inputs.
 
 Bar: relative Frobenius error <= 1e-5 for fp32 storage and <= 2e-2 for bf16
 storage with fp32 accumulation (helpers.TOL), plus the tighter bounds that the
-kernels' own arithmetic guarantees (helpers.DESIGN).  Full-size workloads are
-checked on seeded row / column samples that the oracle computes directly.
+kernels' own arithmetic guarantees (helpers.DESIGN), and every element within
+its own bound.  The codec workloads are checked on every row (in blocks of
+4096); the weight and reparameterized workloads at full size on seeded
+column / row samples that the oracle computes directly.
 """
 import numpy as np
 import pytest
@@ -163,13 +165,6 @@ def _check_codec_rows(cfg, inp, out, rows, label):
           mag_decompress(Zs, None, None, Us))
 
 
-def _sampled_codec_check(cfg, nsample=384):
-    inp, out = _codec_outputs(cfg)
-    _check_codec_rows(cfg, inp, out, sample_rows(cfg.N, nsample, cfg.seed), " (sampled rows)")
-    del inp, out
-    torch.cuda.empty_cache()
-
-
 @pytest.mark.timeout(600)
 def test_stage8b_full_size_all_rows():
     """The 8B-stage workload at full size, every one of the 32768 rows of
@@ -184,14 +179,42 @@ def test_stage8b_full_size_all_rows():
     torch.cuda.empty_cache()
 
 
+def _all_rows_check(cfg, inp, out, label=""):
+    for r0 in range(0, cfg.N, O.ROW_BLOCK):
+        rows = np.arange(r0, min(cfg.N, r0 + O.ROW_BLOCK), dtype=np.int64)
+        _check_codec_rows(cfg, inp, out, rows, f"{label} rows {r0}..{rows[-1]}")
+
+
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("cfg", I.sweep_configs(), ids=lambda c: c.name)
-def test_sweep_full_size_sampled(cfg):
-    _sampled_codec_check(cfg, nsample=256)
+def test_sweep_full_size_all_rows(cfg):
+    """Zipf-id sweep at full size, every row of every op (blocks of 4096)."""
+    inp, out = _codec_outputs(cfg)
+    _all_rows_check(cfg, inp, out)
+    del inp, out
+    torch.cuda.empty_cache()
 
 
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("cfg", I.paper_configs(), ids=lambda c: c.name)
-def test_paper_shapes_full_size_sampled(cfg):
-    _sampled_codec_check(cfg, nsample=256)
+def test_paper_shapes_full_size_all_rows(cfg):
+    """The paper's microbatch shapes at full size, every row of every op, on
+    the basis as stored and on its zero-padded copy (ssn_pad_basis, the
+    layout the bench times for k = 51 and 40): both against the oracle on
+    the unpadded basis."""
+    inp, out = _codec_outputs(cfg)
+    _all_rows_check(cfg, inp, out)
+    k = cfg.k
+    ldu = 16 * ((k + 15) // 16)
+    Up = ssn.pad_basis(inp["U"], ldu)
+    X, ids, E, G, Zin = inp["X"], inp["ids"], inp["E"], inp["G"], inp["Zin"]
+    outp = {"Z": ssn.compress(X, ids, E, Up, k=k), "Y": ssn.decompress(Zin, ids, E, Up),
+            "GZ": ssn.project_grad(G, Up, k=k), "GX": ssn.expand_grad(Zin, Up)}
+    torch.cuda.synchronize()
+    assert outp["Z"].shape == (cfg.N, k) and outp["GZ"].shape == (cfg.N, k)
+    _all_rows_check(cfg, inp, outp, f" padded to {ldu}")
+    del inp, out, outp, Up
+    torch.cuda.empty_cache()
 
 
 # ---------------------------------------------------------------- config 4
