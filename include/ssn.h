@@ -125,6 +125,19 @@ ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, 
                             void *Xout, void *stream);
 
 /*
+ * ssn_check_ids -- the ids contract above, checked on the device: writes to
+ * *bad the number of i in [0, N) with ids[i] < 0 or ids[i] >= V.
+ *   ids [N] int32, bad: one int64 (device memory) output
+ * Section 4.1's receiver gathers E[ids] for every token of a microbatch; a
+ * caller that wants out-of-range ids to be an error rather than unspecified
+ * rows runs this on the same stream before the codec call and reads *bad
+ * after a synchronisation.  One launch of one block; the count is a block
+ * reduction written by one thread (no atomics), so *bad needs no clearing,
+ * and N == 0 writes 0.  Requires V >= 1; bad must not overlap ids.
+ */
+ssn_status_t ssn_check_ids(int64_t N, int64_t V, const int32_t *ids, int64_t *bad, void *stream);
+
+/*
  * ssn_project_grad -- backward compression, section 4.1 ("the backward pass
  * uses the same compression"): the receiver sends G_Z = G . U back.
  *   G  [N, d] dtype      gradient w.r.t. the decompressed activation

@@ -1322,4 +1322,30 @@ hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t
   return launch_decompress_generic<uint16_t, false, false>(N, d, k, V, Zc, ids, E, U, Y, st, Zb, kz64);
 }
 
+// ===========================================================================
+// ids outside [0, V): one block counts them with a grid-free stride loop and
+// a fixed-order LDS reduction; thread 0 writes the count (no atomics).
+// ===========================================================================
+__global__ __launch_bounds__(1024) void check_ids_kernel(const int32_t* __restrict__ ids, int64_t N,
+                                                         int64_t V, int64_t* __restrict__ bad) {
+  __shared__ int64_t part[1024];
+  int64_t cnt = 0;
+  for (int64_t i = threadIdx.x; i < N; i += 1024) {
+    const int64_t v = ids[i];
+    cnt += (v < 0 || v >= V) ? 1 : 0;
+  }
+  part[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int h = 512; h >= 1; h >>= 1) {
+    if ((int)threadIdx.x < h) part[threadIdx.x] += part[threadIdx.x + h];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *bad = part[0];
+}
+
+hipError_t launch_check_ids(int64_t N, int64_t V, const int32_t* ids, int64_t* bad, hipStream_t st) {
+  hipLaunchKernelGGL(check_ids_kernel, dim3(1), dim3(1024), 0, st, ids, N, V, bad);
+  return hipGetLastError();
+}
+
 }  // namespace ssn

@@ -201,6 +201,14 @@ ssn_status_t ssn_pad_basis(ssn_dtype_t dtype, int64_t d, int64_t k, int64_t ldu,
   return launch_status(ssn::launch_pad_basis(dtype, d, k, ldu, U, Up, (hipStream_t)stream));
 }
 
+ssn_status_t ssn_check_ids(int64_t N, int64_t V, const int32_t* ids, int64_t* bad, void* stream) {
+  if (N < 0 || V < 1 || !mul_ok(N, 4)) return SSN_ERR_SHAPE;
+  if (!bad || (N > 0 && !ids)) return SSN_ERR_NULL;
+  if (!aligned_to(bad, 8) || (ids && !aligned_to(ids, 4))) return SSN_ERR_ALIGN;
+  if (ids && overlap(span(bad, 8), span(ids, N * 4))) return SSN_ERR_ALIAS;
+  return launch_status(ssn::launch_check_ids(N, V, ids, bad, (hipStream_t)stream));
+}
+
 ssn_status_t ssn_project_table(ssn_dtype_t dtype, int64_t V, int64_t d, int64_t k, const void* E,
                                const void* U, float* P, void* stream) {
   return ssn_project_grad(dtype, V, d, k, E, U, P, stream);

@@ -40,6 +40,8 @@ hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t
                              const int32_t* ids, const void* E, const void* U, void* Y,
                              bool gather_z, hipStream_t st, const uint16_t* Zb = nullptr,
                              int kz = 0);
+// *bad = number of ids outside [0, V) (one block, written once; N may be 0).
+hipError_t launch_check_ids(int64_t N, int64_t V, const int32_t* ids, int64_t* bad, hipStream_t st);
 // Up [d, ldu] = U [d, k] with zero columns k .. ldu - 1.
 hipError_t launch_pad_basis(int dtype, int64_t d, int64_t k, int64_t ldu, const void* U, void* Up,
                             hipStream_t st);

@@ -60,6 +60,8 @@ def _declare(lib):
     lib.ssn_compress_projected_ex.restype = ctypes.c_int
     lib.ssn_compress_projected_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
                                               _c_i64, _c_p, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]
+    lib.ssn_check_ids.restype = ctypes.c_int
+    lib.ssn_check_ids.argtypes = [_c_i64, _c_i64, _c_p, _c_p, _c_p]
     lib.ssn_pad_basis.restype = ctypes.c_int
     lib.ssn_pad_basis.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]
     lib.ssn_project_table.restype = ctypes.c_int
@@ -247,6 +249,21 @@ def project_grad(G: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] =
     _check("ssn_project_grad_ex", lib().ssn_project_grad_ex(
         _dt_code(t), _dt_code(z_dtype), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2), ldu,
         _dev(out, "out", z_dtype, 2), _stream(stream)))
+    return out
+
+
+def check_ids(ids: torch.Tensor, V: int, out: Optional[torch.Tensor] = None,
+              stream=None) -> torch.Tensor:
+    """Number of ids outside [0, V), counted on the device into a one-element
+    int64 tensor (read it after the stream has run)."""
+    if ids.dim() != 1:
+        raise ValueError(f"ids must be 1-D, got {tuple(ids.shape)}")
+    if out is None:
+        out = torch.empty((1,), dtype=torch.int64, device=ids.device)
+    _same_device(ids, out)
+    _check("ssn_check_ids", lib().ssn_check_ids(
+        ids.shape[0], int(V), _dev(ids, "ids", torch.int32, 1), _dev(out, "out", torch.int64, 1),
+        _stream(stream)))
     return out
 
 

@@ -33,6 +33,10 @@ hipError_t launch_project_ranges(int dtype, int64_t, int64_t, int64_t, const voi
   g_launches += (dtype == kBF16 && ws && smax >= 2) ? 2 : 1;
   return hipSuccess;
 }
+hipError_t launch_check_ids(int64_t, int64_t, const int32_t*, int64_t*, hipStream_t) {
+  ++g_launches;
+  return hipSuccess;
+}
 hipError_t launch_pad_basis(int, int64_t, int64_t, int64_t, const void*, void*, hipStream_t) {
   ++g_launches;
   return hipSuccess;

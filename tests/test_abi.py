@@ -182,6 +182,18 @@ def test_pad_basis_validation(ssn):
     assert f(4, 5120, 51, 64, A, B, None) == ERR_DTYPE
 
 
+def test_check_ids_validation(ssn):
+    f = ssn.lib().ssn_check_ids
+    assert f(-1, 100, A, B, None) == ERR_SHAPE
+    assert f(10, 0, A, B, None) == ERR_SHAPE                    # V >= 1
+    assert f(10, 100, None, B, None) == ERR_NULL
+    assert f(10, 100, A, None, None) == ERR_NULL
+    assert f(0, 100, None, None, None) == ERR_NULL               # the count is always written
+    assert f(10, 100, A + 2, B, None) == ERR_ALIGN
+    assert f(10, 100, A, B + 4, None) == ERR_ALIGN               # int64 count
+    assert f(10, 100, A, A + 8, None) == ERR_ALIAS               # count inside the id array
+
+
 def test_project_weights_validation(ssn):
     L = ssn.lib()
     f = L.ssn_project_weights

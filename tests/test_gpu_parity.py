@@ -723,6 +723,25 @@ def test_out_of_range_ids_are_clamped(N, d, k, dtype):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("N", [0, 1, 1000, 131072 + 77])
+def test_check_ids_counts_out_of_range_ids(N):
+    """ssn_check_ids against a host count, with planted ids below 0, at V,
+    and at the int32 extremes."""
+    V = 128256
+    r = np.random.default_rng(N + 3)
+    h = r.integers(0, V, size=N, dtype=np.int64)
+    if N:
+        bad = r.choice(N, size=min(N, 1 + N // 97), replace=False)
+        h[bad] = r.choice(np.array([-1, V, V + 5, -(2 ** 31), 2 ** 31 - 1, -V]), size=bad.size)
+    h = h.astype(np.int32)
+    ids = torch.from_numpy(h).to(DEV)
+    out = torch.full((1,), -7, dtype=torch.int64, device=DEV)
+    ssn.check_ids(ids, V, out=out)
+    torch.cuda.synchronize()
+    want = int(np.count_nonzero((h.astype(np.int64) < 0) | (h.astype(np.int64) >= V)))
+    assert int(out.item()) == want
+
+
 def test_non_default_stream_and_determinism():
     cfg = I.with_tokens(I.MID, 4096)
     h = structured_inputs(cfg)
