@@ -87,6 +87,13 @@ def parse_args():
                         "keeps its kernels apart from the codec's in a kernel trace)")
     p.add_argument("--sweep-tokens", type=str, default="",
                    help="with --only sweep / paper: comma-separated token counts to keep")
+    p.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"), default=None,
+                   help="no GPU work: turn the counter_collection.csv files of a rocprofv3 "
+                        "--pmc FETCH_SIZE run and a --pmc WRITE_SIZE run of this bench "
+                        "(with --copy-calib 256) into profiles/traffic.json and print the table")
+    p.add_argument("--summarize-trace", metavar="TRACE_CSV", default=None,
+                   help="no GPU work: per-kernel table (grid, block, registers, LDS, calls, "
+                        "median / mean us) of a rocprofv3 --kernel-trace csv")
     p.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                    help="before the timed region, run a plain device copy of MIB MiB three times "
                         "(a known-size kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE); "
@@ -126,6 +133,112 @@ def load_traffic(kernel_key: str):
         return None
     ent = t.get("kernels", {}).get(kernel_key)
     return None if ent is None else ent.get("bytes_per_launch")
+
+
+def _template_args(kernel_name: str):
+    """Template arguments of a demangled kernel name, as strings."""
+    if "<" not in kernel_name:
+        return []
+    inner = kernel_name.split("<", 1)[1].rsplit(">", 1)[0]
+    return [a.strip() for a in inner.split(",")]
+
+
+def traffic_op(kernel_name: str, grid: int):
+    """Which headline op a dispatch of the headline bench run belongs to."""
+    a = _template_args(kernel_name)
+    if "copyBuffer" in kernel_name:
+        return "calibration"
+    if "decompress_mfma_bf16" in kernel_name and a[:1] == ["2"]:
+        return "decompress" if a[1] == "true" else "expand_grad"
+    if "compress_rows_bf16" in kernel_name and a[:1] == ["4"]:
+        if a[1] == "true":
+            return "compress"
+        if a[-1] == "true":
+            return "compress_projected"
+        # the gradient projection over N = 32768 rows, or the table over V rows
+        return "project_grad" if grid == 32768 // 128 * 512 else "project_table"
+    if "project_weights_cols_bf16" in kernel_name:
+        return "project_weights"
+    return None
+
+
+def summarize_traffic(fetch_csv: str, write_csv: str, calib_bytes: int = 256 << 20):
+    """profiles/traffic.json from two rocprofv3 counter runs of this bench.
+
+    Each counter is read in KiB per dispatch; both are scaled by what they
+    read for the plain device copy of known size that --copy-calib runs (on
+    this GPU FETCH_SIZE counts half of a copy's reads).  Per op: the median
+    over its dispatches."""
+    import csv
+    import statistics
+
+    def per_op(path, counter):
+        vals, names = {}, {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] != counter:
+                    continue
+                grid = int(r["Grid_Size"])
+                op = traffic_op(r["Kernel_Name"], grid)
+                if op is None:
+                    continue
+                vals.setdefault(op, []).append(float(r["Counter_Value"]))
+                names[op] = (r["Kernel_Name"].split("(")[0], grid)
+        return vals, names
+
+    fv, names = per_op(fetch_csv, "FETCH_SIZE")
+    wv, _ = per_op(write_csv, "WRITE_SIZE")
+    fscale = calib_bytes / (statistics.median(fv["calibration"]) * 1024.0)
+    wscale = calib_bytes / (statistics.median(wv["calibration"]) * 1024.0)
+    out = {"kernel_source_hash": kernel_source_hash(),
+           "calibration": {"kernel": "__amd_rocclr_copyBuffer (torch copy_ of "
+                                     f"{calib_bytes >> 20} MiB)",
+                           "known_bytes": calib_bytes, "fetch_scale": round(fscale, 4),
+                           "write_scale": round(wscale, 4)},
+           "kernels": {}}
+    rows = []
+    for op in ("project_grad", "project_table", "compress_projected", "compress", "expand_grad",
+               "decompress", "project_weights"):
+        if op not in fv or op not in wv:
+            continue
+        fk, wk = statistics.median(fv[op]), statistics.median(wv[op])
+        rb, wb = int(fk * 1024 * fscale), int(wk * 1024 * wscale)
+        name, grid = names[op]
+        out["kernels"][op] = {"kernel": name, "grid": grid, "fetch_kib": round(fk, 1),
+                              "write_kib": round(wk, 1), "read_bytes": rb, "write_bytes": wb,
+                              "bytes_per_launch": rb + wb}
+        rows.append(f"| {op} | `{name}` | {grid} | {len(fv[op])} | {fk:.0f} | {wk:.0f} | "
+                    f"{rb / 1e6:.1f} | {wb / 1e6:.1f} | {(rb + wb) / 1e6:.1f} |")
+    with open(os.path.join(PROFILES, "traffic.json"), "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(f"scales: fetch {fscale:.4f}, write {wscale:.4f}")
+    print("| op | kernel | grid | dispatches | FETCH KiB | WRITE KiB | scaled MB read | "
+          "scaled MB written | total MB |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    print("\n".join(rows))
+
+
+def summarize_trace(trace_csv: str):
+    """Markdown table of a rocprofv3 kernel trace: one row per kernel and 2-D
+    grid, sorted by total time."""
+    import csv
+    import statistics
+    groups = {}
+    with open(trace_csv) as f:
+        for r in csv.DictReader(f):
+            name = r["Kernel_Name"]
+            name = (name[5:] if name.startswith("void ") else name).split("(")[0]
+            key = (name, f"{r['Grid_Size_X']} x {r['Grid_Size_Y']}",
+                   r["Workgroup_Size_X"], r["VGPR_Count"], r["LDS_Block_Size"])
+            us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            groups.setdefault(key, []).append(us)
+    print("| kernel | grid (threads) | block | VGPR | LDS B | calls | median µs | mean µs |")
+    print("|---|---|---|---|---|---|---|---|")
+    for key, ts in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        name, grid, block, vgpr, lds = key
+        print(f"| `{name}` | {grid} | {block} | {vgpr} | {lds} | {len(ts)} | "
+              f"{statistics.median(ts):.1f} | {statistics.mean(ts):.1f} |")
 
 
 def cpu_model() -> str:
@@ -578,6 +691,12 @@ def run_section(name: str, args, dev):
 
 def main():
     args = parse_args()
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
               "(the codec shards over tokens with no exchange; see the design notes)",

@@ -22,3 +22,40 @@ def test_algorithmic_bytes_count_distinct_rows_once():
     assert bench.algorithmic_bytes("compress", N, d, k, u) == N * d * 2 + u * d * 2 + N * k * 4 + d * k * 2 + 4 * N
     assert bench.algorithmic_bytes("decompress", N, d, k, u) == bench.algorithmic_bytes("compress", N, d, k, u)
     assert bench.algorithmic_bytes("project_grad", N, d, k, u) == N * d * 2 + N * k * 4 + d * k * 2
+
+
+def test_traffic_summary_from_counter_files(tmp_path, monkeypatch):
+    """profiles/traffic.json is rebuilt from two rocprofv3 counter files:
+    each op's median counter, scaled by the known-size copy."""
+    import csv
+    import json
+    import bench
+    cols = ["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    dec = "ssn::decompress_mfma_bf16<2, true, 0, 64, 1, 8, true, false, false, 1, 1, 1>(float const*)"
+    pg = "ssn::compress_rows_bf16<4, false, true, 8, 1, true, false, true, 4, false>(unsigned short const*)"
+    tab = pg
+    cp = "__amd_rocclr_copyBuffer"
+    fetch = [(cp, 1, 131072.0), (dec, 131072, 140000.0), (dec, 131072, 150000.0), (dec, 131072, 145000.0),
+             (pg, 131072, 133000.0), (tab, 524288, 526000.0), ("other_kernel", 64, 1.0)]
+    write = [(cp, 1, 262144.0), (dec, 131072, 262144.0), (dec, 131072, 262144.0), (dec, 131072, 262144.0),
+             (pg, 131072, 7000.0), (tab, 524288, 32768.0), ("other_kernel", 64, 1.0)]
+    paths = []
+    for name, rows, counter in (("f.csv", fetch, "FETCH_SIZE"), ("w.csv", write, "WRITE_SIZE")):
+        p = tmp_path / name
+        with open(p, "w", newline="") as f:
+            w = csv.writer(f)
+            w.writerow(cols)
+            for i, (k, g, v) in enumerate(rows):
+                w.writerow([i, g, k, counter, v])
+        paths.append(str(p))
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    bench.summarize_traffic(*paths)
+    t = json.load(open(tmp_path / "traffic.json"))
+    assert t["kernel_source_hash"] == bench.kernel_source_hash()
+    assert abs(t["calibration"]["fetch_scale"] - 2.0) < 1e-9
+    assert abs(t["calibration"]["write_scale"] - 1.0) < 1e-9
+    d = t["kernels"]["decompress"]
+    assert d["read_bytes"] == int(145000.0 * 1024 * 2.0) and d["write_bytes"] == 262144 * 1024
+    assert t["kernels"]["project_grad"]["grid"] == 131072
+    assert t["kernels"]["project_table"]["read_bytes"] == int(526000.0 * 1024 * 2.0)
+    assert set(t["kernels"]) == {"decompress", "project_grad", "project_table"}
