@@ -183,7 +183,8 @@ def summarize_traffic(fetch_csv: str, write_csv: str, calib_bytes: int = 256 << 
                 if op is None:
                     continue
                 vals.setdefault(op, []).append(float(r["Counter_Value"]))
-                names[op] = (r["Kernel_Name"].split("(")[0], grid)
+                name = r["Kernel_Name"]
+                names[op] = ((name[5:] if name.startswith("void ") else name).split("(")[0], grid)
         return vals, names
 
     fv, names = per_op(fetch_csv, "FETCH_SIZE")
@@ -219,26 +220,51 @@ def summarize_traffic(fetch_csv: str, write_csv: str, calib_bytes: int = 256 << 
     print("\n".join(rows))
 
 
+def kernel_op(kernel_name: str) -> str:
+    """The library operation a kernel of this build serves (for trace tables)."""
+    a = _template_args(kernel_name)
+    for key, op in (("project_weights", "project_weights"), ("factor_grad_reduce", "factor_grad sum"),
+                    ("factor_grad", "factor_grad"), ("reparam_backward_fused", "reparam backward (fused)"),
+                    ("sum_partials", "range sum"), ("sparta", "sparta"), ("check_ids", "check_ids"),
+                    ("pad_basis", "pad_basis"), ("copyBuffer", "device copy")):
+        if key in kernel_name:
+            return op
+    if "decompress" in kernel_name:
+        if len(a) > 7 and a[7] == "true":
+            return "factored_embedding"
+        return "decompress" if a[1:2] == ["true"] else "expand_grad"
+    if "compress_rows_bf16" in kernel_name or "compress_split_bf16" in kernel_name:
+        if a[1:2] == ["true"]:
+            return "compress"
+        has_p = a[-1] == "true" if "compress_rows" in kernel_name else a[2:3] == ["true"]
+        return "compress_projected" if has_p else "project_grad"
+    if "compress_generic" in kernel_name:
+        return "compress / project_grad (generic)"
+    return "other"
+
+
 def summarize_trace(trace_csv: str):
-    """Markdown table of a rocprofv3 kernel trace: one row per kernel and 2-D
-    grid, sorted by total time."""
+    """Markdown table of a rocprofv3 kernel trace: one row per kernel and
+    grid (x, or x by y), sorted by total time; kernels outside this library
+    (torch's input generation and copies) are left out."""
     import csv
-    import statistics
-    groups = {}
+    groups, total = {}, 0.0
     with open(trace_csv) as f:
         for r in csv.DictReader(f):
+            us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            total += us
             name = r["Kernel_Name"]
             name = (name[5:] if name.startswith("void ") else name).split("(")[0]
-            key = (name, f"{r['Grid_Size_X']} x {r['Grid_Size_Y']}",
-                   r["Workgroup_Size_X"], r["VGPR_Count"], r["LDS_Block_Size"])
-            us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-            groups.setdefault(key, []).append(us)
-    print("| kernel | grid (threads) | block | VGPR | LDS B | calls | median µs | mean µs |")
+            if not name.startswith("ssn::"):
+                continue
+            gy = r["Grid_Size_Y"]
+            grid = r["Grid_Size_X"] if gy == "1" else f"{r['Grid_Size_X']}x{gy}"
+            groups.setdefault((name, grid), []).append(us)
+    print("| kernel | op | grid (threads, x or x by y) | calls | avg us | min us | max us | % time |")
     print("|---|---|---|---|---|---|---|---|")
-    for key, ts in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
-        name, grid, block, vgpr, lds = key
-        print(f"| `{name}` | {grid} | {block} | {vgpr} | {lds} | {len(ts)} | "
-              f"{statistics.median(ts):.1f} | {statistics.mean(ts):.1f} |")
+    for (name, grid), ts in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        print(f"| `{name}` | {kernel_op(name)} | {grid} | {len(ts)} | {sum(ts) / len(ts):.1f} | "
+              f"{min(ts):.1f} | {max(ts):.1f} | {100 * sum(ts) / total:.2f} |")
 
 
 def cpu_model() -> str:
