@@ -62,7 +62,7 @@ def kernel_source_hash() -> str:
 def parse_args():
     p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--steps", type=int, default=400)
     p.add_argument("--warmup", type=int, default=200,
                    help="untimed steps first (the GPU's clocks settle after ~30 ms of sustained load)")
     p.add_argument("--settle-seconds", type=float, default=3.0,

@@ -566,7 +566,7 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
   const int lane = tid & 63, wave = tid >> 6;
   const int n16 = lane & 15, g = lane >> 4;
   // wave = part * TW + token tile: DSPLIT parts of d run side by side
-  const int part = wave / TW;
+  const int part = DSPLIT == 1 ? 0 : wave / TW;
   const int64_t tok0 = (int64_t)blockIdx.x * (16 * TW) + (wave % TW) * 16;
 
   // Z^T B fragments of this wave's 16 tokens.  Tokens past N take row N - 1
@@ -630,23 +630,39 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
     erow[q] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * ec : nullptr;
   }
 
-  // U staging: thread tid stages fragments of part tid/PT; fragment
-  // f = tid%PT + PT*q -> tile f/(KS2*64), K step (f/64)%KS2, lane position
-  // f%64 = 16*g' + m: row 16*tile + m, columns 32*s + 8*g'.  Threads past
-  // the last fragment load fragment FR - 1 again and do not store it, and
-  // columns past k load column 0 and store zeros, so that the loads, too,
-  // are unconditional.
-  const int spart = tid / PT, stid = tid % PT;
-  int srow[FPT], scol[FPT];
+  // U staging: thread tid stages fragments of part tid/PT.  Fragment f ->
+  // tile f/(KS2*64), K step (f/64)%KS2, lane position f%64 = 16*g' + m: row
+  // 16*tile + m, columns 32*s + 8*g'.
+  //  KM == 0 (k == 32*KS2): a chunk's 64 rows are one contiguous span of
+  //    64*k elements, so thread piece p = tid%PT + PT*q loads the 16 bytes at
+  //    8p of the span (a wave's load covers 1 KB of whole lines) and stores
+  //    them to the fragment that holds them (row p/(k/8), 8-column group
+  //    p%(k/8)).  Loading each fragment where it sits in U instead (16 rows
+  //    x 64 B per wave instruction) measured 6 % slower (8B-stage decompress).
+  //  otherwise thread piece p is fragment p itself, loaded from its row.
+  // Threads past the last fragment load fragment FR - 1 again and do not
+  // store it, and columns past k load column 0 and store zeros, so that the
+  // loads, too, are unconditional.
+  const int spart = DSPLIT == 1 ? 0 : tid / PT, stid = DSPLIT == 1 ? tid : tid % PT;
+  int srow[FPT], scol[FPT], sdst[FPT];
   bool son[FPT];
 #pragma unroll
   for (int q = 0; q < FPT; ++q) {
     const int f0 = stid + PT * q;
-    son[q] = f0 < FR;
+    son[q] = FR % PT == 0 || f0 < FR;          // compile-time when every thread stores
     const int f = son[q] ? f0 : FR - 1;
-    const int l = f & 63;
-    srow[q] = 16 * (f / (KS2 * kWave)) + (l & 15);
-    scol[q] = 32 * ((f / kWave) % KS2) + 8 * (l >> 4);
+    if constexpr (KM == 0) {
+      constexpr int GPR = 4 * KS2;                 // 8-column groups per row
+      const int r = f / GPR, cg = f % GPR;
+      srow[q] = r;
+      scol[q] = 8 * cg;
+      sdst[q] = ((r >> 4) * KS2 + (cg >> 2)) * kWave + 16 * (cg & 3) + (r & 15);
+    } else {
+      const int l = f & 63;
+      srow[q] = 16 * (f / (KS2 * kWave)) + (l & 15);
+      scol[q] = 32 * ((f / kWave) % KS2) + 8 * (l >> 4);
+      sdst[q] = f;
+    }
   }
   // U fragments travel as 16-byte pieces, or (KM == 2) as unaligned windows
   // that are realigned when they are stored to LDS.  Two register sets:
@@ -680,7 +696,7 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
                           : u32x4{0u, 0u, 0u, 0u};
         else
           v = (KFULL32 || scol[q] < k) ? u[q] : u32x4{0u, 0u, 0u, 0u};
-        ufr[buf][spart * FR + stid + PT * q] = v;
+        ufr[buf][spart * FR + sdst[q]] = v;
       }
   };
   // E rows of chunk j travel in ring slot j % (PF + 1), PF chunks ahead.

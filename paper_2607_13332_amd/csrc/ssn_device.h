@@ -20,9 +20,13 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
-// Two floats -> one dword of packed bf16 (lo in bits 0..15).
+// Two floats -> one dword of packed bf16 (lo in bits 0..15), each rounded to
+// nearest even: one two-source v_cvt_pk_bf16_f32 (the scalar form above
+// costs two conversions plus a shift and an or per pair).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // Low / high bf16 of a packed dword, widened to float.
