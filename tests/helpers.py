@@ -131,3 +131,20 @@ def mag_reparam_grad_input(G, Zp, U):
 
 def mag_reparam_grad_factor(H, G, U):
     return O.reparam_grad_factor(absval(H), absval(G), absval(U)), U.shape[0] + H.shape[0], True
+
+
+def check(name, got, ref, dtype, kind, mag=None):
+    """Relative Frobenius error against the parity bar and the design bound;
+    with `mag` = (M, L, split) also every element against its own bound
+    (helpers.elementwise_bound), so that one wrong element cannot hide in
+    the norm of a large output."""
+    err = rel(got, ref)
+    q = None
+    if mag is not None:
+        M, L, split = mag
+        q = check_elementwise(name, got, ref, M, L, split, out_bf16=(kind == "bf16out"))
+    print(f"[parity] {name}: rel={err:.3e}" + ("" if q is None else f" max|err|/bound={q:.3f}"),
+          flush=True)
+    assert err <= TOL[dtype], f"{name}: rel {err:.3e} above the parity bar {TOL[dtype]}"
+    assert err <= DESIGN[(dtype, kind)], f"{name}: rel {err:.3e} above design bound"
+    return err

@@ -9,13 +9,12 @@ import numpy as np
 import pytest
 import torch
 
-from helpers import (mag_compress, mag_decompress, mag_project, mag_reparam_forward,
+from helpers import (check, mag_compress, mag_decompress, mag_project, mag_reparam_forward,
                      mag_reparam_grad_factor, mag_reparam_grad_input, mag_weights, rel,
                      sample_rows)
 from oracle import ssn_oracle as O
 from paper_2607_13332_amd import inputs as I
 from paper_2607_13332_amd import ssn
-from test_gpu_parity import check
 
 pytestmark = pytest.mark.gpu
 

@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 import torch
 
-from helpers import (DESIGN, TOL, check_elementwise, mag_compress, mag_decompress, mag_project,
+from helpers import (DESIGN, TOL, check, check_elementwise, mag_compress, mag_decompress, mag_project,
                      mag_reparam_forward, mag_reparam_grad_factor, mag_reparam_grad_input,
                      mag_weights, rand_coords, rel, sample_rows, structured_inputs)
 from oracle import ssn_oracle as O
@@ -30,23 +30,6 @@ def dev(a, dtype):
 
 def host(t):
     return I.to_host(t)
-
-
-def check(name, got, ref, dtype, kind, mag=None):
-    """Relative Frobenius error against the parity bar and the design bound;
-    with `mag` = (M, L, split) also every element against its own bound
-    (helpers.elementwise_bound), so that one wrong element cannot hide in
-    the norm of a large output."""
-    err = rel(got, ref)
-    q = None
-    if mag is not None:
-        M, L, split = mag
-        q = check_elementwise(name, got, ref, M, L, split, out_bf16=(kind == "bf16out"))
-    print(f"[parity] {name}: rel={err:.3e}" + ("" if q is None else f" max|err|/bound={q:.3f}"),
-          flush=True)
-    assert err <= TOL[dtype], f"{name}: rel {err:.3e} above the parity bar {TOL[dtype]}"
-    assert err <= DESIGN[(dtype, kind)], f"{name}: rel {err:.3e} above design bound"
-    return err
 
 
 def test_library_is_the_in_tree_build():
