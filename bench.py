@@ -91,9 +91,14 @@ def parse_args():
                    help="no GPU work: turn the counter_collection.csv files of a rocprofv3 "
                         "--pmc FETCH_SIZE run and a --pmc WRITE_SIZE run of this bench "
                         "(with --copy-calib 256) into profiles/traffic.json and print the table")
+    p.add_argument("--summarize-counters", nargs="+", metavar="COUNTER_CSV", default=None,
+                   help="no GPU work: per-kernel table (median per dispatch of every counter) of "
+                        "the counter_collection.csv files of rocprofv3 --pmc runs of this bench; "
+                        "FETCH_SIZE / WRITE_SIZE are scaled to bytes by the device copy that "
+                        "--copy-calib MIB ran in the same process")
     p.add_argument("--summarize-trace", metavar="TRACE_CSV", default=None,
-                   help="no GPU work: per-kernel table (grid, block, registers, LDS, calls, "
-                        "median / mean us) of a rocprofv3 --kernel-trace csv")
+                   help="no GPU work: per-kernel table (grid, calls, average / min / max us, "
+                        "share of the traced time) of a rocprofv3 --kernel-trace csv")
     p.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                    help="before the timed region, run a plain device copy of MIB MiB three times "
                         "(a known-size kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE); "
@@ -218,6 +223,82 @@ def summarize_traffic(fetch_csv: str, write_csv: str, calib_bytes: int = 256 << 
           "scaled MB written | total MB |")
     print("|---|---|---|---|---|---|---|---|---|")
     print("\n".join(rows))
+
+
+def summarize_counters(paths, calib_mib: int = 256):
+    """Markdown table of rocprofv3 --pmc runs of this bench: one row per
+    kernel of this library and grid, the median per dispatch of every
+    counter collected.  FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are
+    scaled to bytes by what the same counter read for the plain device copy
+    of calib_mib MiB that --copy-calib runs in each process (the copy
+    dispatches of the largest grid in that file); the L2 hit share is
+    TCC_HIT_sum / (TCC_HIT_sum + TCC_MISS_sum) where both were collected."""
+    import csv
+    import statistics
+
+    def short(name):
+        return (name[5:] if name.startswith("void ") else name).split("(")[0]
+
+    rows, counters, scale = {}, [], {}
+    for path in paths:
+        copies, recs = {}, []
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                name, c = short(r["Kernel_Name"]), r["Counter_Name"]
+                key = (r["Dispatch_Id"], c)
+                if "copyBuffer" in name:
+                    copies.setdefault(int(r["Grid_Size"]), {})[key] = float(r["Counter_Value"])
+                elif name.startswith("ssn::"):
+                    recs.append((name, int(r["Grid_Size"]), key, c, float(r["Counter_Value"])))
+        if copies:
+            big = copies[max(copies)]
+            for c in ("FETCH_SIZE", "WRITE_SIZE"):
+                v = [x for (_, cc), x in big.items() if cc == c]
+                if v and statistics.median(v) > 0:
+                    scale[(path, c)] = calib_mib * 1024.0 / statistics.median(v)
+        for name, grid, key, c, v in recs:
+            if c not in counters:
+                counters.append(c)
+            rows.setdefault((name, grid), {}).setdefault(c, {})[(path,) + key] = v
+
+    def med(ent, c):
+        return statistics.median(ent[c].values()) if c in ent else None
+
+    def scaled(ent, c):
+        # bytes per dispatch: each run's median scaled by that run's copy
+        per_run = {}
+        for (path, _, _), v in ent.get(c, {}).items():
+            per_run.setdefault(path, []).append(v)
+        if not per_run or any((p, c) not in scale for p in per_run):
+            return None
+        return statistics.median([statistics.median(v) * 1024.0 * scale[(p, c)]
+                                  for p, v in per_run.items()])
+
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        fs = sorted({round(s, 3) for (p, cc), s in scale.items() if cc == c})
+        if fs:
+            print(f"{c} scale(s) from the {calib_mib} MiB copy: {', '.join(map(str, fs))}")
+    has_bytes = any(c in counters for c in ("FETCH_SIZE", "WRITE_SIZE"))
+    has_l2 = "TCC_HIT_sum" in counters and "TCC_MISS_sum" in counters
+    head = ["kernel", "op", "grid (threads)", "dispatches"] + counters
+    if has_bytes:
+        head += ["scaled MB read", "scaled MB written", "total MB"]
+    if has_l2:
+        head += ["L2 hit %"]
+    print("| " + " | ".join(head) + " |")
+    print("|" + "---|" * len(head))
+    for (name, grid), ent in sorted(rows.items(), key=lambda kv: (kernel_op(kv[0][0]), kv[0])):
+        n = max(len(v) for v in ent.values())
+        cells = [f"`{name}`", kernel_op(name), str(grid), str(n)]
+        cells += ["" if med(ent, c) is None else f"{med(ent, c):.6g}" for c in counters]
+        if has_bytes:
+            rb, wb = scaled(ent, "FETCH_SIZE"), scaled(ent, "WRITE_SIZE")
+            cells += ["" if rb is None else f"{rb / 1e6:.1f}", "" if wb is None else f"{wb / 1e6:.1f}",
+                      "" if rb is None or wb is None else f"{(rb + wb) / 1e6:.1f}"]
+        if has_l2:
+            h, m = med(ent, "TCC_HIT_sum"), med(ent, "TCC_MISS_sum")
+            cells += ["" if h is None or m is None or h + m == 0 else f"{100 * h / (h + m):.1f}"]
+        print("| " + " | ".join(cells) + " |")
 
 
 def kernel_op(kernel_name: str) -> str:
@@ -722,6 +803,9 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, args.copy_calib or 256)
         return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "

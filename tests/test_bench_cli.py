@@ -59,3 +59,43 @@ def test_traffic_summary_from_counter_files(tmp_path, monkeypatch):
     assert t["kernels"]["project_grad"]["grid"] == 131072
     assert t["kernels"]["project_table"]["read_bytes"] == int(526000.0 * 1024 * 2.0)
     assert set(t["kernels"]) == {"decompress", "project_grad", "project_table"}
+
+
+def test_counter_summary_table(tmp_path, capsys):
+    """The general counter table: medians per kernel and grid, FETCH_SIZE /
+    WRITE_SIZE scaled by the largest copy of each file (small copies of the
+    same run are ignored), L2 hit share from TCC_HIT_sum / TCC_MISS_sum, and
+    kernels outside the library left out."""
+    import csv
+    import bench
+    cols = ["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    sp = "void ssn::sparta_copy4(float const*, float*, long)"
+    cp = "__amd_rocclr_copyBuffer"
+
+    def write(name, rows):
+        p = tmp_path / name
+        with open(p, "w", newline="") as f:
+            w = csv.writer(f)
+            w.writerow(cols)
+            for i, (k, g, c, v) in enumerate(rows):
+                w.writerow([i, g, k, c, v])
+        return str(p)
+
+    fetch = write("f.csv", [(cp, 131072, "FETCH_SIZE", 131072.0), (cp, 512, "FETCH_SIZE", 2.0),
+                            (cp, 512, "FETCH_SIZE", 2.0), (cp, 512, "FETCH_SIZE", 2.0),
+                            (sp, 1000, "FETCH_SIZE", 30000.0), (sp, 1000, "FETCH_SIZE", 31000.0),
+                            (sp, 1000, "FETCH_SIZE", 32000.0), ("torch_kernel", 64, "FETCH_SIZE", 5.0)])
+    wr = write("w.csv", [(cp, 131072, "WRITE_SIZE", 262144.0), (sp, 1000, "WRITE_SIZE", 62500.0)])
+    l2 = write("l.csv", [(sp, 1000, "TCC_HIT_sum", 300.0), (sp, 1000, "TCC_MISS_sum", 100.0)])
+    bench.summarize_counters([fetch, wr, l2], 256)
+    out = capsys.readouterr().out
+    rows = [r for r in out.splitlines() if r.startswith("| `")]
+    assert len(rows) == 1 and "torch_kernel" not in out
+    cells = [c.strip() for c in rows[0].strip("|").split("|")]
+    head = [c.strip() for c in [r for r in out.splitlines() if r.startswith("| kernel")][0].strip("|").split("|")]
+    got = dict(zip(head, cells))
+    assert got["op"] == "sparta" and got["grid (threads)"] == "1000" and got["dispatches"] == "3"
+    assert got["FETCH_SIZE"] == "31000" and got["WRITE_SIZE"] == "62500"
+    assert got["scaled MB read"] == f"{31000 * 1024 * 2.0 / 1e6:.1f}"
+    assert got["scaled MB written"] == f"{62500 * 1024 * 1.0 / 1e6:.1f}"
+    assert got["L2 hit %"] == "75.0"
