@@ -86,7 +86,11 @@ def parse_args():
                    help="profiling aid: run only this section and print its JSON (no headline; "
                         "keeps its kernels apart from the codec's in a kernel trace)")
     p.add_argument("--sweep-tokens", type=str, default="",
-                   help="with --only sweep / paper: comma-separated token counts to keep")
+                   help="with --only sweep / paper / reparam: comma-separated token counts to keep")
+    p.add_argument("--select", type=str, default="",
+                   help="with --only sweep / paper / reparam: comma-separated workload names to "
+                        "keep (e.g. paper8b_b1,paper8b_b3), so that launches of equal total grid "
+                        "from different workloads stay apart in a counter run")
     p.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"), default=None,
                    help="no GPU work: turn the counter_collection.csv files of a rocprofv3 "
                         "--pmc FETCH_SIZE run and a --pmc WRITE_SIZE run of this bench "
@@ -779,20 +783,25 @@ def copy_rate(dev, mib: int = 512, reps: int = 20) -> float:
 def run_section(name: str, args, dev):
     from paper_2607_13332_amd import inputs as I
     keep = {int(x) for x in args.sweep_tokens.split(",") if x.strip()}
+    names = {x.strip() for x in args.select.split(",") if x.strip()}
+
+    def kept(nm, n):
+        return (not keep or n in keep) and (not names or nm in names)
+
     if name in ("sweep", "paper"):
         cfgs = ([c for c in I.sweep_configs() if c.k == 64] if name == "sweep" else I.paper_configs())
         return {c.name: time_codec_config(c, max(10, args.steps // 2), args.warmup, dev)
-                for c in cfgs if not keep or c.N in keep}
+                for c in cfgs if kept(c.name, c.N)}
     if name == "weights":
         return {wc.name: time_weights(wc, args.steps, dev)
                 for wc in (I.WEIGHTS, I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B)}
     if name == "reparam":
-        return {
-            "paper8b_mlp_out": time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2), dev),
-            "paper8b_mlp_out_padded64": time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2),
-                                                     dev, pad_to=64),
-            "stage8b_mlp_out": time_reparam(32768, 14336, 4096, 64, max(10, args.steps // 2), dev),
-        }
+        steps = max(10, args.steps // 2)
+        shapes = (("paper8b_mlp_out", (4096, 18432, 5120, 51), {}),
+                  ("paper8b_mlp_out_padded64", (4096, 18432, 5120, 51), {"pad_to": 64}),
+                  ("stage8b_mlp_out", (32768, 14336, 4096, 64), {}))
+        return {nm: time_reparam(*shape, steps, dev, **kw) for nm, shape, kw in shapes
+                if kept(nm, shape[0])}
     return time_sparta(I.SPARTA_BLOCK8B, args.steps, dev)
 
 
