@@ -6,7 +6,7 @@
  * token, the k coordinates of its residual-stream activation in a fixed
  * orthonormal basis U (d x k) after subtracting the fixed token embedding
  * E[ids] that both sides of the boundary hold (Eq. (2)); the receiver rebuilds
- * the activation with U^T; gradients travel back through the same compression;
+ * the activation with U^T; gradients travel back through the same projection;
  * and the original SSN re-projects its full-width output projections into
  * span(U) after every optimizer step.  The data-parallel side (section 4.2)
  * adds the per-GPU steps of sparse weight averaging with the delta rule.
@@ -138,8 +138,8 @@ ssn_status_t ssn_decompress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, 
 ssn_status_t ssn_check_ids(int64_t N, int64_t V, const int32_t *ids, int64_t *bad, void *stream);
 
 /*
- * ssn_project_grad -- backward compression, section 4.1 ("the backward pass
- * uses the same compression"): the receiver sends G_Z = G . U back.
+ * ssn_project_grad -- backward compression, section 4.1 (gradients cross the
+ * boundary through the same projection): the receiver sends G_Z = G . U back.
  *   G  [N, d] dtype      gradient w.r.t. the decompressed activation
  *   U  [d, k] dtype
  *   GZ [N, k] float32    output

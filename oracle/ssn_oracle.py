@@ -15,9 +15,9 @@ with Reparameterized SSNs"):
   here; Pluralis-8B uses rotary positions, so there is no additive positional
   term) and sends the k coordinates (X - E[ids]) U_k per token.
 * The receiver rebuilds the activation with U_k^T: X' = E[ids] + Z U_k^T.
-* The backward pass uses the same compression: the gradient arriving at the
-  receiver's input is sent back as G U_k, and the sender expands it to
-  G_Z U_k^T (chain rule through Eq. (2)).
+* Gradients cross the boundary through the same projection: the gradient
+  arriving at the receiver's input is sent back as G U_k, and the sender
+  expands it to G_Z U_k^T (chain rule through Eq. (2)).
 * The original SSN keeps full-width output projections and, after every
   optimizer step, projects them back into the subspace.  With PyTorch's
   [out = d, in = n] weight layout the constrained index is the row index, so

@@ -1,8 +1,8 @@
 // Stage-boundary codec kernels: compress / gradient projection (contract over
 // d) and decompress / gradient expansion (contract over k).
 //
-// Paper: section 4.1, Eq. (2) -- Z = (X - E[ids]) U, reconstruction with U^T,
-// and "the backward pass uses the same compression" (G_Z = G U at the
+// Paper: section 4.1, Eq. (2) -- Z = (X - E[ids]) U, reconstruction with U^T;
+// gradients cross the boundary through the same projection (G_Z = G U at the
 // receiver, G_Z U^T at the sender).
 #include "ssn_device.h"
 #include "ssn_launch.h"
