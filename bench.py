@@ -51,11 +51,22 @@ KERNEL_SOURCES = ["paper_2607_13332_amd/csrc/codec_kernels.hip",
                   "paper_2607_13332_amd/csrc/ssn_device.h"]
 
 
+def _code_only(src: str) -> str:
+    """C++ source without comments and whitespace (the kernel sources hold no
+    string literals that contain comment markers)."""
+    import re
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return "".join(src.split())
+
+
 def kernel_source_hash() -> str:
+    """Hash of the kernel sources' code (comments and layout do not change
+    what the counters measure)."""
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 
