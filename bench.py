@@ -45,6 +45,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_2607_13332_amd/csrc/codec_kernels.hip",
+                  "paper_2607_13332_amd/csrc/f32_kernels.hip",
                   "paper_2607_13332_amd/csrc/weights_kernels.hip",
                   "paper_2607_13332_amd/csrc/reparam_kernels.hip",
                   "paper_2607_13332_amd/csrc/sparta_kernels.hip",

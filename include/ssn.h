@@ -82,9 +82,12 @@ const char *ssn_status_string(int status);
  * unknown op.  Pure host function (no HIP call), for tests and reports.
  * The MFMA kernels cover bf16 with k <= 128 and: compress / project_grad /
  * compress_projected / decompress d % 128 == 0; project_weights d % 32 == 0
- * (and, when k % 8 != 0, every n % 8 == 0).  Everything else runs the
- * generic kernels (fp32 arithmetic, one wavefront per token / one block per
- * column).
+ * (and, when k % 8 != 0, every n % 8 == 0); and float32 storage for
+ * compress / project_grad / compress_projected / decompress with d % 64 == 0
+ * and U rows of 16, 32, .., 128 floats (k, or ldu of a zero-padded basis),
+ * on float32 MFMA (float32 products and accumulation).  Everything else runs
+ * the generic kernels (fp32 arithmetic, one wavefront per token / one block
+ * per column).
  */
 const char *ssn_kernel_family(ssn_op_t op, ssn_dtype_t dtype, int64_t d, int64_t k);
 
@@ -97,9 +100,10 @@ const char *ssn_kernel_family(ssn_op_t op, ssn_dtype_t dtype, int64_t d, int64_t
  *   U   [d, k]  dtype      orthonormal basis (used as stored)
  *   Z   [N, k]  float32    output coordinates
  * Requires 1 <= k <= d, V >= 1.  The subtraction is distributed over the
- * contraction on the MFMA path (X.U and E[ids].U accumulate by identical
- * fp32 sequences and are subtracted once); the generic path subtracts in fp32
- * first.  On both, compress(E[ids]) is exactly zero.
+ * contraction on the bf16 MFMA path (X.U and E[ids].U accumulate by
+ * identical fp32 sequences and are subtracted once); the float32 and generic
+ * paths subtract in fp32 first.  On all of them compress(E[ids]) is exactly
+ * zero.
  */
 ssn_status_t ssn_compress(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k, int64_t V,
                           const void *X, const int32_t *ids, const void *E, const void *U,

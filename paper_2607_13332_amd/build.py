@@ -19,8 +19,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libssn.so")
-SOURCES = ["ssn_api.hip", "noalloc.hip", "codec_kernels.hip", "weights_kernels.hip",
-           "reparam_kernels.hip", "sparta_kernels.hip"]
+SOURCES = ["ssn_api.hip", "noalloc.hip", "codec_kernels.hip", "f32_kernels.hip",
+           "weights_kernels.hip", "reparam_kernels.hip", "sparta_kernels.hip"]
 ARCH = "gfx950"
 
 

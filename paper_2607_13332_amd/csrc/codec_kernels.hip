@@ -826,8 +826,8 @@ __global__ __launch_bounds__(64 * TW * DSPLIT) void decompress_mfma_bf16(
 
 // ===========================================================================
 // Generic kernels: any storage dtype, any d and k.  One wave per token,
-// fp32 arithmetic, wavefront reductions.  Used for fp32 storage and for shapes
-// the MFMA kernels do not tile.
+// fp32 arithmetic, wavefront reductions.  Used for the shapes the MFMA
+// kernels (bf16 here, float32 in f32_kernels.hip) do not tile.
 // ===========================================================================
 template <typename T, bool HAS_E, bool HAS_P = false>
 __global__ __launch_bounds__(256) void compress_generic(
@@ -1158,6 +1158,9 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
   const int kz = (int)(kz64 < 128 ? kz64 : 128);   // the MFMA paths take k <= 128
   const bool has_e = (E != nullptr), has_p = (P != nullptr);
   const void* zout = Zb ? (const void*)Zb : (const void*)Z;
+  if (dtype == kF32 && f32_uses_mfma(d, k) && al16(X) && al16(U) && (!has_e || al16(E)))
+    return launch_compress_f32(N, d, k, V, (const float*)X, ids, (const float*)E, (const float*)U, Z,
+                               P, st, Zb, kz);
   if (compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(zout) && (!has_e || al16(E)) &&
       (!has_p || al16(P))) {
     if (compress_uses_split(N, d, k, has_e)) {
@@ -1245,19 +1248,14 @@ hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, con
 // each block's chunk count is even.  The activation rows are written with
 // non-temporal stores (streamed out instead of parked dirty in the caches,
 // where they slowed the next kernel's reads).
-template <int KS2, bool HAS_E, int KM, bool GZ>
-static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const float* Zc,
-                                       const int32_t* ids, const void* E, const void* U, void* Y,
-                                       hipStream_t st, const uint16_t* Zb, int kz) {
-  constexpr int TW = 8;
-  const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
+// Ranges of d (grid.y) for `blocks` token blocks over `chunks` chunks of d:
+// 1 when the blocks alone reach one per compute unit; else the smallest
+// divisor of the chunk count that leaves every block at least two chunks and
+// fills at least 90 % of the blocks' last round, else the smallest that
+// reaches one block per unit (N = 12288, d = 5120, k = 51: 96 blocks in 5
+// ranges 57.9 us, in 4 ranges 64.3 us).
+int decompress_grid_split(int64_t blocks, int chunks) {
   const int64_t cus = device_cu_count();
-  const int chunks = d / kDecompressDC;
-  // with fewer blocks than compute units: the smallest split of d (a divisor
-  // of the chunk count, at least two chunks per block) whose blocks fill at
-  // least 90 % of their last round, else the smallest that reaches one block
-  // per unit (N = 12288, d = 5120, k = 51: 96 blocks in 5 ranges 57.9 us, in
-  // 4 ranges 64.3 us)
   int gy = 1;
   if (blocks < cus) {
     int first = 0;
@@ -1272,6 +1270,17 @@ static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const
     }
     if (gy == 1) gy = first > 0 ? first : 1;
   }
+  return gy;
+}
+
+template <int KS2, bool HAS_E, int KM, bool GZ>
+static hipError_t launch_decompress_km(int64_t N, int d, int k, int64_t V, const float* Zc,
+                                       const int32_t* ids, const void* E, const void* U, void* Y,
+                                       hipStream_t st, const uint16_t* Zb, int kz) {
+  constexpr int TW = 8;
+  const int64_t blocks = (N + 16 * TW - 1) / (16 * TW);
+  const int chunks = d / kDecompressDC;
+  const int gy = decompress_grid_split(blocks, chunks);
   const dim3 grid((unsigned)blocks, (unsigned)gy);
   if (!HAS_E && (chunks / gy) % 2 == 0)
     hipLaunchKernelGGL((decompress_mfma_bf16<KS2, HAS_E, KM, kDecompressDC, 1, TW, true, GZ, false,
@@ -1323,6 +1332,9 @@ hipError_t launch_decompress(int dtype, int64_t N, int64_t d, int64_t k, int64_t
   const int kz = (int)(kz64 < 128 ? kz64 : 128);   // the MFMA paths take k <= 128
   const bool has_e = (E != nullptr);
   const void* zin = Zb ? (const void*)Zb : (const void*)Zc;
+  if (dtype == kF32 && f32_uses_mfma(d, k) && al16(U) && al16(Y) && (!has_e || al16(E)))
+    return launch_decompress_f32(N, d, k, V, Zc, ids, (const float*)E, (const float*)U, (float*)Y,
+                                 gather_z, st, Zb, kz);
   if (decompress_uses_mfma(dtype, d, k) && al16(zin) && al16(U) && al16(Y) && (!has_e || al16(E))) {
     if (has_e) return launch_decompress_mfma<true, false>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb, kz);
     if (gather_z) return launch_decompress_mfma<false, true>(N, (int)d, (int)k, V, Zc, ids, E, U, Y, st, Zb, kz);

@@ -18,6 +18,20 @@ int device_cu_count();
 bool compress_uses_mfma(int dtype, int64_t d, int64_t k);
 bool decompress_uses_mfma(int dtype, int64_t d, int64_t k);
 bool weights_use_mfma(int dtype, int64_t d, int64_t k);
+// float32 storage on the matrix cores (v_mfma_f32_16x16x4_f32): d a multiple
+// of 64 and U rows of k = 16, 32, .., 128 floats (a zero-padded basis for
+// other ranks).
+bool f32_uses_mfma(int64_t d, int64_t k);
+// Ranges of d (grid.y) for `blocks` token blocks of the decompress kernels.
+int decompress_grid_split(int64_t blocks, int chunks);
+// float32 forms of launch_compress / launch_decompress (same arguments;
+// only where f32_uses_mfma holds and X, E, U, Y are 16-byte aligned).
+hipError_t launch_compress_f32(int64_t N, int64_t d, int64_t k, int64_t V, const float* X,
+                               const int32_t* ids, const float* E, const float* U, float* Z,
+                               const float* P, hipStream_t st, uint16_t* Zb, int kz);
+hipError_t launch_decompress_f32(int64_t N, int64_t d, int64_t k, int64_t V, const float* Z,
+                                 const int32_t* ids, const float* E, const float* U, float* Y,
+                                 bool gather_z, hipStream_t st, const uint16_t* Zb, int kz);
 
 // E non-NULL: Z = (X - E[ids]).U; P non-NULL: Z = X.U - P[ids]; neither: Z = X.U.
 // Zb non-NULL: the coordinates are written to Zb in bf16 (rounded to nearest

@@ -72,7 +72,14 @@ def test_kernel_family_rules(ssn):
     assert kf("project_weights", "f32", 4096, 64) == "generic"
     assert kf("compress_projected", "bf16", 4096, 64) == "mfma"
     assert kf("compress_projected", "bf16", 5120, 51) == "mfma"
-    assert kf("compress_projected", "f32", 4096, 64) == "generic"
+    # float32 storage: the matrix-core kernels where d is a multiple of 64 and
+    # U rows hold 16, 32, .., 128 floats; generic otherwise
+    assert kf("compress_projected", "f32", 4096, 64) == "mfma"
+    assert kf("compress", "f32", 5120, 16) == "mfma"
+    assert kf("decompress", "f32", 4096, 128) == "mfma"
+    assert kf("project_grad", "f32", 4096, 51) == "generic"
+    assert kf("decompress", "f32", 4096, 144) == "generic"
+    assert kf("decompress", "f32", 4100, 64) == "generic"
     assert ssn.lib().ssn_kernel_family(9, 1, 4096, 64) == b"invalid"
 
 

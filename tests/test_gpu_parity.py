@@ -8,6 +8,8 @@ its own bound.  The codec workloads are checked on every row (in blocks of
 4096); the weight and reparameterized workloads at full size on seeded
 column / row samples that the oracle computes directly.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -140,12 +142,32 @@ def _check_codec_rows(cfg, inp, out, rows, label):
     loc = np.arange(len(rows), dtype=np.int32)
     check(f"{cfg.name} compress{label}", host(out["Z"][r]), O.compress(Xs, loc, Es, Us), t, "f32out",
           mag_compress(Xs, loc, Es, Us))
-    check(f"{cfg.name} decompress{label}", host(out["Y"][r]), O.decompress(Zs, loc, Es, Us), t, "bf16out",
+    outkind = "bf16out" if t == "bf16" else "f32out_dec"
+    check(f"{cfg.name} decompress{label}", host(out["Y"][r]), O.decompress(Zs, loc, Es, Us), t, outkind,
           mag_decompress(Zs, loc, Es, Us))
     check(f"{cfg.name} project_grad{label}", host(out["GZ"][r]), O.project_grad(Gs, Us), t, "f32out",
           mag_project(Gs, Us))
-    check(f"{cfg.name} expand_grad{label}", host(out["GX"][r]), O.expand_grad(Zs, Us), t, "bf16out",
+    check(f"{cfg.name} expand_grad{label}", host(out["GX"][r]), O.expand_grad(Zs, Us), t, outkind,
           mag_decompress(Zs, None, None, Us))
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("N", [32768, 4100])
+def test_f32_storage_full_size_sampled(N):
+    """float32 storage at the 8B-stage shape (d = 4096, k = 64, V = 131072),
+    on the float32 matrix-core kernels: 8-wave compress blocks at N = 32768,
+    4-wave blocks and a split of d for decompress at N = 4100 (ragged).  All
+    four ops on seeded rows plus the first and last 64, against the oracle."""
+    cfg = dataclasses.replace(I.with_tokens(I.STAGE8B, N, seed=1094), name=f"stage8b_f32_n{N}",
+                              dtype="f32")
+    assert ssn.kernel_family("compress", "f32", cfg.d, cfg.k) == "mfma"
+    assert ssn.kernel_family("decompress", "f32", cfg.d, cfg.k) == "mfma"
+    inp, out = _codec_outputs(cfg)
+    rows = np.unique(np.concatenate([sample_rows(N, 512, cfg.seed), np.arange(64),
+                                     np.arange(N - 64, N)])).astype(np.int64)
+    _check_codec_rows(cfg, inp, out, rows, " sampled")
+    del inp, out
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.timeout(600)
@@ -613,7 +635,8 @@ def test_reparam_paper_shape_sampled(N, din, d, k):
 
 
 @pytest.mark.parametrize("N,d,k,V,dtype", [(300, 256, 16, 50, "bf16"), (4096, 5120, 51, 128256, "bf16"),
-                                          (100, 96, 7, 10, "f32")])
+                                          (100, 96, 7, 10, "f32"), (300, 256, 16, 50, "f32"),
+                                          (4100, 4096, 64, 1024, "f32")])
 def test_factored_embedding(N, d, k, V, dtype):
     seed = N + d + k
     r = np.random.default_rng(seed)
