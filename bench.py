@@ -16,7 +16,8 @@ compressed activations of a stage belong to different microbatches in a
 pipeline), so compress never finds the rows decompress just gathered in the
 caches.  Inputs are resident in HBM before the timed region starts.  The once-per-optimizer-step weight
 re-projection (4 layers x (4096x4096 + 4096x14336)) is timed separately and
-reported under "weights".  The same step with compress against the projected
+reported under "weights" (bf16 storage) and "weights_f32" (float32 master
+weights).  The same step with compress against the projected
 embedding table (Z = X U - (E U)[ids], table formed once outside the timed
 region) is timed separately and reported under "variants"; the headline value
 is the step with compress as written in Eq. (2).  The same step at the
@@ -43,6 +44,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+MFMA_F32_PEAK_TFLOPS = 157.3    # MI355X dense float32 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_2607_13332_amd/csrc/codec_kernels.hip",
                   "paper_2607_13332_amd/csrc/f32_kernels.hip",
@@ -417,16 +419,17 @@ def cpu_baseline(sample, cfg, seconds: float):
     return out
 
 
-def time_weights(wc, steps: int, dev):
-    """W <- U (U^T W) over one stage's output projections, one batched launch."""
+def time_weights(wc, steps: int, dev, dtype: str = "bf16"):
+    """W <- U (U^T W) over one stage's output projections, one batched launch,
+    in the storage dtype `dtype` (bf16, or float32 master weights)."""
     import torch
     from paper_2607_13332_amd import inputs as I
     from paper_2607_13332_amd import ssn
     Ws = []
     for layer in range(wc.layers):
         for j, (dd, n) in enumerate(wc.shapes):
-            Ws.append(I.weights_device(dd, n, wc.seed * 100 + 10 * layer + j, dev))
-    Uw = I.to_device(I.store(I.gaussian_orthonormal_basis(wc.d, wc.k, wc.seed), "bf16"), "bf16", dev)
+            Ws.append(I.weights_device(dd, n, wc.seed * 100 + 10 * layer + j, dev, dtype))
+    Uw = I.to_device(I.store(I.gaussian_orthonormal_basis(wc.d, wc.k, wc.seed), dtype), dtype, dev)
     # a few untimed calls (the matrices were just written by the generator);
     # long back-to-back runs of this kernel drift slower on the box (power
     # management), which a once-per-optimizer-step operation never sees
@@ -452,21 +455,23 @@ def time_weights(wc, steps: int, dev):
         torch.cuda.synchronize()
         iso.append(e0.elapsed_time(e1))
     iso_ms = sorted(iso)[len(iso) // 2]
-    wbytes = sum(2 * W.numel() * 2 for W in Ws) + wc.d * wc.k * 2
+    es = 2 if dtype == "bf16" else 4
+    mfma_peak = MFMA_BF16_PEAK_TFLOPS if dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
+    wbytes = sum(2 * W.numel() * es for W in Ws) + wc.d * wc.k * es
     wflops = sum(4.0 * wc.d * wc.k * W.shape[1] for W in Ws)
     shapes = " + ".join(f"{a}x{b}" for a, b in wc.shapes)
     out = {
-        "workload": f"W <- U(U^T W) for {wc.layers} layers x ({shapes}) bf16, k={wc.k}, one launch",
+        "workload": f"W <- U(U^T W) for {wc.layers} layers x ({shapes}) {dtype}, k={wc.k}, one launch",
         "ms": round(wms, 5),
         "algorithmic_GBps": round(wbytes / (wms * 1e-3) / 1e9, 1),
         "frac_hbm_peak": round(wbytes / (wms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "mfma_TFLOPs": round(wflops / (wms * 1e-3) / 1e12, 2),
-        "frac_mfma_peak": round(wflops / (wms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        "frac_mfma_peak": round(wflops / (wms * 1e-3) / 1e12 / mfma_peak, 4),
         "isolated_call": {"what": "median of 5 single calls, each after 20 ms of idle GPU",
                           "ms": round(iso_ms, 5),
                           "frac_hbm_peak": round(wbytes / (iso_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
     }
-    if wc.name == I.WEIGHTS.name:
+    if wc.name == I.WEIGHTS.name and dtype == "bf16":
         out["traffic"] = load_traffic("project_weights")
     if wc.k % 16 != 0:
         # U stored with zero columns up to whole 16-column tiles: the same
@@ -805,8 +810,9 @@ def run_section(name: str, args, dev):
         return {c.name: time_codec_config(c, max(10, args.steps // 2), args.warmup, dev)
                 for c in cfgs if kept(c.name, c.N)}
     if name == "weights":
-        return {wc.name: time_weights(wc, args.steps, dev)
-                for wc in (I.WEIGHTS, I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B)}
+        return {wc.name + ("" if dt == "bf16" else "_f32"): time_weights(wc, args.steps, dev, dt)
+                for wc in (I.WEIGHTS, I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B) for dt in ("bf16", "f32")
+                if not names or wc.name in names}
     if name == "reparam":
         steps = max(10, args.steps // 2)
         shapes = (("paper8b_mlp_out", (4096, 18432, 5120, 51), {}),
@@ -1105,6 +1111,7 @@ def main():
     # ---------------- weight re-projection (once per optimizer step) ----------------
     if not args.no_weights:
         result["weights"] = time_weights(I.WEIGHTS, args.steps, dev)
+        result["weights_f32"] = time_weights(I.WEIGHTS, args.steps, dev, "f32")
 
     # ---------------- sweep points at k = 64 (Zipf ids) ----------------
     if not args.no_sweep:

@@ -85,7 +85,8 @@ const char *ssn_status_string(int status);
  * (and, when k % 8 != 0, every n % 8 == 0); and float32 storage for
  * compress / project_grad / compress_projected / decompress with d % 64 == 0
  * and U rows of 16, 32, .., 128 floats (k, or ldu of a zero-padded basis),
- * on float32 MFMA (float32 products and accumulation).  Everything else runs
+ * and project_weights with d % 32 == 0, k <= 128 and every n % 4 == 0, on
+ * float32 MFMA (float32 products and accumulation).  Everything else runs
  * the generic kernels (fp32 arithmetic, one wavefront per token / one block
  * per column).
  */
@@ -262,7 +263,11 @@ ssn_status_t ssn_project_weights(ssn_dtype_t dtype, int64_t d, int64_t n, int64_
  * pipeline stage), in one launch.
  *   W[b] [d, n[b]] dtype, in place, for b in [0, count)
  *   W and n are HOST arrays of `count` entries; 1 <= count <= SSN_MAX_BATCH.
- * Matrices must not overlap each other.
+ * Matrices must not overlap each other.  With bf16 storage a matrix gets the
+ * same bits alone and in a batch.  The float32 kernel splits the sum over d
+ * between the waves that share a column tile, and that split follows the
+ * column partition of the launch (the total column count and the device's
+ * compute units), so there the two may differ in the last bits.
  */
 ssn_status_t ssn_project_weights_batched(ssn_dtype_t dtype, int64_t count, int64_t d,
                                          const int64_t *n, int64_t k, void *const *W,

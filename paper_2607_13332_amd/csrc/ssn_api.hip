@@ -67,7 +67,9 @@ const char* ssn_kernel_family(ssn_op_t op, ssn_dtype_t dtype, int64_t d, int64_t
     case SSN_OP_DECOMPRESS:
       mfma = ssn::decompress_uses_mfma(dtype, d, k) || (dtype == SSN_F32 && ssn::f32_uses_mfma(d, k));
       break;
-    case SSN_OP_PROJECT_WEIGHTS: mfma = ssn::weights_use_mfma(dtype, d, k); break;
+    case SSN_OP_PROJECT_WEIGHTS:
+      mfma = ssn::weights_use_mfma(dtype, d, k) || (dtype == SSN_F32 && ssn::weights_f32_uses_mfma(d, k));
+      break;
     default: return "invalid";
   }
   return mfma ? "mfma" : "generic";

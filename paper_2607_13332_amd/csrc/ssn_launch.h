@@ -22,6 +22,12 @@ bool weights_use_mfma(int dtype, int64_t d, int64_t k);
 // of 64 and U rows of k = 16, 32, .., 128 floats (a zero-padded basis for
 // other ranks).
 bool f32_uses_mfma(int64_t d, int64_t k);
+// float32 weight re-projection on the matrix cores: d a multiple of 32 and
+// k <= 128 (plus, checked by the launcher, every n a multiple of 4 and 16-byte
+// aligned U and W).
+bool weights_f32_uses_mfma(int64_t d, int64_t k);
+hipError_t launch_project_weights_f32(int count, int64_t d, const int64_t* n, int64_t k,
+                                      float* const* W, const float* U, hipStream_t st);
 // Ranges of d (grid.y) for `blocks` token blocks of the decompress kernels.
 int decompress_grid_split(int64_t blocks, int chunks);
 // float32 forms of launch_compress / launch_decompress (same arguments;

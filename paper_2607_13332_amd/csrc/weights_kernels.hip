@@ -598,7 +598,7 @@ static hipError_t launch_cols(const ColumnBatch& cb, int cus, const void* U, int
 hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t* n, int64_t k,
                                   void* const* W, const void* U, hipStream_t st) {
   bool aligned = (((uintptr_t)U & 15u) == 0);
-  bool cols8 = true;
+  bool cols8 = true, cols4 = true;
   // the MFMA kernels keep each matrix's row stride n in 32 bits; wider
   // matrices take the generic kernel, whose indexing is 64-bit throughout
   bool n32 = true;
@@ -606,9 +606,15 @@ hipError_t launch_project_weights(int dtype, int count, int64_t d, const int64_t
   for (int b = 0; b < count; ++b) {
     aligned = aligned && (((uintptr_t)W[b] & 15u) == 0);
     cols8 = cols8 && (n[b] % 8 == 0);
+    cols4 = cols4 && (n[b] % 4 == 0);
     n32 = n32 && n[b] <= INT32_MAX;
     panels += (n[b] + 63) / 64;
     tiles += (n[b] + 15) / 16;
+  }
+  if (dtype == kF32 && weights_f32_uses_mfma(d, k) && aligned && n32 && cols4 && tiles <= INT32_MAX / 2) {
+    float* Wf[kMaxBatch];
+    for (int b = 0; b < count; ++b) Wf[b] = (float*)W[b];
+    return launch_project_weights_f32(count, d, n, k, Wf, (const float*)U, st);
   }
   const bool mfma = weights_use_mfma(dtype, d, k) && aligned && n32;
   if (mfma && cols8 && tiles <= INT32_MAX / 2) {

@@ -15,6 +15,8 @@ int device_cu_count() { return 256; }
 bool compress_uses_mfma(int dtype, int64_t d, int64_t k) { return dtype == kBF16 && d % 128 == 0 && k <= 128; }
 bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) { return dtype == kBF16 && d % 128 == 0 && k <= 128; }
 bool weights_use_mfma(int dtype, int64_t d, int64_t k) { return dtype == kBF16 && d % 32 == 0 && k <= 128; }
+bool f32_uses_mfma(int64_t d, int64_t k) { return d % 64 == 0 && k % 16 == 0 && k <= 128; }
+bool weights_f32_uses_mfma(int64_t d, int64_t k) { return d % 32 == 0 && k <= 128; }
 
 hipError_t launch_compress(int, int64_t, int64_t, int64_t, int64_t, const void*, const int32_t*,
                            const void*, const void*, float*, const float*, hipStream_t, uint16_t*, int) {

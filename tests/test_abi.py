@@ -69,7 +69,10 @@ def test_kernel_family_rules(ssn):
     assert kf("project_weights", "bf16", 5120, 51) == "mfma"
     assert kf("decompress", "bf16", 4064, 64) == "generic"
     assert kf("project_weights", "bf16", 4096, 64) == "mfma"
-    assert kf("project_weights", "f32", 4096, 64) == "generic"
+    assert kf("project_weights", "f32", 4096, 64) == "mfma"
+    assert kf("project_weights", "f32", 5120, 51) == "mfma"
+    assert kf("project_weights", "f32", 4100, 64) == "generic"
+    assert kf("project_weights", "f32", 4096, 144) == "generic"
     assert kf("compress_projected", "bf16", 4096, 64) == "mfma"
     assert kf("compress_projected", "bf16", 5120, 51) == "mfma"
     # float32 storage: the matrix-core kernels where d is a multiple of 64 and
