@@ -245,9 +245,12 @@ constexpr int cols_max_waves(int kt, bool kv, int ct) { return (kt > 4 || !kv ||
 // NTL: W is read with non-temporal loads (each piece is read once and then
 // overwritten by pass 2).  The 128-byte lines at the boundary of two strips
 // are fetched by both blocks, and a streamed line is not kept for the
-// neighbour, so streaming pays only while few lines are shared (measured on
-// MI355X: 4 x (4096^2, 4096 x 14336), k = 64, 576-byte strips: 224 -> 202 us;
-// 288-byte strips at d = 2048 and 736-byte strips at k = 51: slower).
+// neighbour.  Measured on MI355X (8-matrix batches, k = 64, d = 4096 and
+// 5120, streamed against cached loads): 16 tiles per block (512-byte
+// strips) 171 / 193 us, 18 tiles 204 / 233 us (d = 5120: 280 / 288), 20
+// tiles 237 / 243 us; but 22 tiles 274 / 264 us, 23 tiles 452 / 413 us
+// (d = 5120) and 361 / 320 us (d = 4096), and 9 tiles (288-byte strips,
+// d = 2048) 85 / 78 us.  So the launcher streams for 16 to 20 tiles.
 // XCD: blocks are dispatched to the 8 XCDs round robin (block b on XCD
 // b mod 8); with XCD the block of launch index b takes strip
 // (b mod 8) * (grid / 8) + b / 8, so that neighbouring strips, which share
@@ -562,9 +565,9 @@ static hipError_t launch_cols_kv(ColumnBatch cb, int cus, const void* U, int d, 
   cb.tpb = tpb < 1 ? 1 : (tpb > kMaxTpb ? kMaxTpb : tpb);
   const unsigned grid = (unsigned)((cb.tiles + cb.tpb - 1) / cb.tpb);
   // XCD-aware strip order when the grid is a multiple of the 8 XCDs;
-  // streamed W loads with k % 8 == 0 and strips of at least 512 bytes
+  // streamed W loads with k % 8 == 0 and 16 to 20 tiles per block (measured)
   const bool xcd = grid % 8 == 0;
-  const bool ntl = KV && cb.tpb * 32 >= 512;
+  const bool ntl = KV && cb.tpb >= 16 && cb.tpb <= 20;
 #define SSN_COLS(CT)                                                                              \
   do {                                                                                            \
     if (xcd && ntl)                                                                               \
