@@ -67,15 +67,17 @@ def test_codec_past_2_31_elements():
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("n", [2 ** 19 + 8, 2 ** 19 + 1])
-def test_weight_projection_past_2_31_elements(n):
-    """W [4096, n] with 4096 n > 2^31, re-projected in place: n % 8 == 0 runs
-    the column-strip kernel, odd n the 64-column panel kernel."""
+@pytest.mark.parametrize("n,dtype", [(2 ** 19 + 8, "bf16"), (2 ** 19 + 1, "bf16"), (2 ** 19 + 4, "f32")])
+def test_weight_projection_past_2_31_elements(n, dtype):
+    """W [4096, n] with 4096 n > 2^31, re-projected in place: in bf16, n % 8 ==
+    0 runs the column-strip kernel and odd n the 64-column panel kernel; in
+    float32 (8.6 GB) n % 4 == 0 runs the float32 column-strip kernel."""
     d, k = 4096, 64
     assert d * n > TWO31
-    print(f"[case] weights d={d} n={n} k={k}", flush=True)
-    U = I.to_device(I.store(I.gaussian_orthonormal_basis(d, k, 1091), "bf16"), "bf16", DEV)
-    W = I.weights_device(d, n, 1091, DEV)
+    print(f"[case] weights d={d} n={n} k={k} {dtype} family="
+          f"{ssn.kernel_family('project_weights', dtype, d, k)}", flush=True)
+    U = I.to_device(I.store(I.gaussian_orthonormal_basis(d, k, 1091), dtype), dtype, DEV)
+    W = I.weights_device(d, n, 1091, DEV, dtype)
     cols = boundary_rows(n, 1, 256, 1091)
     cols = np.unique(np.concatenate([cols, np.arange(n - 70, n)]))
     c = torch.from_numpy(cols).to(DEV)
@@ -83,8 +85,8 @@ def test_weight_projection_past_2_31_elements(n):
     ssn.project_weights(W, U)
     torch.cuda.synchronize()
     Uh = host(U)
-    check(f"large weights n={n}", host(W[:, c]), O.project_weights(before, Uh), "bf16", "bf16out",
-          mag_weights(before, Uh))
+    check(f"large weights n={n} {dtype}", host(W[:, c]), O.project_weights(before, Uh), dtype,
+          "bf16out" if dtype == "bf16" else "f32out", mag_weights(before, Uh))
     del W, U
     torch.cuda.empty_cache()
 
