@@ -84,8 +84,8 @@ const char *ssn_status_string(int status);
  * compress_projected / decompress d % 128 == 0; project_weights d % 32 == 0
  * (and, when k % 8 != 0, every n % 8 == 0); and float32 storage for
  * compress / project_grad / compress_projected / decompress with d % 64 == 0
- * and U rows of 16, 32, .., 128 floats (k, or ldu of a zero-padded basis),
- * and project_weights with d % 32 == 0, k <= 128 and every n % 4 == 0, on
+ * and U rows of 1 to 128 floats (k, or ldu of a zero-padded basis), and
+ * project_weights with d % 32 == 0, k <= 128 and every n % 4 == 0, on
  * float32 MFMA (float32 products and accumulation).  Everything else runs
  * the generic kernels (fp32 arithmetic, one wavefront per token / one block
  * per column).

@@ -27,39 +27,77 @@ __device__ __forceinline__ f32x4 mfma16x16x4f32(float a, float b, f32x4 c) {
 constexpr int kF32Chunk = 64;
 
 bool f32_uses_mfma(int64_t d, int64_t k) {
-  return d % kF32Chunk == 0 && d <= INT32_MAX && k % 16 == 0 && k >= 16 && k <= 128;
+  return d % kF32Chunk == 0 && d <= INT32_MAX && k >= 1 && k <= 128;
 }
 
-// U rows [64 c, 64 c + 64) of U [d, K] are one contiguous span of 64 K
-// floats; thread tid stages its 16-byte pieces p = tid + T i into the LDS tile
-// (row 4p / K, column 4p % K, pitch K + 4).  Threads past the last piece load
-// the last piece again and do not store it.
-template <int K, int T>
+// U rows [64 c, 64 c + 64) of U [d, ku] are one contiguous span of 64 ku
+// floats (16-byte aligned with U: 256 ku bytes per chunk).  Thread tid stages
+// its 16-byte pieces p = tid + T i of the span into the LDS tile of pitch
+// K + 4.  SPAN false (ku == K): piece p lands whole at row 4p / K, column
+// 4p % K.  SPAN (ku < K, any width): the piece's four floats go one by one
+// to (row, column) = divmod(4p + e, ku); columns ku .. K - 1 are zeroed once
+// by zero_pad and never written, so the tile is the zero-padded basis.
+// Threads past the last piece load the last piece again (SPAN: nothing) and
+// do not store it.
+template <int K, int T, bool SPAN>
 struct UStage {
   static constexpr int UP = K + 4;
-  static constexpr int NP = kF32Chunk * K / 4;
-  static constexpr int FPT = (NP + T - 1) / T;
-  int src[FPT], dst[FPT];
+  static constexpr int NPMAX = kF32Chunk * K / 4;
+  static constexpr int FPT = (NPMAX + T - 1) / T;
+  int src[FPT];
+  int dst[FPT][SPAN ? 4 : 1];
   bool on[FPT];
-  __device__ __forceinline__ explicit UStage(int tid) {
+  int ku;
+  __device__ __forceinline__ UStage(int tid, int ku_) : ku(SPAN ? ku_ : K) {
+    const int np = SPAN ? kF32Chunk * ku / 4 : NPMAX;
 #pragma unroll
     for (int i = 0; i < FPT; ++i) {
       const int p0 = tid + T * i;
-      on[i] = NP % T == 0 || p0 < NP;
-      const int p = on[i] ? p0 : NP - 1;
+      on[i] = (!SPAN && NPMAX % T == 0) || p0 < np;
+      const int p = on[i] ? p0 : np - 1;
       src[i] = 4 * p;
-      dst[i] = (4 * p / K) * UP + (4 * p) % K;
+      if constexpr (SPAN) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int idx = 4 * p + e, row = idx / ku;
+          dst[i][e] = row * UP + (idx - row * ku);
+        }
+      } else {
+        dst[i][0] = (4 * p / K) * UP + (4 * p) % K;
+      }
     }
   }
   __device__ __forceinline__ void load(const float* __restrict__ U, int c, f32x4 (&r)[FPT]) const {
-    const float* base = U + (int64_t)c * kF32Chunk * K;
+    const float* base = U + (int64_t)c * kF32Chunk * ku;
 #pragma unroll
-    for (int i = 0; i < FPT; ++i) r[i] = *(const f32x4*)(base + src[i]);
+    for (int i = 0; i < FPT; ++i) {
+      if constexpr (SPAN)
+        r[i] = on[i] ? *(const f32x4*)(base + src[i]) : f32x4{0.f, 0.f, 0.f, 0.f};
+      else
+        r[i] = *(const f32x4*)(base + src[i]);
+    }
   }
   __device__ __forceinline__ void store(float* tile, const f32x4 (&r)[FPT]) const {
 #pragma unroll
     for (int i = 0; i < FPT; ++i)
-      if (on[i]) *(f32x4*)(tile + dst[i]) = r[i];
+      if (on[i]) {
+        if constexpr (SPAN) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) tile[dst[i][e]] = r[i][e];
+        } else {
+          *(f32x4*)(tile + dst[i][0]) = r[i];
+        }
+      }
+  }
+  // columns ku .. K - 1 of the 64 rows of `tiles` consecutive tiles
+  __device__ __forceinline__ void zero_pad(float* tile, int tiles, int tid) const {
+    if constexpr (SPAN) {
+      const int w = K - ku, n = tiles * kF32Chunk * w;
+      for (int i = tid; i < n; i += T) {
+        const int row = i / w;
+        tile[row * UP + ku + (i - row * w)] = 0.f;
+      }
+    }
   }
 };
 
@@ -77,14 +115,14 @@ struct UStage {
 // N - 1 and store the same bytes there.  GZ: the coordinate row of token t is
 // Z[ids[t]] (a gathered table), with no embedding added.
 // ===========================================================================
-template <int KQ, bool HAS_E, bool GZ>
+template <int KQ, bool HAS_E, bool GZ, bool SPAN>
 __global__ __launch_bounds__(512) void decompress_f32_mfma(
     const float* __restrict__ Zc, const int32_t* __restrict__ ids, const float* __restrict__ E,
     const float* __restrict__ U, float* __restrict__ Y, int64_t N, int d, int64_t V,
-    const uint16_t* __restrict__ Zb, int kz) {
+    const uint16_t* __restrict__ Zb, int kz, int ku) {
   static_assert(!(HAS_E && GZ), "gathered coordinates carry no additive embedding");
   constexpr int K = 16 * KQ, DC = kF32Chunk, W = 8;
-  using Stage = UStage<K, 64 * W>;
+  using Stage = UStage<K, 64 * W, SPAN>;
   constexpr int UP = Stage::UP, FPT = Stage::FPT;
   __shared__ __align__(16) float ut[2][DC * UP];
   __shared__ f32x4 st[W][16 * 16];                 // [wave][token * 16 + (cell ^ token)]
@@ -117,7 +155,8 @@ __global__ __launch_bounds__(512) void decompress_f32_mfma(
     yrow[m] = Y + t * d + 4 * n16;
     erow[m] = HAS_E ? E + clamp_id(ids[t], V) * d + 4 * n16 : nullptr;
   }
-  const Stage stage(tid);
+  const Stage stage(tid, ku);
+  stage.zero_pad(&ut[0][0], 2, tid);
   f32x4 ust[2][FPT];
   f32x4 ering[2][4];
   auto load_e = [&](int c, f32x4(&eo)[4]) {
@@ -193,14 +232,14 @@ __global__ __launch_bounds__(512) void decompress_f32_mfma(
 // coordinates KP j .. KP j + KP - 1 of tokens 4 g .. 4 g + 3.  Block = W
 // waves x 16 tokens, every wave sweeping all of d (start rotated per block).
 // ===========================================================================
-template <int KP, bool HAS_E, bool HAS_P, int W>
+template <int KP, bool HAS_E, bool HAS_P, int W, bool SPAN>
 __global__ __launch_bounds__(64 * W) void compress_f32_mfma(
     const float* __restrict__ X, const int32_t* __restrict__ ids, const float* __restrict__ E,
     const float* __restrict__ U, float* __restrict__ Z, int64_t N, int d, int64_t V,
-    const float* __restrict__ Pt, uint16_t* __restrict__ Zb, int kz) {
+    const float* __restrict__ Pt, uint16_t* __restrict__ Zb, int kz, int ku) {
   static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
   constexpr int K = 16 * KP, DC = kF32Chunk;
-  using Stage = UStage<K, 64 * W>;
+  using Stage = UStage<K, 64 * W, SPAN>;
   constexpr int UP = Stage::UP, FPT = Stage::FPT;
   __shared__ __align__(16) float ut[2][DC * UP];
   __shared__ f32x4 dt[W][16 * 16];                 // [wave][token * 16 + (cell ^ token)]
@@ -219,7 +258,8 @@ __global__ __launch_bounds__(64 * W) void compress_f32_mfma(
     xrow[m] = X + t * d + 4 * n16;
     erow[m] = HAS_E ? E + clamp_id(ids[t], V) * d + 4 * n16 : nullptr;
   }
-  const Stage stage(tid);
+  const Stage stage(tid, ku);
+  stage.zero_pad(&ut[0][0], 2, tid);
   f32x4 ust[2][FPT];
   f32x4 xs[2][4], es[2][4];
   auto load_rows = [&](int c, f32x4(&xo)[4], f32x4(&eo)[4]) {
@@ -668,21 +708,31 @@ __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBa
 // ===========================================================================
 // Launchers.
 // ===========================================================================
-template <int KQ>
+template <int KQ, bool SPAN>
 static hipError_t launch_decompress_f32_kq(dim3 grid, int64_t N, int d, int64_t V, const float* Z,
                                            const int32_t* ids, const float* E, const float* U,
                                            float* Y, bool gather_z, hipStream_t st,
-                                           const uint16_t* Zb, int kz) {
+                                           const uint16_t* Zb, int kz, int ku) {
   if (E)
-    hipLaunchKernelGGL((decompress_f32_mfma<KQ, true, false>), grid, dim3(512), 0, st, Z, ids, E, U,
-                       Y, N, d, V, Zb, kz);
+    hipLaunchKernelGGL((decompress_f32_mfma<KQ, true, false, SPAN>), grid, dim3(512), 0, st, Z, ids, E,
+                       U, Y, N, d, V, Zb, kz, ku);
   else if (gather_z)
-    hipLaunchKernelGGL((decompress_f32_mfma<KQ, false, true>), grid, dim3(512), 0, st, Z, ids, E, U,
-                       Y, N, d, V, Zb, kz);
+    hipLaunchKernelGGL((decompress_f32_mfma<KQ, false, true, SPAN>), grid, dim3(512), 0, st, Z, ids, E,
+                       U, Y, N, d, V, Zb, kz, ku);
   else
-    hipLaunchKernelGGL((decompress_f32_mfma<KQ, false, false>), grid, dim3(512), 0, st, Z, ids, E,
-                       U, Y, N, d, V, Zb, kz);
+    hipLaunchKernelGGL((decompress_f32_mfma<KQ, false, false, SPAN>), grid, dim3(512), 0, st, Z, ids,
+                       E, U, Y, N, d, V, Zb, kz, ku);
   return hipGetLastError();
+}
+
+template <int KQ>
+static hipError_t launch_decompress_f32_span(dim3 grid, int64_t N, int d, int64_t V, const float* Z,
+                                             const int32_t* ids, const float* E, const float* U,
+                                             float* Y, bool gather_z, hipStream_t st,
+                                             const uint16_t* Zb, int kz, int ku) {
+  return ku == 16 * KQ
+             ? launch_decompress_f32_kq<KQ, false>(grid, N, d, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku)
+             : launch_decompress_f32_kq<KQ, true>(grid, N, d, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku);
 }
 
 hipError_t launch_decompress_f32(int64_t N, int64_t d, int64_t k, int64_t V, const float* Z,
@@ -691,61 +741,63 @@ hipError_t launch_decompress_f32(int64_t N, int64_t d, int64_t k, int64_t V, con
   const int64_t blocks = (N + 127) / 128;
   const int gy = decompress_grid_split(blocks, (int)(d / kF32Chunk));
   const dim3 grid((unsigned)blocks, (unsigned)gy);
-  const int dd = (int)d;
-  switch (k / 16) {
-    case 1: return launch_decompress_f32_kq<1>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz);
-    case 2: return launch_decompress_f32_kq<2>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz);
-    case 3: return launch_decompress_f32_kq<3>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz);
-    case 4: return launch_decompress_f32_kq<4>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz);
-    case 5: return launch_decompress_f32_kq<5>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz);
-    case 6: return launch_decompress_f32_kq<6>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz);
-    case 7: return launch_decompress_f32_kq<7>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz);
-    default: return launch_decompress_f32_kq<8>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz);
+  const int dd = (int)d, ku = (int)k;
+  switch ((k + 15) / 16) {
+    case 1: return launch_decompress_f32_span<1>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku);
+    case 2: return launch_decompress_f32_span<2>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku);
+    case 3: return launch_decompress_f32_span<3>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku);
+    case 4: return launch_decompress_f32_span<4>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku);
+    case 5: return launch_decompress_f32_span<5>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku);
+    case 6: return launch_decompress_f32_span<6>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku);
+    case 7: return launch_decompress_f32_span<7>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku);
+    default: return launch_decompress_f32_span<8>(grid, N, dd, V, Z, ids, E, U, Y, gather_z, st, Zb, kz, ku);
   }
 }
 
-template <int KP, int W>
+template <int KP, int W, bool SPAN>
 static hipError_t launch_compress_f32_kp(int64_t N, int d, int64_t V, const float* X,
                                          const int32_t* ids, const float* E, const float* U,
                                          float* Z, const float* P, hipStream_t st, uint16_t* Zb,
-                                         int kz) {
+                                         int kz, int ku) {
   const dim3 grid((unsigned)((N + 16 * W - 1) / (16 * W)));
   if (E)
-    hipLaunchKernelGGL((compress_f32_mfma<KP, true, false, W>), grid, dim3(64 * W), 0, st, X, ids, E,
-                       U, Z, N, d, V, P, Zb, kz);
+    hipLaunchKernelGGL((compress_f32_mfma<KP, true, false, W, SPAN>), grid, dim3(64 * W), 0, st, X, ids,
+                       E, U, Z, N, d, V, P, Zb, kz, ku);
   else if (P)
-    hipLaunchKernelGGL((compress_f32_mfma<KP, false, true, W>), grid, dim3(64 * W), 0, st, X, ids, E,
-                       U, Z, N, d, V, P, Zb, kz);
+    hipLaunchKernelGGL((compress_f32_mfma<KP, false, true, W, SPAN>), grid, dim3(64 * W), 0, st, X, ids,
+                       E, U, Z, N, d, V, P, Zb, kz, ku);
   else
-    hipLaunchKernelGGL((compress_f32_mfma<KP, false, false, W>), grid, dim3(64 * W), 0, st, X, ids,
-                       E, U, Z, N, d, V, P, Zb, kz);
+    hipLaunchKernelGGL((compress_f32_mfma<KP, false, false, W, SPAN>), grid, dim3(64 * W), 0, st, X,
+                       ids, E, U, Z, N, d, V, P, Zb, kz, ku);
   return hipGetLastError();
 }
 
 template <int KP>
 static hipError_t launch_compress_f32_w(int64_t N, int d, int64_t V, const float* X,
                                         const int32_t* ids, const float* E, const float* U, float* Z,
-                                        const float* P, hipStream_t st, uint16_t* Zb, int kz) {
+                                        const float* P, hipStream_t st, uint16_t* Zb, int kz, int ku) {
   // 8 waves (128 tokens) per block once those blocks fill the compute units,
-  // else 4 (64 tokens)
-  if ((N + 127) / 128 >= device_cu_count())
-    return launch_compress_f32_kp<KP, 8>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz);
-  return launch_compress_f32_kp<KP, 4>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz);
+  // else 4 (64 tokens); U rows of any width other than 16 KP are staged span-wise
+  const bool eight = (N + 127) / 128 >= device_cu_count(), span = ku != 16 * KP;
+  if (eight && !span) return launch_compress_f32_kp<KP, 8, false>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+  if (eight) return launch_compress_f32_kp<KP, 8, true>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+  if (!span) return launch_compress_f32_kp<KP, 4, false>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+  return launch_compress_f32_kp<KP, 4, true>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
 }
 
 hipError_t launch_compress_f32(int64_t N, int64_t d, int64_t k, int64_t V, const float* X,
                                const int32_t* ids, const float* E, const float* U, float* Z,
                                const float* P, hipStream_t st, uint16_t* Zb, int kz) {
-  const int dd = (int)d;
-  switch (k / 16) {
-    case 1: return launch_compress_f32_w<1>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz);
-    case 2: return launch_compress_f32_w<2>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz);
-    case 3: return launch_compress_f32_w<3>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz);
-    case 4: return launch_compress_f32_w<4>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz);
-    case 5: return launch_compress_f32_w<5>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz);
-    case 6: return launch_compress_f32_w<6>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz);
-    case 7: return launch_compress_f32_w<7>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz);
-    default: return launch_compress_f32_w<8>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz);
+  const int dd = (int)d, ku = (int)k;
+  switch ((k + 15) / 16) {
+    case 1: return launch_compress_f32_w<1>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+    case 2: return launch_compress_f32_w<2>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+    case 3: return launch_compress_f32_w<3>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+    case 4: return launch_compress_f32_w<4>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+    case 5: return launch_compress_f32_w<5>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+    case 6: return launch_compress_f32_w<6>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+    case 7: return launch_compress_f32_w<7>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
+    default: return launch_compress_f32_w<8>(N, dd, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
   }
 }
 

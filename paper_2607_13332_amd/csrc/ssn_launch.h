@@ -19,8 +19,8 @@ bool compress_uses_mfma(int dtype, int64_t d, int64_t k);
 bool decompress_uses_mfma(int dtype, int64_t d, int64_t k);
 bool weights_use_mfma(int dtype, int64_t d, int64_t k);
 // float32 storage on the matrix cores (v_mfma_f32_16x16x4_f32): d a multiple
-// of 64 and U rows of k = 16, 32, .., 128 floats (a zero-padded basis for
-// other ranks).
+// of 64 and U rows of 1 to 128 floats (rows whose width is not a multiple of
+// 16 are staged element by element into a zero-padded tile).
 bool f32_uses_mfma(int64_t d, int64_t k);
 // float32 weight re-projection on the matrix cores: d a multiple of 32 and
 // k <= 128 (plus, checked by the launcher, every n a multiple of 4 and 16-byte

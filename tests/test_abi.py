@@ -60,7 +60,8 @@ def test_kernel_family_rules(ssn):
     assert kf("compress", "bf16", 4096, 128) == "mfma"
     assert kf("compress", "bf16", 4096, 129) == "generic"
     assert kf("compress", "bf16", 4100, 64) == "generic"
-    assert kf("compress", "f32", 256, 8) == "generic"
+    assert kf("compress", "f32", 256, 8) == "mfma"
+    assert kf("compress", "f32", 4000, 8) == "generic"
     assert kf("project_grad", "bf16", 2048, 32) == "mfma"
     assert kf("decompress", "bf16", 4096, 64) == "mfma"
     assert kf("decompress", "bf16", 4096, 51) == "mfma"
@@ -80,7 +81,8 @@ def test_kernel_family_rules(ssn):
     assert kf("compress_projected", "f32", 4096, 64) == "mfma"
     assert kf("compress", "f32", 5120, 16) == "mfma"
     assert kf("decompress", "f32", 4096, 128) == "mfma"
-    assert kf("project_grad", "f32", 4096, 51) == "generic"
+    assert kf("project_grad", "f32", 4096, 51) == "mfma"
+    assert kf("decompress", "f32", 5120, 1) == "mfma"
     assert kf("decompress", "f32", 4096, 144) == "generic"
     assert kf("decompress", "f32", 4100, 64) == "generic"
     assert ssn.lib().ssn_kernel_family(9, 1, 4096, 64) == b"invalid"
