@@ -44,53 +44,65 @@ struct UStage {
   static constexpr int UP = K + 4;
   static constexpr int NPMAX = kF32Chunk * K / 4;
   static constexpr int FPT = (NPMAX + T - 1) / T;
-  int src[FPT];
-  int dst[FPT][SPAN ? 4 : 1];
-  bool on[FPT];
-  int ku;
-  __device__ __forceinline__ UStage(int tid, int ku_) : ku(SPAN ? ku_ : K) {
-    const int np = SPAN ? kF32Chunk * ku / 4 : NPMAX;
-#pragma unroll
-    for (int i = 0; i < FPT; ++i) {
-      const int p0 = tid + T * i;
-      on[i] = (!SPAN && NPMAX % T == 0) || p0 < np;
-      const int p = on[i] ? p0 : np - 1;
-      src[i] = 4 * p;
-      if constexpr (SPAN) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int idx = 4 * p + e, row = idx / ku;
-          dst[i][e] = row * UP + (idx - row * ku);
-        }
-      } else {
-        dst[i][0] = (4 * p / K) * UP + (4 * p) % K;
-      }
+  int tid, ku;
+  int row0, col0, drow, dcol;   // SPAN: (row, column) of element 4 tid, and the step of 4 T elements
+  __device__ __forceinline__ UStage(int tid_, int ku_) : tid(tid_), ku(SPAN ? ku_ : K) {
+    if constexpr (SPAN) {
+      row0 = 4 * tid / ku;
+      col0 = 4 * tid - row0 * ku;
+      drow = 4 * T / ku;
+      dcol = 4 * T - drow * ku;
+    } else {
+      row0 = col0 = drow = dcol = 0;
     }
+  }
+  // piece tid + T i exists (threads past the last piece of the fixed-width
+  // layout load the last piece again and do not store it)
+  __device__ __forceinline__ bool on(int i) const {
+    return SPAN ? tid + T * i < kF32Chunk * ku / 4 : (NPMAX % T == 0 || tid + T * i < NPMAX);
   }
   __device__ __forceinline__ void load(const float* __restrict__ U, int c, f32x4 (&r)[FPT]) const {
     const float* base = U + (int64_t)c * kF32Chunk * ku;
 #pragma unroll
     for (int i = 0; i < FPT; ++i) {
-      if constexpr (SPAN)
-        r[i] = on[i] ? *(const f32x4*)(base + src[i]) : f32x4{0.f, 0.f, 0.f, 0.f};
-      else
-        r[i] = *(const f32x4*)(base + src[i]);
+      if constexpr (SPAN) {
+        r[i] = on(i) ? *(const f32x4*)(base + 4 * (tid + T * i)) : f32x4{0.f, 0.f, 0.f, 0.f};
+      } else {
+        const int p = on(i) ? tid + T * i : NPMAX - 1;
+        r[i] = *(const f32x4*)(base + 4 * p);
+      }
     }
   }
   __device__ __forceinline__ void store(float* tile, const f32x4 (&r)[FPT]) const {
+    int row = row0, col = col0;
 #pragma unroll
-    for (int i = 0; i < FPT; ++i)
-      if (on[i]) {
-        if constexpr (SPAN) {
+    for (int i = 0; i < FPT; ++i) {
+      if constexpr (SPAN) {
+        if (on(i)) {
+          int rr = row, cc = col;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) tile[dst[i][e]] = r[i][e];
-        } else {
-          *(f32x4*)(tile + dst[i][0]) = r[i];
+          for (int e = 0; e < 4; ++e) {
+            tile[rr * UP + cc] = r[i][e];
+            if (++cc == ku) {
+              cc = 0;
+              ++rr;
+            }
+          }
         }
+        col += dcol;
+        row += drow;
+        if (col >= ku) {
+          col -= ku;
+          ++row;
+        }
+      } else {
+        const int p = tid + T * i;
+        if (on(i)) *(f32x4*)(tile + (4 * p / K) * UP + (4 * p) % K) = r[i];
       }
+    }
   }
   // columns ku .. K - 1 of the 64 rows of `tiles` consecutive tiles
-  __device__ __forceinline__ void zero_pad(float* tile, int tiles, int tid) const {
+  __device__ __forceinline__ void zero_pad(float* tile, int tiles) const {
     if constexpr (SPAN) {
       const int w = K - ku, n = tiles * kF32Chunk * w;
       for (int i = tid; i < n; i += T) {
@@ -156,7 +168,7 @@ __global__ __launch_bounds__(512) void decompress_f32_mfma(
     erow[m] = HAS_E ? E + clamp_id(ids[t], V) * d + 4 * n16 : nullptr;
   }
   const Stage stage(tid, ku);
-  stage.zero_pad(&ut[0][0], 2, tid);
+  stage.zero_pad(&ut[0][0], 2);
   f32x4 ust[2][FPT];
   f32x4 ering[2][4];
   auto load_e = [&](int c, f32x4(&eo)[4]) {
@@ -259,7 +271,7 @@ __global__ __launch_bounds__(64 * W) void compress_f32_mfma(
     erow[m] = HAS_E ? E + clamp_id(ids[t], V) * d + 4 * n16 : nullptr;
   }
   const Stage stage(tid, ku);
-  stage.zero_pad(&ut[0][0], 2, tid);
+  stage.zero_pad(&ut[0][0], 2);
   f32x4 ust[2][FPT];
   f32x4 xs[2][4], es[2][4];
   auto load_rows = [&](int c, f32x4(&xo)[4], f32x4(&eo)[4]) {
@@ -345,6 +357,149 @@ __global__ __launch_bounds__(64 * W) void compress_f32_mfma(
       const int col = KP * n16 + h;
       if (col >= kz) continue;
       float v = acc[h][r];
+      if constexpr (HAS_P) v -= Pt[clamp_id(ids[t], V) * kz + col];
+      if (Zb)
+        Zb[t * kz + col] = (uint16_t)f32_to_bf16(v);
+      else
+        Z[t * kz + col] = v;
+    }
+  }
+}
+
+// ===========================================================================
+// compress / gradient projection for few tokens (the kernel above runs
+// N / 64 blocks, a fraction of the chip).  Block = 16 tokens x PW waves; wave
+// w walks the w-th of PW equal ranges of d with a wave-private U tile and D
+// tile, so no barrier is needed until the end (a wave's LDS operations
+// complete in order).  U for the next chunks travels in UD register sets;
+// the MFMA loop is the one above.  The PW partial products meet in LDS and
+// are added in wave order (deterministic); wave w finishes the coordinates
+// KP j + h with h = w mod PW.
+// ===========================================================================
+template <int KP, bool HAS_E, bool HAS_P, bool SPAN, int PW, int UD>
+__global__ __launch_bounds__(64 * PW) void compress_f32_split(
+    const float* __restrict__ X, const int32_t* __restrict__ ids, const float* __restrict__ E,
+    const float* __restrict__ U, float* __restrict__ Z, int64_t N, int d, int64_t V,
+    const float* __restrict__ Pt, uint16_t* __restrict__ Zb, int kz, int ku) {
+  static_assert(!(HAS_E && HAS_P), "the embedding is subtracted as rows or as projected rows");
+  static_assert(UD == 1 || UD == 2, "U register sets");
+  constexpr int K = 16 * KP, DC = kF32Chunk;
+  using Stage = UStage<K, 64, SPAN>;
+  constexpr int UP = Stage::UP, FPT = Stage::FPT;
+  static_assert(KP * 64 * 4 <= DC * UP, "the partial products fit a wave's U tile");
+  __shared__ __align__(16) float ut[PW][DC * UP];
+  __shared__ f32x4 dt[PW][16 * 16];                // [wave][token * 16 + (cell ^ token)]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n16 = lane & 15, g = lane >> 4;
+  const int64_t tok0 = (int64_t)blockIdx.x * 16;
+
+  // rows: instruction m covers tokens 4 m .. 4 m + 3, 16 lanes (256 bytes) each
+  const float* xrow[4];
+  const float* erow[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    int64_t t = tok0 + 4 * m + g;
+    t = t < N ? t : N - 1;
+    xrow[m] = X + t * d + 4 * n16;
+    erow[m] = HAS_E ? E + clamp_id(ids[t], V) * d + 4 * n16 : nullptr;
+  }
+  const Stage stage(lane, ku);
+  float* const ub = ut[wave];
+  stage.zero_pad(ub, 1);
+  f32x4* const dw = dt[wave];
+  f32x4 ust[UD][FPT];
+  f32x4 xs[2][4], es[2][4];
+  auto load_rows = [&](int c, f32x4(&xo)[4], f32x4(&eo)[4]) {
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      xo[m] = __builtin_nontemporal_load((const f32x4*)(xrow[m] + c * DC));
+      if constexpr (HAS_E) eo[m] = *(const f32x4*)(erow[m] + c * DC);
+    }
+  };
+
+  const int nch = d / (DC * PW), c0 = wave * nch;
+  f32x4 acc[KP];
+#pragma unroll
+  for (int i = 0; i < KP; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // chunk i: its rows in set i % 2, its U already in the tile; chunk i + 1's
+  // U in register set (i + 1) % UD
+  auto body = [&](int i, auto Bc) {
+    constexpr int B = decltype(Bc)::value;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const int r = 4 * m + g;
+      dw[r * 16 + (n16 ^ r)] = HAS_E ? xs[B][m] - es[B][m] : xs[B][m];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 a = dw[n16 * 16 + ((4 * q + g) ^ n16)];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const float* ur = ub + (16 * q + 4 * g + s) * UP + KP * n16;
+        float b[KP];
+        if constexpr (KP % 4 == 0) {
+#pragma unroll
+          for (int h = 0; h < KP; h += 4) {
+            const f32x4 v = *(const f32x4*)(ur + h);
+            b[h] = v[0]; b[h + 1] = v[1]; b[h + 2] = v[2]; b[h + 3] = v[3];
+          }
+        } else if constexpr (KP % 2 == 0) {
+#pragma unroll
+          for (int h = 0; h < KP; h += 2) {
+            const f32x2 v = *(const f32x2*)(ur + h);
+            b[h] = v[0]; b[h + 1] = v[1];
+          }
+        } else {
+#pragma unroll
+          for (int h = 0; h < KP; ++h) b[h] = ur[h];
+        }
+#pragma unroll
+        for (int h = 0; h < KP; ++h) acc[h] = mfma16x16x4f32(a[s], b[h], acc[h]);
+      }
+    }
+    if (i + 1 < nch) {
+      // the tile's reads above were issued first, so this overwrite is safe
+      stage.store(ub, ust[(B + 1) % UD]);
+      if (i + 1 + UD < nch) stage.load(U, c0 + i + 1 + UD, ust[(B + 1) % UD]);
+      if (i + 2 < nch) load_rows(c0 + i + 2, xs[B], es[B]);
+    }
+  };
+
+  stage.load(U, c0, ust[0]);
+  load_rows(c0, xs[0], es[0]);
+  stage.store(ub, ust[0]);
+#pragma unroll
+  for (int j = 1; j <= UD; ++j)
+    if (j < nch) stage.load(U, c0 + j, ust[j % UD]);
+  if (nch > 1) load_rows(c0 + 1, xs[1], es[1]);
+  int i = 0;
+  for (; i + 1 < nch; i += 2) {
+    body(i, std::integral_constant<int, 0>{});
+    body(i + 1, std::integral_constant<int, 1>{});
+  }
+  if (i < nch) body(i, std::integral_constant<int, 0>{});
+
+  // partial products of all waves, then coordinates KP j + h (h = w mod PW)
+  __syncthreads();
+  f32x4* const red = (f32x4*)&ut[0][0];           // [wave][h][lane]
+#pragma unroll
+  for (int h = 0; h < KP; ++h) red[(wave * KP + h) * 64 + lane] = acc[h];
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < KP; ++h) {
+    if (h % PW != wave) continue;
+    f32x4 s = red[h * 64 + lane];
+#pragma unroll
+    for (int w2 = 1; w2 < PW; ++w2) s += red[(w2 * KP + h) * 64 + lane];
+    const int col = KP * n16 + h;
+    if (col >= kz) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t t = tok0 + 4 * g + r;
+      if (t >= N) continue;
+      float v = s[r];
       if constexpr (HAS_P) v -= Pt[clamp_id(ids[t], V) * kz + col];
       if (Zb)
         Zb[t * kz + col] = (uint16_t)f32_to_bf16(v);
@@ -772,13 +927,41 @@ static hipError_t launch_compress_f32_kp(int64_t N, int d, int64_t V, const floa
   return hipGetLastError();
 }
 
+template <int KP, bool SPAN>
+static hipError_t launch_compress_f32_split(int64_t N, int d, int64_t V, const float* X,
+                                            const int32_t* ids, const float* E, const float* U,
+                                            float* Z, const float* P, hipStream_t st, uint16_t* Zb,
+                                            int kz, int ku) {
+  constexpr int PW = 4, UD = KP <= 4 ? 2 : 1;
+  const dim3 grid((unsigned)((N + 15) / 16));
+  if (E)
+    hipLaunchKernelGGL((compress_f32_split<KP, true, false, SPAN, PW, UD>), grid, dim3(64 * PW), 0, st, X,
+                       ids, E, U, Z, N, d, V, P, Zb, kz, ku);
+  else if (P)
+    hipLaunchKernelGGL((compress_f32_split<KP, false, true, SPAN, PW, UD>), grid, dim3(64 * PW), 0, st, X,
+                       ids, E, U, Z, N, d, V, P, Zb, kz, ku);
+  else
+    hipLaunchKernelGGL((compress_f32_split<KP, false, false, SPAN, PW, UD>), grid, dim3(64 * PW), 0, st,
+                       X, ids, E, U, Z, N, d, V, P, Zb, kz, ku);
+  return hipGetLastError();
+}
+
 template <int KP>
 static hipError_t launch_compress_f32_w(int64_t N, int d, int64_t V, const float* X,
                                         const int32_t* ids, const float* E, const float* U, float* Z,
                                         const float* P, hipStream_t st, uint16_t* Zb, int kz, int ku) {
   // 8 waves (128 tokens) per block once those blocks fill the compute units,
-  // else 4 (64 tokens); U rows of any width other than 16 KP are staged span-wise
-  const bool eight = (N + 127) / 128 >= device_cu_count(), span = ku != 16 * KP;
+  // else 4 (64 tokens); U rows of any width other than 16 KP are staged
+  // span-wise.  With at most half as many 64-token blocks as compute units,
+  // d is split over the 4 waves of 16-token blocks instead (measured on
+  // MI355X, compress / projection: N = 2048, d = 2048, k = 40: 53 -> 22 us;
+  // N = 4096, d = 5120, k = 51: 152 -> 62 us; N = 8192, d = 2048: 57 ->
+  // 43 us; but N = 12288, d = 5120: 167 us against 185 us split).
+  const int64_t cus = device_cu_count();
+  const bool eight = (N + 127) / 128 >= cus, span = ku != 16 * KP;
+  if (2 * ((N + 63) / 64) <= cus && d % (4 * kF32Chunk) == 0)
+    return span ? launch_compress_f32_split<KP, true>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku)
+                : launch_compress_f32_split<KP, false>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
   if (eight && !span) return launch_compress_f32_kp<KP, 8, false>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
   if (eight) return launch_compress_f32_kp<KP, 8, true>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
   if (!span) return launch_compress_f32_kp<KP, 4, false>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
