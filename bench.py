@@ -33,6 +33,7 @@ on one GPU.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -96,7 +97,7 @@ def parse_args():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle baseline sample")
     p.add_argument("--tokens", type=int, default=0, help="override N (testing only)")
-    p.add_argument("--only", choices=("reparam", "sparta", "sweep", "paper", "weights"), default=None,
+    p.add_argument("--only", choices=("reparam", "sparta", "sweep", "paper", "weights", "f32"), default=None,
                    help="profiling aid: run only this section and print its JSON (no headline; "
                         "keeps its kernels apart from the codec's in a kernel trace)")
     p.add_argument("--sweep-tokens", type=str, default="",
@@ -328,6 +329,16 @@ def kernel_op(kernel_name: str) -> str:
                     ("pad_basis", "pad_basis"), ("copyBuffer", "device copy")):
         if key in kernel_name:
             return op
+    if "decompress_f32" in kernel_name:
+        # <KQ, HAS_E, GZ, SPAN>
+        if a[2:3] == ["true"]:
+            return "factored_embedding"
+        return "decompress" if a[1:2] == ["true"] else "expand_grad"
+    if "compress_f32" in kernel_name:
+        # <KP, HAS_E, HAS_P, ...>
+        if a[1:2] == ["true"]:
+            return "compress"
+        return "compress_projected" if a[2:3] == ["true"] else "project_grad"
     if "decompress" in kernel_name:
         if len(a) > 7 and a[7] == "true":
             return "factored_embedding"
@@ -647,10 +658,12 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
     from paper_2607_13332_amd import inputs as I
     from paper_2607_13332_amd import ssn
     N, d, k = cfg.N, cfg.d, cfg.k
+    es = 2 if cfg.dtype == "bf16" else 4
+    act = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     base = I.codec_inputs_device(cfg, dev, need=("U", "E"))
     U, E = base["U"], base["E"]
     # X, G, Y, G_X and the embedding rows of decompress and compress
-    set_bytes = 6 * N * d * 2
+    set_bytes = 6 * N * d * es
     nsets = min(24, max(2, -(-(1 << 30) // set_bytes)))
     sets = []
     for j in range(nsets):
@@ -660,8 +673,8 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         inp["GZin"] = I.coords_device(N, k, c.seed + 2, dev)
         inp["Z"] = torch.empty((N, k), dtype=torch.float32, device=dev)
         inp["GZ"] = torch.empty((N, k), dtype=torch.float32, device=dev)
-        inp["Y"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
-        inp["GX"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        inp["Y"] = torch.empty((N, d), dtype=act, device=dev)
+        inp["GX"] = torch.empty((N, d), dtype=act, device=dev)
         inp["ids_c"] = I.codec_inputs_device(I.with_tokens(cfg, N, seed=c.seed + 7), dev,
                                              need=("ids",))["ids"]
         inp["u"] = int(torch.unique(inp["ids"]).numel())
@@ -737,14 +750,14 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
     step_bytes = 0
     for op in ops:
         t = op_ms[op]
-        byts = float(np.mean([algorithmic_bytes(op, N, d, k, op_u(op, s)) for s in sets]))
+        byts = float(np.mean([algorithmic_bytes(op, N, d, k, op_u(op, s), es) for s in sets]))
         step_bytes += byts
         per_op[op] = {"ms": round(t, 5), "algorithmic_GBps": round(byts / (t * 1e-3) / 1e9, 1),
                       "frac_hbm_peak": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     gms = time_step_graph(sets, lambda s: step(s, Ub), steps, warmup)
     basis = f"U [{d}, {k}] stored zero-padded to {ldu} columns (ssn_pad_basis, once per basis)" \
         if ldu != k else f"U [{d}, {k}]"
-    out = {"workload": f"N={N} (B={cfg.B} x S={cfg.S}), d={d}, k={k}, V={cfg.V}, bf16, "
+    out = {"workload": f"N={N} (B={cfg.B} x S={cfg.S}), d={d}, k={k}, V={cfg.V}, {cfg.dtype}, "
                        f"{cfg.ids_dist} ids",
            "basis": basis,
            "input_sets": f"{nsets} rotating sets, {nsets * set_bytes / 2**30:.2f} GiB "
@@ -809,6 +822,13 @@ def run_section(name: str, args, dev):
         cfgs = ([c for c in I.sweep_configs() if c.k == 64] if name == "sweep" else I.paper_configs())
         return {c.name: time_codec_config(c, max(10, args.steps // 2), args.warmup, dev)
                 for c in cfgs if kept(c.name, c.N)}
+    if name == "f32":
+        # float32 storage (activations, embedding, basis) on the matrix cores
+        cfgs = [dataclasses.replace(I.STAGE8B, dtype="f32", name="stage8b_f32")] + \
+               [dataclasses.replace(c, dtype="f32", name=c.name + "_f32") for c in I.paper_configs()
+                if c.B == 1]
+        return {c.name: time_codec_config(c, max(10, args.steps // 2), args.warmup, dev)
+                for c in cfgs if kept(c.name, c.N)}
     if name == "weights":
         return {wc.name + ("" if dt == "bf16" else "_f32"): time_weights(wc, args.steps, dev, dt)
                 for wc in (I.WEIGHTS, I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B) for dt in ("bf16", "f32")
@@ -871,8 +891,8 @@ def main():
         inp["GZin"] = I.coords_device(N, k, c.seed + 2, dev)
         inp["Z"] = torch.empty((N, k), dtype=torch.float32, device=dev)
         inp["GZ"] = torch.empty((N, k), dtype=torch.float32, device=dev)
-        inp["Y"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
-        inp["GX"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        inp["Y"] = torch.empty((N, d), dtype=act, device=dev)
+        inp["GX"] = torch.empty((N, d), dtype=act, device=dev)
         inp["ids_c"] = I.codec_inputs_device(I.with_tokens(cfg, N, seed=c.seed + 7), dev,
                                              need=("ids",))["ids"]
         inp["u"] = int(torch.unique(inp["ids"]).numel())
