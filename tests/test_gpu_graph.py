@@ -15,22 +15,24 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 
 
-def _codec_inputs(N, d, k, V, seed):
-    cfg = I.CodecConfig("graph", B=1, S=N, d=d, k=k, V=V, dtype="bf16", seed=seed, structured=False)
+def _codec_inputs(N, d, k, V, seed, dtype="bf16"):
+    cfg = I.CodecConfig("graph", B=1, S=N, d=d, k=k, V=V, dtype=dtype, seed=seed, structured=False)
     h = I.codec_inputs_device(cfg, DEV)
     h["Zin"] = I.coords_device(N, k, seed + 1, DEV)
     h["GZin"] = I.coords_device(N, k, seed + 2, DEV)
     return h
 
 
-@pytest.mark.parametrize("N,d,k", [(4096, 5120, 51), (2048, 4096, 64)])
-def test_codec_step_replays_match_eager(N, d, k):
+@pytest.mark.parametrize("N,d,k,dtype", [(4096, 5120, 51, "bf16"), (2048, 4096, 64, "bf16"),
+                                         (4096, 5120, 51, "f32"), (20000, 1024, 64, "f32")])
+def test_codec_step_replays_match_eager(N, d, k, dtype):
     V = 4096
-    print(f"[graph] codec N={N} d={d} k={k}", flush=True)
-    static = _codec_inputs(N, d, k, V, 7000)
-    outs = {"Y": torch.empty((N, d), dtype=torch.bfloat16, device=DEV),
+    print(f"[graph] codec N={N} d={d} k={k} {dtype}", flush=True)
+    act = torch.bfloat16 if dtype == "bf16" else torch.float32
+    static = _codec_inputs(N, d, k, V, 7000, dtype)
+    outs = {"Y": torch.empty((N, d), dtype=act, device=DEV),
             "GZ": torch.empty((N, k), device=DEV), "Z": torch.empty((N, k), device=DEV),
-            "GX": torch.empty((N, d), dtype=torch.bfloat16, device=DEV)}
+            "GX": torch.empty((N, d), dtype=act, device=DEV)}
 
     def step(s, o):
         ssn.decompress(s["Zin"], s["ids"], s["E"], s["U"], out=o["Y"])
@@ -44,7 +46,7 @@ def test_codec_step_replays_match_eager(N, d, k):
     with torch.cuda.graph(g):
         step(static, outs)
     for rep in range(3):
-        fresh = _codec_inputs(N, d, k, V, 7100 + rep)
+        fresh = _codec_inputs(N, d, k, V, 7100 + rep, dtype)
         for key in ("X", "G", "E", "U", "ids", "Zin", "GZin"):
             static[key].copy_(fresh[key])
         g.replay()
@@ -151,3 +153,28 @@ def test_reparam_and_averaging_capture(N, din, d, k):
         torch.cuda.synchronize()
         for key in outs:
             assert torch.equal(got[key], ref[key]), f"replay {rep}: {key} differs from eager"
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_weight_reprojection_capture(dtype):
+    """The batched weight re-projection, in place, captured and replayed on
+    fresh matrices: each replay equals an eager call on the same matrices."""
+    d, k, ns = 2048, 48, (2048, 7168, 1000)
+    print(f"[graph] weights d={d} k={k} n={ns} {dtype}", flush=True)
+    U = I.to_device(I.store(I.gaussian_orthonormal_basis(d, k, 7400), dtype), dtype, DEV)
+    Ws = [I.weights_device(d, n, 7400 + j, DEV, dtype) for j, n in enumerate(ns)]
+    ssn.project_weights_batched(Ws, U)        # warm-up outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        ssn.project_weights_batched(Ws, U)
+    for rep in range(3):
+        fresh = [I.weights_device(d, n, 7500 + 10 * rep + j, DEV, dtype) for j, n in enumerate(ns)]
+        for W, F in zip(Ws, fresh):
+            W.copy_(F)
+        g.replay()
+        ref = [F.clone() for F in fresh]
+        ssn.project_weights_batched(ref, U)   # eager on the same matrices
+        torch.cuda.synchronize()
+        for j, (W, R) in enumerate(zip(Ws, ref)):
+            assert torch.equal(W, R), f"replay {rep}: matrix {j} differs from eager"
