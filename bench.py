@@ -507,33 +507,36 @@ def time_weights(wc, steps: int, dev, dtype: str = "bf16"):
 
 
 def time_reparam(N: int, din: int, d: int, k: int, steps: int, dev, seed: int = 1040,
-                 pad_to: int = 0):
+                 pad_to: int = 0, dtype: str = "bf16"):
     """Reparameterized-SSN projection of one layer: forward (H Zp) U^T and the
-    backward (G U, (G U) Zp^T, H^T (G U)), bf16 storage.  pad_to > k: Zp and U
-    stored with zero columns up to pad_to (the same layer: the padding columns
-    of T, G U and the factor gradient stay zero)."""
+    backward (G U, (G U) Zp^T, H^T (G U)), storage dtype `dtype` (bf16 or
+    f32).  pad_to > k: Zp and U stored with zero columns up to pad_to (the
+    same layer: the padding columns of T, G U and the factor gradient stay
+    zero)."""
     import numpy as np
     import torch
     from paper_2607_13332_amd import inputs as I
     from paper_2607_13332_amd import ssn
+    sdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    es = 2 if dtype == "bf16" else 4
     g = torch.Generator(device=dev).manual_seed(seed)
-    H = torch.randn((N, din), generator=g, device=dev).to(torch.bfloat16)
-    G = torch.randn((N, d), generator=g, device=dev).to(torch.bfloat16)
-    Zp = (0.02 * torch.randn((din, k), generator=g, device=dev)).to(torch.bfloat16)
-    U = I.to_device(I.store(I.gaussian_orthonormal_basis(d, k, seed), "bf16"), "bf16", dev)
+    H = torch.randn((N, din), generator=g, device=dev).to(sdt)
+    G = torch.randn((N, d), generator=g, device=dev).to(sdt)
+    Zp = (0.02 * torch.randn((din, k), generator=g, device=dev)).to(sdt)
+    U = I.to_device(I.store(I.gaussian_orthonormal_basis(d, k, seed), dtype), dtype, dev)
     kalg = k
     if pad_to > k:
-        Zq = torch.zeros((din, pad_to), dtype=torch.bfloat16, device=dev)
-        Uq = torch.zeros((d, pad_to), dtype=torch.bfloat16, device=dev)
+        Zq = torch.zeros((din, pad_to), dtype=sdt, device=dev)
+        Uq = torch.zeros((d, pad_to), dtype=sdt, device=dev)
         Zq[:, :k] = Zp
         Uq[:, :k] = U
         Zp, U, k = Zq, Uq, pad_to
     T = torch.empty((N, k), dtype=torch.float32, device=dev)
-    Y = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+    Y = torch.empty((N, d), dtype=sdt, device=dev)
     GT = torch.empty((N, k), dtype=torch.float32, device=dev)
-    GH = torch.empty((N, din), dtype=torch.bfloat16, device=dev)
+    GH = torch.empty((N, din), dtype=sdt, device=dev)
     GZ = torch.empty((din, k), dtype=torch.float32, device=dev)
-    ws = torch.empty((max(4, ssn.reparam_workspace_bytes("bf16", N, din, k)) + 3) // 4,
+    ws = torch.empty((max(4, ssn.reparam_workspace_bytes(dtype, N, din, k)) + 3) // 4,
                      dtype=torch.float32, device=dev)
     for _ in range(3):
         ssn.reparam_forward(H, Zp, U, T, Y)
@@ -549,11 +552,11 @@ def time_reparam(N: int, din: int, d: int, k: int, steps: int, dev, seed: int = 
     torch.cuda.synchronize()
     fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
     bwd = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
-    fb = 2.0 * N * din + 2.0 * N * d + 8.0 * N * kalg + 2.0 * (din + d) * kalg
-    bb = 2.0 * N * d + 4.0 * N * din + 12.0 * N * kalg + 2.0 * (din + d) * kalg + 4.0 * din * kalg
+    fb = es * N * din + es * N * d + 8.0 * N * kalg + es * (din + d) * kalg
+    bb = es * N * d + 2 * es * N * din + 12.0 * N * kalg + es * (din + d) * kalg + 4.0 * din * kalg
     pad = f", stored zero-padded to {k} columns" if k != kalg else ""
     out = {"workload": f"one projection layer: H [{N}, {din}], Zp [{din}, {kalg}], "
-                       f"U [{d}, {kalg}]{pad}, bf16",
+                       f"U [{d}, {kalg}]{pad}, {dtype}",
            "forward_ms": round(fwd, 5),
            "forward_frac_hbm_peak": round(fb / (fwd * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "backward_ms": round(bwd, 5),
@@ -827,8 +830,12 @@ def run_section(name: str, args, dev):
         cfgs = [dataclasses.replace(I.STAGE8B, dtype="f32", name="stage8b_f32")] + \
                [dataclasses.replace(c, dtype="f32", name=c.name + "_f32") for c in I.paper_configs()
                 if c.B == 1]
-        return {c.name: time_codec_config(c, max(10, args.steps // 2), args.warmup, dev)
-                for c in cfgs if kept(c.name, c.N)}
+        out = {c.name: time_codec_config(c, max(10, args.steps // 2), args.warmup, dev)
+               for c in cfgs if kept(c.name, c.N)}
+        if not names or "paper8b_mlp_out_f32" in names:
+            out["paper8b_mlp_out_f32"] = time_reparam(4096, 18432, 5120, 51, max(10, args.steps // 2), dev,
+                                                      dtype="f32")
+        return out
     if name == "weights":
         return {wc.name + ("" if dt == "bf16" else "_f32"): time_weights(wc, args.steps, dev, dt)
                 for wc in (I.WEIGHTS, I.WEIGHTS_PAPER8B, I.WEIGHTS_PAPER1B) for dt in ("bf16", "f32")

@@ -590,10 +590,15 @@ __device__ __forceinline__ W32Piece w32_piece(const ColumnBatchF32& cb, int t0, 
 // U (32 whole rows, one contiguous span of 32 k floats that starts 16-byte
 // aligned) is read with 16-byte loads and scattered element by element into
 // the zero-padded row tile, and pass 2 reads its U operands element by element.
-template <int KT, int CT, int RS, bool KV>
+// FG: the reparameterized layer's factor gradient (section 4.1, Eq. (3)),
+// dZp = H^T GT, with H [N, din] as the single matrix of the batch, GT [N, k]
+// in place of U and N rows in place of d (any N: rows past N load as zero):
+// pass 1 alone, then T = GT^T H is written transposed to fg_out [din, k].
+template <int KT, int CT, int RS, bool KV, bool FG>
 __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBatchF32 cb,
                                                                        const float* __restrict__ U,
-                                                                       int d, int k, int xcd) {
+                                                                       int d, int k, int xcd,
+                                                                       float* __restrict__ fg_out) {
   static_assert(CT >= 1 && CT <= 3 && (RS == 1 || RS == 2 || RS == 4 || RS == 8), "tile groups");
   constexpr int TW = 8 / RS;                    // tile groups
   constexpr int K = 16 * KT, R1 = kW32Rows, R2 = kW32Rows * RS;
@@ -625,7 +630,7 @@ __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBa
   const int bx = xcd ? (int)((blockIdx.x % 8u) * (gridDim.x / 8u) + blockIdx.x / 8u) : (int)blockIdx.x;
   const int t0 = bx * tpb;
   const int tcount = min(tpb, cb.tiles - t0);
-  const int nch1 = d / R1, nch2 = (d + R2 - 1) / R2;
+  const int nch1 = FG ? (d + R1 - 1) / R1 : d / R1, nch2 = (d + R2 - 1) / R2;
   // this wave's tiles: tw + TW v for v < nv
   const int nv = tcount > tw ? min(CT, (tcount - tw + TW - 1) / TW) : 0;
 
@@ -657,14 +662,28 @@ __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBa
 #pragma unroll
     for (int i = 0; i < NP1; ++i) {
       const f32x4* src = (const f32x4*)(wp[i].ptr + (int64_t)c * R1 * wp[i].ld);
+      const bool ok = wp[i].on && (!FG || c * R1 + wp[i].row < d);
       if constexpr (RS == 1)
-        wv[i] = wp[i].on ? __builtin_nontemporal_load(src) : f32x4{0.f, 0.f, 0.f, 0.f};
+        wv[i] = ok ? __builtin_nontemporal_load(src) : f32x4{0.f, 0.f, 0.f, 0.f};
       else
-        wv[i] = wp[i].on ? *src : f32x4{0.f, 0.f, 0.f, 0.f};
+        wv[i] = ok ? *src : f32x4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
-    for (int i = 0; i < NUP; ++i)
-      uv[i] = uon[i] ? *(const f32x4*)(U + (int64_t)c * R1 * k + us[i]) : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < NUP; ++i) {
+      const int64_t e0 = (int64_t)c * R1 * k + us[i];
+      if constexpr (FG) {
+        // elements past the N k floats of GT load as zero
+        const int64_t lim = (int64_t)d * k;
+        if (uon[i] && e0 + 4 <= lim) {
+          uv[i] = *(const f32x4*)(U + e0);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) uv[i][e] = (uon[i] && e0 + e < lim) ? U[e0 + e] : 0.f;
+        }
+      } else {
+        uv[i] = uon[i] ? *(const f32x4*)(U + e0) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
   };
   auto store_chunk = [&](int buf) {
 #pragma unroll
@@ -785,6 +804,31 @@ __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBa
 #pragma unroll
         for (int v = 0; v < NV; ++v) acc[kt][v] = red[(tw * E + kt * CT + v) * 64 + lane];
       __syncthreads();                          // totals read before pass 2 parks rows
+    }
+
+    if constexpr (FG) {
+      // lane (n16, g) holds T[16 kt + 4 g + r][16 j + n16]: dZp row 16 j + n16
+      // (of din), columns 16 kt + 4 g + r (of k); one wave per tile group writes
+      if (rs == 0) {
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          const int col = 16 * (t0 + tw + TW * v) + n16;
+          if (col >= cb.n[0]) continue;
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt) {
+            const int kc = 16 * kt + 4 * g;
+            float* dst = fg_out + (int64_t)col * k + kc;
+            if (KV && kc < k && (((uintptr_t)fg_out & 15u) == 0)) {
+              *(f32x4*)dst = acc[kt][v];
+            } else {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (kc + r < k) dst[r] = acc[kt][v][r];
+            }
+          }
+        }
+      }
+      return;
     }
 
     // ---- pass 2: W = U T ----
@@ -984,37 +1028,56 @@ hipError_t launch_compress_f32(int64_t N, int64_t d, int64_t k, int64_t V, const
   }
 }
 
-template <int KT, int CT, int RS>
+template <int KT, int CT, int RS, bool FG>
 static hipError_t launch_weights_f32_cfg(const ColumnBatchF32& cb, const float* U, int d, int k,
-                                         hipStream_t st) {
+                                         float* fg_out, hipStream_t st) {
   const unsigned grid = (unsigned)((cb.tiles + cb.tpb - 1) / cb.tpb);
   const int xcd = grid % 8 == 0 ? 1 : 0;
   if (k % 4 == 0)
-    hipLaunchKernelGGL((project_weights_f32_mfma<KT, CT, RS, true>), dim3(grid), dim3(kW32Threads), 0, st,
-                       cb, U, d, k, xcd);
+    hipLaunchKernelGGL((project_weights_f32_mfma<KT, CT, RS, true, FG>), dim3(grid), dim3(kW32Threads), 0,
+                       st, cb, U, d, k, xcd, fg_out);
   else
-    hipLaunchKernelGGL((project_weights_f32_mfma<KT, CT, RS, false>), dim3(grid), dim3(kW32Threads), 0, st,
-                       cb, U, d, k, xcd);
+    hipLaunchKernelGGL((project_weights_f32_mfma<KT, CT, RS, false, FG>), dim3(grid), dim3(kW32Threads), 0,
+                       st, cb, U, d, k, xcd, fg_out);
   return hipGetLastError();
 }
 
 // Tile groups by tiles per block: 8 groups of one wave for tpb >= 8 (CT =
 // ceil(tpb / 8) tiles per wave), 4 groups of 2 waves for 4..7, 2 of 4 for 2..3,
 // one of 8 for a single tile.
-template <int KT>
+template <int KT, bool FG>
 static hipError_t launch_weights_f32_kt(const ColumnBatchF32& cb, const float* U, int d, int k,
-                                        hipStream_t st) {
+                                        float* fg_out, hipStream_t st) {
   const int tpb = cb.tpb;
   if constexpr (KT <= 5) {
-    if (tpb >= 17) return launch_weights_f32_cfg<KT, 3, 1>(cb, U, d, k, st);
+    if (tpb >= 17) return launch_weights_f32_cfg<KT, 3, 1, FG>(cb, U, d, k, fg_out, st);
   }
-  if (tpb >= 9) return launch_weights_f32_cfg<KT, 2, 1>(cb, U, d, k, st);
-  if (tpb == 8) return launch_weights_f32_cfg<KT, 1, 1>(cb, U, d, k, st);
-  if (tpb >= 5) return launch_weights_f32_cfg<KT, 2, 2>(cb, U, d, k, st);
-  if (tpb == 4) return launch_weights_f32_cfg<KT, 1, 2>(cb, U, d, k, st);
-  if (tpb == 3) return launch_weights_f32_cfg<KT, 2, 4>(cb, U, d, k, st);
-  if (tpb == 2) return launch_weights_f32_cfg<KT, 1, 4>(cb, U, d, k, st);
-  return launch_weights_f32_cfg<KT, 1, 8>(cb, U, d, k, st);
+  if (tpb >= 9) return launch_weights_f32_cfg<KT, 2, 1, FG>(cb, U, d, k, fg_out, st);
+  if (tpb == 8) return launch_weights_f32_cfg<KT, 1, 1, FG>(cb, U, d, k, fg_out, st);
+  if (tpb >= 5) return launch_weights_f32_cfg<KT, 2, 2, FG>(cb, U, d, k, fg_out, st);
+  if (tpb == 4) return launch_weights_f32_cfg<KT, 1, 2, FG>(cb, U, d, k, fg_out, st);
+  if (tpb == 3) return launch_weights_f32_cfg<KT, 2, 4, FG>(cb, U, d, k, fg_out, st);
+  if (tpb == 2) return launch_weights_f32_cfg<KT, 1, 4, FG>(cb, U, d, k, fg_out, st);
+  return launch_weights_f32_cfg<KT, 1, 8, FG>(cb, U, d, k, fg_out, st);
+}
+
+template <bool FG>
+static hipError_t launch_strips_f32(ColumnBatchF32& cb, const float* U, int d, int k, float* fg_out,
+                                    hipStream_t st) {
+  // one block per compute unit while a strip fits the LDS tiles
+  const int cus = device_cu_count();
+  const int tpb = (cb.tiles + cus - 1) / cus, tmax = w32_max_tpb(k);
+  cb.tpb = tpb < 1 ? 1 : (tpb > tmax ? tmax : tpb);
+  switch ((k + 15) / 16) {
+    case 1: return launch_weights_f32_kt<1, FG>(cb, U, d, k, fg_out, st);
+    case 2: return launch_weights_f32_kt<2, FG>(cb, U, d, k, fg_out, st);
+    case 3: return launch_weights_f32_kt<3, FG>(cb, U, d, k, fg_out, st);
+    case 4: return launch_weights_f32_kt<4, FG>(cb, U, d, k, fg_out, st);
+    case 5: return launch_weights_f32_kt<5, FG>(cb, U, d, k, fg_out, st);
+    case 6: return launch_weights_f32_kt<6, FG>(cb, U, d, k, fg_out, st);
+    case 7: return launch_weights_f32_kt<7, FG>(cb, U, d, k, fg_out, st);
+    default: return launch_weights_f32_kt<8, FG>(cb, U, d, k, fg_out, st);
+  }
 }
 
 bool weights_f32_uses_mfma(int64_t d, int64_t k) {
@@ -1038,20 +1101,25 @@ hipError_t launch_project_weights_f32(int count, int64_t d, const int64_t* n, in
   for (int b = nb; b <= kMaxBatch; ++b) cb.first_tile[b] = acc;
   cb.count = nb;
   cb.tiles = acc;
-  // one block per compute unit while a strip fits the LDS tiles
-  const int cus = device_cu_count();
-  const int tpb = (acc + cus - 1) / cus, tmax = w32_max_tpb(k);
-  cb.tpb = tpb < 1 ? 1 : (tpb > tmax ? tmax : tpb);
-  switch ((k + 15) / 16) {
-    case 1: return launch_weights_f32_kt<1>(cb, U, (int)d, (int)k, st);
-    case 2: return launch_weights_f32_kt<2>(cb, U, (int)d, (int)k, st);
-    case 3: return launch_weights_f32_kt<3>(cb, U, (int)d, (int)k, st);
-    case 4: return launch_weights_f32_kt<4>(cb, U, (int)d, (int)k, st);
-    case 5: return launch_weights_f32_kt<5>(cb, U, (int)d, (int)k, st);
-    case 6: return launch_weights_f32_kt<6>(cb, U, (int)d, (int)k, st);
-    case 7: return launch_weights_f32_kt<7>(cb, U, (int)d, (int)k, st);
-    default: return launch_weights_f32_kt<8>(cb, U, (int)d, (int)k, st);
-  }
+  return launch_strips_f32<false>(cb, U, (int)d, (int)k, nullptr, st);
+}
+
+bool factor_grad_f32_uses_mfma(int64_t N, int64_t din, int64_t k) {
+  return N >= 0 && N <= INT32_MAX && din >= 1 && din % 4 == 0 && din <= INT32_MAX / 2 && k >= 1 &&
+         k <= 128;
+}
+
+hipError_t launch_factor_grad_f32(int64_t N, int64_t din, int64_t k, const float* H, const float* GT,
+                                  float* dZp, hipStream_t st) {
+  ColumnBatchF32 cb{};
+  cb.W[0] = const_cast<float*>(H);    // read only: the factor-gradient mode has no second pass
+  cb.n[0] = (int32_t)din;
+  const int32_t tiles = (int32_t)((din + 15) / 16);
+  cb.first_tile[0] = 0;
+  for (int b = 1; b <= kMaxBatch; ++b) cb.first_tile[b] = tiles;
+  cb.count = 1;
+  cb.tiles = tiles;
+  return launch_strips_f32<true>(cb, GT, (int)N, (int)k, dZp, st);
 }
 
 }  // namespace ssn

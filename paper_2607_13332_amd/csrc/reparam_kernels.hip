@@ -429,7 +429,7 @@ __global__ __launch_bounds__(256) void factor_grad_reduce(const float* __restric
   }
 }
 
-// Generic kernel (fp32 H, or din not a multiple of 16): one thread per
+// Generic kernel (shapes neither matrix-core kernel takes): one thread per
 // output element, fp32 FMA over the tokens in order.
 template <typename T>
 __global__ __launch_bounds__(256) void factor_grad_generic(const T* __restrict__ H,
@@ -546,6 +546,9 @@ hipError_t launch_reparam_backward_fused(int64_t N, int64_t din, int64_t k, cons
 
 hipError_t launch_factor_grad(int dtype, int64_t N, int64_t din, int64_t k, const void* H,
                               const float* GT, float* dZp, float* ws, hipStream_t st) {
+  if (dtype == kF32 && factor_grad_f32_uses_mfma(N, din, k) && ((uintptr_t)H & 15u) == 0 &&
+      ((uintptr_t)GT & 15u) == 0)
+    return launch_factor_grad_f32(N, din, k, (const float*)H, GT, dZp, st);
   if (factor_grad_uses_mfma(dtype, din, k) && ((uintptr_t)H & 15u) == 0) {
     const int64_t S = factor_grad_splits(N, din, k);
     const int64_t chunks = (N + kFgRows - 1) / kFgRows;

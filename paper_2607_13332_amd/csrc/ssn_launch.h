@@ -28,6 +28,13 @@ bool f32_uses_mfma(int64_t d, int64_t k);
 bool weights_f32_uses_mfma(int64_t d, int64_t k);
 hipError_t launch_project_weights_f32(int count, int64_t d, const int64_t* n, int64_t k,
                                       float* const* W, const float* U, hipStream_t st);
+// The reparameterized layer's factor gradient dZp = H^T GT in float32 on the
+// matrix cores (the weight kernel's first pass over column strips of H):
+// din a multiple of 4, k <= 128, H and GT 16-byte aligned (checked by the
+// caller), any N.
+bool factor_grad_f32_uses_mfma(int64_t N, int64_t din, int64_t k);
+hipError_t launch_factor_grad_f32(int64_t N, int64_t din, int64_t k, const float* H, const float* GT,
+                                  float* dZp, hipStream_t st);
 // Ranges of d (grid.y) for `blocks` token blocks of the decompress kernels.
 int decompress_grid_split(int64_t blocks, int chunks);
 // float32 forms of launch_compress / launch_decompress (same arguments;

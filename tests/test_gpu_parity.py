@@ -534,6 +534,11 @@ REPARAM_SHAPES = [  # (N, din, d, k, dtype): every kernel family and tail
     # has too few chunks per range and keeps the d-split kernel): k = 64 and
     # 128 in 8 ranges, k = 32 in 16 ranges
     (4096, 18432, 2048, 64, "bf16"), (4096, 8192, 2048, 128, "bf16"), (2048, 16384, 1024, 32, "bf16"),
+    # float32 storage: the matrix-core kernels, the factor gradient as the
+    # weight kernel's first pass over column strips of H (ragged token
+    # counts, k % 4 != 0, narrow din) and the generic paths (din % 4 != 0)
+    (1000, 2048, 1024, 51, "f32"), (777, 1024, 512, 64, "f32"), (33, 100, 96, 10, "f32"),
+    (130, 4096, 2048, 128, "f32"), (4096, 18432, 5120, 51, "f32"), (50, 102, 128, 16, "f32"),
 ]
 
 
