@@ -49,6 +49,8 @@ MFMA_F32_PEAK_TFLOPS = 157.3    # MI355X dense float32 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_2607_13332_amd/csrc/codec_kernels.hip",
                   "paper_2607_13332_amd/csrc/f32_kernels.hip",
+                  "paper_2607_13332_amd/csrc/f32_strips.h",
+                  "paper_2607_13332_amd/csrc/f32_weights.hip",
                   "paper_2607_13332_amd/csrc/weights_kernels.hip",
                   "paper_2607_13332_amd/csrc/reparam_kernels.hip",
                   "paper_2607_13332_amd/csrc/sparta_kernels.hip",

@@ -19,8 +19,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libssn.so")
-SOURCES = ["ssn_api.hip", "noalloc.hip", "codec_kernels.hip", "f32_kernels.hip",
-           "weights_kernels.hip", "reparam_kernels.hip", "sparta_kernels.hip"]
+SOURCES = ["ssn_api.hip", "noalloc.hip", "codec_kernels.hip", "f32_kernels.hip", "f32_weights.hip",
+           "f32_strips_a.hip", "f32_strips_b.hip", "weights_kernels.hip", "reparam_kernels.hip",
+           "sparta_kernels.hip"]
 ARCH = "gfx950"
 
 

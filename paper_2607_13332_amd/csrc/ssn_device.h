@@ -44,6 +44,14 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// 16x16x4 float32 MFMA.  A (16 x 4): lane l holds row l%16, K element l/16;
+// B (4 x 16): lane l holds column l%16, K element l/16; C (16 x 16): lane l
+// holds rows 4 (l/16) .. +3 of column l%16.  Only the pairing of K elements
+// between A and B matters, so each kernel picks the index a K slot carries.
+__device__ __forceinline__ f32x4 mfma16x16x4f32(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
 // Split 8 floats into bf16 hi + lo parts with x ~= hi + lo to ~2^-17 relative:
 // two MFMAs on (hi, lo) carry a float32 operand at close to fp32 accuracy.
 __device__ __forceinline__ void split_bf16x8(const float* v, u32x4& hi, u32x4& lo) {
