@@ -900,8 +900,8 @@ def main():
         inp["GZin"] = I.coords_device(N, k, c.seed + 2, dev)
         inp["Z"] = torch.empty((N, k), dtype=torch.float32, device=dev)
         inp["GZ"] = torch.empty((N, k), dtype=torch.float32, device=dev)
-        inp["Y"] = torch.empty((N, d), dtype=act, device=dev)
-        inp["GX"] = torch.empty((N, d), dtype=act, device=dev)
+        inp["Y"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        inp["GX"] = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
         inp["ids_c"] = I.codec_inputs_device(I.with_tokens(cfg, N, seed=c.seed + 7), dev,
                                              need=("ids",))["ids"]
         inp["u"] = int(torch.unique(inp["ids"]).numel())
