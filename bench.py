@@ -325,6 +325,8 @@ def summarize_counters(paths, calib_mib: int = 256):
 def kernel_op(kernel_name: str) -> str:
     """The library operation a kernel of this build serves (for trace tables)."""
     a = _template_args(kernel_name)
+    if "project_weights_f32" in kernel_name and a[-1:] == ["true"]:
+        return "factor_grad"                    # the strip kernel's factor-gradient mode
     for key, op in (("project_weights", "project_weights"), ("factor_grad_reduce", "factor_grad sum"),
                     ("factor_grad", "factor_grad"), ("reparam_backward_fused", "reparam backward (fused)"),
                     ("sum_partials", "range sum"), ("sparta", "sparta"), ("check_ids", "check_ids"),

@@ -99,3 +99,83 @@ def test_counter_summary_table(tmp_path, capsys):
     assert got["scaled MB read"] == f"{31000 * 1024 * 2.0 / 1e6:.1f}"
     assert got["scaled MB written"] == f"{62500 * 1024 * 1.0 / 1e6:.1f}"
     assert got["L2 hit %"] == "75.0"
+
+
+def test_bench_has_no_undefined_names():
+    """Every name bench.py reads is bound in its own scope, an enclosing
+    scope, the module or the builtins: the bench only runs on a GPU, so a
+    stray name would otherwise surface there first."""
+    import ast
+    import builtins
+
+    src = open(os.path.join(ROOT, "bench.py"), encoding="utf-8").read()
+    tree = ast.parse(src)
+
+    def bound_names(node):
+        """Names bound directly in the scope of `node` (not in nested scopes)."""
+        names = set()
+        if isinstance(node, (ast.FunctionDef, ast.AsyncFunctionDef, ast.Lambda)):
+            a = node.args
+            for arg in a.posonlyargs + a.args + a.kwonlyargs:
+                names.add(arg.arg)
+            if a.vararg:
+                names.add(a.vararg.arg)
+            if a.kwarg:
+                names.add(a.kwarg.arg)
+        body = node.body if isinstance(node.body, list) else [node.body]
+        stack = list(body)
+        while stack:
+            n = stack.pop()
+            if isinstance(n, (ast.FunctionDef, ast.AsyncFunctionDef, ast.ClassDef)):
+                names.add(n.name)
+                stack.extend(n.decorator_list)
+                continue
+            if isinstance(n, ast.Lambda):
+                continue
+            if isinstance(n, (ast.ListComp, ast.SetComp, ast.DictComp, ast.GeneratorExp)):
+                continue
+            if isinstance(n, ast.Name) and isinstance(n.ctx, (ast.Store, ast.Del)):
+                names.add(n.id)
+            elif isinstance(n, (ast.Import, ast.ImportFrom)):
+                for al in n.names:
+                    names.add((al.asname or al.name).split(".")[0])
+            elif isinstance(n, ast.ExceptHandler) and n.name:
+                names.add(n.name)
+            elif isinstance(n, (ast.Global, ast.Nonlocal)):
+                names.update(n.names)
+            stack.extend(ast.iter_child_nodes(n))
+        return names
+
+    module_names = bound_names(tree) | set(dir(builtins)) | {"__file__", "__name__"}
+    missing = []
+
+    def visit(node, env):
+        if isinstance(node, (ast.FunctionDef, ast.AsyncFunctionDef, ast.Lambda)):
+            for dflt in node.args.defaults + node.args.kw_defaults:
+                if dflt is not None:
+                    visit(dflt, env)
+            env = env | bound_names(node)
+            body = node.body if isinstance(node.body, list) else [node.body]
+            for n in body:
+                visit(n, env)
+            return
+        if isinstance(node, (ast.ListComp, ast.SetComp, ast.DictComp, ast.GeneratorExp)):
+            inner = set(env)
+            for gen in node.generators:
+                visit(gen.iter, inner)
+                for t in ast.walk(gen.target):
+                    if isinstance(t, ast.Name):
+                        inner.add(t.id)
+                for cond in gen.ifs:
+                    visit(cond, inner)
+            for part in ([node.key, node.value] if isinstance(node, ast.DictComp) else [node.elt]):
+                visit(part, inner)
+            return
+        if isinstance(node, ast.Name) and isinstance(node.ctx, ast.Load) and node.id not in env:
+            missing.append(f"{node.id} (line {node.lineno})")
+        for child in ast.iter_child_nodes(node):
+            visit(child, env)
+
+    for n in tree.body:
+        visit(n, module_names)
+    assert not missing, "names read but never bound: " + ", ".join(missing)
