@@ -18,8 +18,10 @@ namespace ssn {
 // step after each optimizer update, sections 4.1 and 6.1).  The columns of
 // all matrices of a batch form one sequence of 16-column tiles; block b owns
 // tpb consecutive tiles (a strip), one block per compute unit.  The 8 waves
-// form TW = 8 / RS tile groups of RS waves: wave w = tw + TW rs owns the
-// tiles tw, tw + TW, .. of the strip and row share rs.  Few tiles per block
+// form TW = 8 / RS tile groups of RS waves: wave w = RS tw + rs owns the
+// tiles tw, tw + TW, .. of the strip and row share rs (a group's waves are
+// consecutive, so they sit on different SIMDs when waves are placed on the
+// four SIMDs in turn, and groups with one tile more do not pile onto one SIMD).  Few tiles per block
 // (small matrices) thus still keep all four SIMDs on the matrix cores.
 // Pass 1, T = U^T W, over d in chunks of 32 rows: the chunk's rows of the
 // strip and of U are staged into LDS row tiles (double buffered, one barrier
@@ -125,7 +127,7 @@ __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBa
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n16 = lane & 15, g = lane >> 4;
-  const int tw = wave % TW, rs = wave / TW;
+  const int tw = wave / RS, rs = wave % RS;
   const int tpb = cb.tpb;
   const int WP1 = pitch_rows4q(16 * tpb);
   const int WP2 = pitch_rows4g(16 * tpb);
@@ -290,9 +292,9 @@ __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBa
       for (int i = 0; i < NE; ++i) {
         const int e = rs + RS * i;
         if (e < E && e % CT < NV) {
-          f32x4 s = red[(tw * E + e) * 64 + lane];
+          f32x4 s = red[(RS * tw * E + e) * 64 + lane];
 #pragma unroll
-          for (int r2 = 1; r2 < RS; ++r2) s += red[((tw + TW * r2) * E + e) * 64 + lane];
+          for (int r2 = 1; r2 < RS; ++r2) s += red[((RS * tw + r2) * E + e) * 64 + lane];
           tot[i] = s;
         }
       }
@@ -300,13 +302,13 @@ __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBa
 #pragma unroll
       for (int i = 0; i < NE; ++i) {
         const int e = rs + RS * i;
-        if (e < E && e % CT < NV) red[(tw * E + e) * 64 + lane] = tot[i];
+        if (e < E && e % CT < NV) red[(RS * tw * E + e) * 64 + lane] = tot[i];
       }
       __syncthreads();
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
-        for (int v = 0; v < NV; ++v) acc[kt][v] = red[(tw * E + kt * CT + v) * 64 + lane];
+        for (int v = 0; v < NV; ++v) acc[kt][v] = red[(RS * tw * E + kt * CT + v) * 64 + lane];
       __syncthreads();                          // totals read before pass 2 parks rows
     }
 
