@@ -762,6 +762,24 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         per_op[op] = {"ms": round(t, 5), "algorithmic_GBps": round(byts / (t * 1e-3) / 1e9, 1),
                       "frac_hbm_peak": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     gms = time_step_graph(sets, lambda s: step(s, Ub), steps, warmup)
+    # the same step with compress against the projected table P = E U (the
+    # NEXT form of section 4.1: E and U are fixed, so P is formed once)
+    P = ssn.project_table(E, U)
+
+    def step_projected(s):
+        ssn.decompress(s["Zin"], s["ids"], E, Ub, out=s["Y"])
+        ssn.project_grad(s["G"], Ub, out=s["GZ"], k=k)
+        ssn.compress_projected(s["X"], s["ids_c"], P, Ub, out=s["Z"])
+        ssn.expand_grad(s["GZin"], Ub, out=s["GX"])
+
+    for i in range(warmup):
+        step_projected(sets[i % nsets])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step_projected(sets[i % nsets])
+    torch.cuda.synchronize()
+    pms = (time.perf_counter() - t0) * 1e3 / steps
     basis = f"U [{d}, {k}] stored zero-padded to {ldu} columns (ssn_pad_basis, once per basis)" \
         if ldu != k else f"U [{d}, {k}]"
     out = {"workload": f"N={N} (B={cfg.B} x S={cfg.S}), d={d}, k={k}, V={cfg.V}, {cfg.dtype}, "
@@ -773,7 +791,10 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
            "step_frac_hbm_peak": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "ms_per_step_hip_graph": round(gms, 5),
            "tokens_per_s_hip_graph": round(N / (gms * 1e-3), 1),
-           "per_op": per_op}
+           "per_op": per_op,
+           "step_with_projected_compress": {
+               "what": "the same step with compress as X U - P[ids], P = E U [V, k] float32 formed once",
+               "ms_per_step": round(pms, 5), "tokens_per_s": round(N / (pms * 1e-3), 1)}}
     if pad_ms is not None:
         out["pad_basis_ms"] = round(pad_ms, 5)
         ums, uop = measure(U)
@@ -781,7 +802,7 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
             "what": f"the same step on U [{d}, {k}] as stored (k % 16 != 0: odd-width U rows)",
             "ms_per_step": round(ums, 5), "tokens_per_s": round(N / (ums * 1e-3), 1),
             "per_op_ms": {op: round(v, 5) for op, v in uop.items()}}
-    del sets, base, U, E, Ub
+    del sets, base, U, E, Ub, P
     torch.cuda.empty_cache()
     return out
 
