@@ -141,6 +141,16 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
     xr[i] = X + t * d + 8 * lc;
     er[i] = HAS_E ? E + clamp_id(ids[t], V) * d + 8 * lc : nullptr;
   }
+  // HAS_P: the table rows of the epilogue's tokens 4g + j, looked up now so
+  // that the end of the kernel waits for one load instead of two
+  int64_t prow[HAS_P ? 4 : 1];
+  if constexpr (HAS_P) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t tj = tok0 + 4 * g + j;
+      prow[j] = tj < N ? clamp_id(ids[tj], V) * kz : 0;
+    }
+  }
   // blockIdx.y selects one of gridDim.y equal ranges of d (a plain
   // projection with few tokens: the range's partial product goes to rows
   // [blockIdx.y * N, (blockIdx.y + 1) * N) of Z, summed afterwards)
@@ -243,7 +253,7 @@ __global__ __launch_bounds__(64 * WAVES) void compress_rows_bf16(
 #pragma unroll
       for (int i = 0; i < KP; ++i) v[i] = HAS_E ? accX[i][j] - accE[i][j] : accX[i][j];
       if constexpr (HAS_P) {
-        const float* pp = P + clamp_id(ids[tj], V) * kz + col0;
+        const float* pp = P + prow[j] + col0;
         if constexpr (KFULL && KP % 4 == 0) {
           if (whole) {
 #pragma unroll
@@ -351,6 +361,24 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
   const int nchp = d / (DC * P * (int)gridDim.y);   // chunks of this wave
   const int c0 = ((int)blockIdx.y * P + wave) * nchp;
   if constexpr (!HAS_E && !HAS_P) Z += (int64_t)blockIdx.y * N * kz;
+  // the final sums: thread tid finishes tile-lanes idx = tid + 64 P j; with
+  // HAS_P the table values it subtracts there are loaded now, so that their
+  // two dependent loads (id, then table row) overlap the main loop
+  constexpr int NEP = (TTW * KP * 64 + 64 * P - 1) / (64 * P);
+  float pv[HAS_P ? NEP : 1][4];
+  if constexpr (HAS_P) {
+#pragma unroll
+    for (int j = 0; j < NEP; ++j) {
+      const int idx = tid + 64 * P * j;
+      const int l = idx % 64, ti = idx / 64, i = ti % KP, tt = ti / KP;
+      const int col = 16 * i + (l & 15);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t t = tok0 + 16 * tt + 4 * (l >> 4) + e;
+        pv[j][e] = (idx < TTW * KP * 64 && col < kz && t < N) ? Pt[clamp_id(ids[t], V) * kz + col] : 0.f;
+      }
+    }
+  }
   u32x4* const xtw = (u32x4*)(smem + wave * WAVE_BYTES);           // [X/E][row * 8 + cell']
   uint16_t* const utw = (uint16_t*)(smem + wave * WAVE_BYTES + XT_BYTES);
 
@@ -492,7 +520,10 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
     for (int i = 0; i < KP; ++i)
       red[((wave * TTW + tt) * KP + i) * 64 + lane] = HAS_E ? accX[tt][i] - accE[tt][i] : accX[tt][i];
   __syncthreads();
-  for (int idx = tid; idx < TTW * KP * 64; idx += 64 * P) {
+#pragma unroll
+  for (int j = 0; j < NEP; ++j) {
+    const int idx = tid + 64 * P * j;
+    if (idx >= TTW * KP * 64) break;
     const int l = idx % 64, ti = idx / 64, i = ti % KP, tt = ti / KP;
     f32x4 sum = red[ti * 64 + l];
 #pragma unroll
@@ -505,7 +536,7 @@ __global__ __launch_bounds__(64 * P) __attribute__((amdgpu_waves_per_eu(1, 2))) 
         const int64_t t = tok0 + 16 * tt + 4 * (l >> 4) + e;
         if (t < N) {
           float v = sum[e];
-          if constexpr (HAS_P) v -= Pt[clamp_id(ids[t], V) * kz + col];
+          if constexpr (HAS_P) v -= pv[j][e];
           if (Zb)
             Zb[t * kz + col] = (uint16_t)f32_to_bf16(v);
           else
