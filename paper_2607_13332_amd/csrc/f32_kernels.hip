@@ -361,9 +361,9 @@ __global__ __launch_bounds__(64 * W) void compress_f32_mfma(
 // ===========================================================================
 // compress / gradient projection for few tokens (the kernel above runs
 // N / 64 blocks, a fraction of the chip).  Block = 16 tokens x PW waves; wave
-// w walks the w-th of PW equal ranges of d with a wave-private U tile and D
-// tile, so no barrier is needed until the end (a wave's LDS operations
-// complete in order).  U for the next chunks travels in UD register sets;
+// w walks the w-th of PW equal ranges of d with a wave-private U tile and
+// its A operands read straight from the rows, so no barrier is needed until
+// the end (a wave's LDS operations complete in order).  U for the next chunks travels in UD register sets;
 // the MFMA loop is the one above.  The PW partial products meet in LDS and
 // are added in wave order (deterministic); wave w finishes the coordinates
 // KP j + h with h = w mod PW.
@@ -380,33 +380,28 @@ __global__ __launch_bounds__(64 * PW) void compress_f32_split(
   constexpr int UP = Stage::UP, FPT = Stage::FPT;
   static_assert(KP * 64 * 4 <= DC * UP, "the partial products fit a wave's U tile");
   __shared__ __align__(16) float ut[PW][DC * UP];
-  __shared__ f32x4 dt[PW][16 * 16];                // [wave][token * 16 + (cell ^ token)]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n16 = lane & 15, g = lane >> 4;
   const int64_t tok0 = (int64_t)blockIdx.x * 16;
 
-  // rows: instruction m covers tokens 4 m .. 4 m + 3, 16 lanes (256 bytes) each
-  const float* xrow[4];
-  const float* erow[4];
-#pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    int64_t t = tok0 + 4 * m + g;
-    t = t < N ? t : N - 1;
-    xrow[m] = X + t * d + 4 * n16;
-    erow[m] = HAS_E ? E + clamp_id(ids[t], V) * d + 4 * n16 : nullptr;
-  }
+  // A operand straight from the rows: lane (n16, g) reads d = 16 q + 4 g ..
+  // + 3 of token n16 (16 tokens x 64 contiguous bytes per instruction) and
+  // forms X - E in registers
+  int64_t tn = tok0 + n16;
+  tn = tn < N ? tn : N - 1;
+  const float* const xa = X + tn * d + 4 * g;
+  const float* const ea = HAS_E ? E + clamp_id(ids[tn], V) * d + 4 * g : nullptr;
   const Stage stage(lane, ku);
   float* const ub = ut[wave];
   stage.zero_pad(ub, 1);
-  f32x4* const dw = dt[wave];
   f32x4 ust[UD][FPT];
   f32x4 xs[2][4], es[2][4];
   auto load_rows = [&](int c, f32x4(&xo)[4], f32x4(&eo)[4]) {
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      xo[m] = __builtin_nontemporal_load((const f32x4*)(xrow[m] + c * DC));
-      if constexpr (HAS_E) eo[m] = *(const f32x4*)(erow[m] + c * DC);
+    for (int q = 0; q < 4; ++q) {
+      xo[q] = __builtin_nontemporal_load((const f32x4*)(xa + c * DC + 16 * q));
+      if constexpr (HAS_E) eo[q] = *(const f32x4*)(ea + c * DC + 16 * q);
     }
   };
 
@@ -420,13 +415,8 @@ __global__ __launch_bounds__(64 * PW) void compress_f32_split(
   auto body = [&](int i, auto Bc) {
     constexpr int B = decltype(Bc)::value;
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      const int r = 4 * m + g;
-      dw[r * 16 + (n16 ^ r)] = HAS_E ? xs[B][m] - es[B][m] : xs[B][m];
-    }
-#pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const f32x4 a = dw[n16 * 16 + ((4 * q + g) ^ n16)];
+      const f32x4 a = HAS_E ? xs[B][q] - es[B][q] : xs[B][q];
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         const float* ur = ub + (16 * q + 4 * g + s) * UP + KP * n16;
@@ -573,7 +563,7 @@ static hipError_t launch_compress_f32_split(int64_t N, int d, int64_t V, const f
                                             const int32_t* ids, const float* E, const float* U,
                                             float* Z, const float* P, hipStream_t st, uint16_t* Zb,
                                             int kz, int ku) {
-  constexpr int PW = 4, UD = KP <= 4 ? 2 : 1;
+  constexpr int PW = KP <= 4 ? 8 : 4, UD = KP <= 2 ? 2 : 1;
   const dim3 grid((unsigned)((N + 15) / 16));
   if (E)
     hipLaunchKernelGGL((compress_f32_split<KP, true, false, SPAN, PW, UD>), grid, dim3(64 * PW), 0, st, X,
@@ -600,7 +590,7 @@ static hipError_t launch_compress_f32_w(int64_t N, int d, int64_t V, const float
   // 43 us; but N = 12288, d = 5120: 167 us against 185 us split).
   const int64_t cus = device_cu_count();
   const bool eight = (N + 127) / 128 >= cus, span = ku != 16 * KP;
-  if (2 * ((N + 63) / 64) <= cus && d % (4 * kF32Chunk) == 0)
+  if (2 * ((N + 63) / 64) <= cus && d % ((KP <= 4 ? 8 : 4) * kF32Chunk) == 0)
     return span ? launch_compress_f32_split<KP, true>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku)
                 : launch_compress_f32_split<KP, false>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
   if (eight && !span) return launch_compress_f32_kp<KP, 8, false>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
