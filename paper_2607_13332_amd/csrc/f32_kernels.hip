@@ -583,14 +583,16 @@ static hipError_t launch_compress_f32_w(int64_t N, int d, int64_t V, const float
                                         const float* P, hipStream_t st, uint16_t* Zb, int kz, int ku) {
   // 8 waves (128 tokens) per block once those blocks fill the compute units,
   // else 4 (64 tokens); U rows of any width other than 16 KP are staged
-  // span-wise.  With at most half as many 64-token blocks as compute units,
-  // d is split over the 4 waves of 16-token blocks instead (measured on
-  // MI355X, compress / projection: N = 2048, d = 2048, k = 40: 53 -> 22 us;
-  // N = 4096, d = 5120, k = 51: 152 -> 62 us; N = 8192, d = 2048: 57 ->
-  // 43 us; but N = 12288, d = 5120: 167 us against 185 us split).
+  // span-wise.  With at most three quarters as many 64-token blocks as
+  // compute units, d is split over the waves of 16-token blocks instead
+  // (measured on MI355X, compress / projection: N = 2048, d = 2048, k = 40:
+  // 53 / 53 -> 21 / 17 us; N = 4096, d = 5120, k = 51: 152 / 150 -> 54 /
+  // 45 us; N = 8192, d = 2048: 57 / 56 -> 40 / 35 us; N = 12288, d = 5120:
+  // 167 / 182 -> 164 / 146 us; but N = 16384, d = 4096, k = 64: 130 / 108
+  // us on the 64-token blocks against 166 / 143 us split).
   const int64_t cus = device_cu_count();
   const bool eight = (N + 127) / 128 >= cus, span = ku != 16 * KP;
-  if (2 * ((N + 63) / 64) <= cus && d % ((KP <= 4 ? 8 : 4) * kF32Chunk) == 0)
+  if (4 * ((N + 63) / 64) <= 3 * cus && d % ((KP <= 4 ? 8 : 4) * kF32Chunk) == 0)
     return span ? launch_compress_f32_split<KP, true>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku)
                 : launch_compress_f32_split<KP, false>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
   if (eight && !span) return launch_compress_f32_kp<KP, 8, false>(N, d, V, X, ids, E, U, Z, P, st, Zb, kz, ku);
