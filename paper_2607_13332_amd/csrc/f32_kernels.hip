@@ -4,11 +4,13 @@
 // Z = (X - E[ids]) U, X' = E[ids] + Z U^T; the gradient forms are the same
 // kernels without the embedding.
 //
-// Both kernels walk d in 64-wide chunks (256 contiguous bytes of a float32
-// row) and stage the chunk's 64 rows of U [d, K] (K = 16, 32, .., 128 floats
-// per row) once per block into a row-major LDS tile of pitch K + 4 floats,
-// double buffered, one barrier per chunk.  Activation and embedding rows
-// travel as 4 rows x 256 contiguous bytes per instruction.
+// The kernels walk d in 64-wide chunks (256 contiguous bytes of a float32
+// row) and stage the chunk's 64 rows of U [d, ku] (any ku <= 128) into a
+// row-major LDS tile K = 16 ceil(ku / 16) wide (pitch K + 4 floats, zero past
+// ku): the many-token kernels once per block, double buffered, one barrier
+// per chunk, their activation and embedding rows moving as 4 rows x 256
+// contiguous bytes per instruction; the few-token compress / projection once
+// per wave, with no barrier.
 #include "ssn_device.h"
 #include "ssn_launch.h"
 
