@@ -21,8 +21,9 @@ namespace ssn {
 // form TW = 8 / RS tile groups of RS waves: wave w = RS tw + rs owns the
 // tiles tw, tw + TW, .. of the strip and row share rs (a group's waves are
 // consecutive, so they sit on different SIMDs when waves are placed on the
-// four SIMDs in turn, and groups with one tile more do not pile onto one SIMD).  Few tiles per block
-// (small matrices) thus still keep all four SIMDs on the matrix cores.
+// four SIMDs in turn, and groups with one tile more do not pile onto one
+// SIMD).  Few tiles per block (small matrices) thus still keep all four
+// SIMDs on the matrix cores.
 // Pass 1, T = U^T W, over d in chunks of 32 rows: the chunk's rows of the
 // strip and of U are staged into LDS row tiles (double buffered, one barrier
 // per chunk, pitches chosen so that the 64 lanes of a read hit 64 banks).
@@ -36,8 +37,9 @@ namespace ssn {
 // registers.  Pass 2, W = U T, in chunks of 32 RS rows, wave rs taking rows
 // 32 rs .. + 31 of each: A = 16 contiguous bytes of a U row (from L2), the
 // output rows parked in one of two LDS row tiles (one barrier per chunk) and
-// stored by the block in 16-byte pieces (non-temporal: W is not read again).  Columns past a matrix's n (in
-// its last tile) are neither used nor stored.
+// stored by the block in 16-byte pieces (non-temporal: W is not read
+// again).  Columns past a matrix's n (in its last tile) are neither used nor
+// stored.
 // ===========================================================================
 struct ColumnBatchF32 {
   float* W[kMaxBatch];
