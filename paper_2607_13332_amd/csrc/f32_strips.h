@@ -446,9 +446,10 @@ hipError_t launch_weights_f32_kt(const ColumnBatchF32& cb, const float* U, int d
 }
 
 // Explicitly instantiated in f32_strips_a.hip (KT 1..4) and f32_strips_b.hip
-// (KT 5..8).
+// (KT 5..8); the dispatching unit declares them extern.
 #define SSN_STRIPS_F32_KT(KT, FG)                                                                 \
   template hipError_t launch_weights_f32_kt<KT, FG>(const ColumnBatchF32&, const float*, int, int, \
                                                     float*, hipStream_t)
+#define SSN_STRIPS_F32_KT_EXTERN(KT, FG) extern SSN_STRIPS_F32_KT(KT, FG)
 
 }  // namespace ssn

@@ -5,22 +5,22 @@
 
 namespace ssn {
 
-extern template hipError_t launch_weights_f32_kt<1, false>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<2, false>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<3, false>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<4, false>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<5, false>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<6, false>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<7, false>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<8, false>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<1, true>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<2, true>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<3, true>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<4, true>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<5, true>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<6, true>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<7, true>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
-extern template hipError_t launch_weights_f32_kt<8, true>(const ColumnBatchF32&, const float*, int, int, float*, hipStream_t);
+SSN_STRIPS_F32_KT_EXTERN(1, false);
+SSN_STRIPS_F32_KT_EXTERN(2, false);
+SSN_STRIPS_F32_KT_EXTERN(3, false);
+SSN_STRIPS_F32_KT_EXTERN(4, false);
+SSN_STRIPS_F32_KT_EXTERN(5, false);
+SSN_STRIPS_F32_KT_EXTERN(6, false);
+SSN_STRIPS_F32_KT_EXTERN(7, false);
+SSN_STRIPS_F32_KT_EXTERN(8, false);
+SSN_STRIPS_F32_KT_EXTERN(1, true);
+SSN_STRIPS_F32_KT_EXTERN(2, true);
+SSN_STRIPS_F32_KT_EXTERN(3, true);
+SSN_STRIPS_F32_KT_EXTERN(4, true);
+SSN_STRIPS_F32_KT_EXTERN(5, true);
+SSN_STRIPS_F32_KT_EXTERN(6, true);
+SSN_STRIPS_F32_KT_EXTERN(7, true);
+SSN_STRIPS_F32_KT_EXTERN(8, true);
 
 template <bool FG>
 static hipError_t launch_strips_f32(ColumnBatchF32& cb, const float* U, int d, int k, float* fg_out,
