@@ -539,6 +539,9 @@ REPARAM_SHAPES = [  # (N, din, d, k, dtype): every kernel family and tail
     # counts, k % 4 != 0, narrow din) and the generic paths (din % 4 != 0)
     (1000, 2048, 1024, 51, "f32"), (777, 1024, 512, 64, "f32"), (33, 100, 96, 10, "f32"),
     (130, 4096, 2048, 128, "f32"), (4096, 18432, 5120, 51, "f32"), (50, 102, 128, 16, "f32"),
+    # the factor gradient's other tile-group layouts: 2 tiles per block (4
+    # waves per group) and 9 (one wave per group, two tiles per wave)
+    (300, 8192, 1024, 40, "f32"), (200, 36864, 512, 24, "f32"),
 ]
 
 
