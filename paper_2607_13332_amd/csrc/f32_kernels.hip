@@ -253,6 +253,15 @@ __global__ __launch_bounds__(64 * W) void compress_f32_mfma(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n16 = lane & 15, g = lane >> 4;
   const int64_t tok0 = (int64_t)blockIdx.x * (16 * W) + 16 * wave;
+  // HAS_P: table row offsets of the epilogue's tokens 4 g + r, looked up now
+  int64_t prow[HAS_P ? 4 : 1];
+  if constexpr (HAS_P) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t t = tok0 + 4 * g + r;
+      prow[r] = t < N ? clamp_id(ids[t], V) * kz : 0;
+    }
+  }
 
   // rows: instruction m covers tokens 4 m .. 4 m + 3, 16 lanes (256 bytes) each
   const float* xrow[4];
@@ -351,7 +360,7 @@ __global__ __launch_bounds__(64 * W) void compress_f32_mfma(
       const int col = KP * n16 + h;
       if (col >= kz) continue;
       float v = acc[h][r];
-      if constexpr (HAS_P) v -= Pt[clamp_id(ids[t], V) * kz + col];
+      if constexpr (HAS_P) v -= Pt[prow[r] + col];
       if (Zb)
         Zb[t * kz + col] = (uint16_t)f32_to_bf16(v);
       else
@@ -386,6 +395,15 @@ __global__ __launch_bounds__(64 * PW) void compress_f32_split(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n16 = lane & 15, g = lane >> 4;
   const int64_t tok0 = (int64_t)blockIdx.x * 16;
+  // HAS_P: table row offsets of the epilogue's tokens 4 g + r, looked up now
+  int64_t prow[HAS_P ? 4 : 1];
+  if constexpr (HAS_P) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t t = tok0 + 4 * g + r;
+      prow[r] = t < N ? clamp_id(ids[t], V) * kz : 0;
+    }
+  }
 
   // A operand straight from the rows: lane (n16, g) reads d = 16 q + 4 g ..
   // + 3 of token n16 (16 tokens x 64 contiguous bytes per instruction) and
@@ -484,7 +502,7 @@ __global__ __launch_bounds__(64 * PW) void compress_f32_split(
       const int64_t t = tok0 + 4 * g + r;
       if (t >= N) continue;
       float v = s[r];
-      if constexpr (HAS_P) v -= Pt[clamp_id(ids[t], V) * kz + col];
+      if constexpr (HAS_P) v -= Pt[prow[r] + col];
       if (Zb)
         Zb[t * kz + col] = (uint16_t)f32_to_bf16(v);
       else
