@@ -688,14 +688,25 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         inp["u_c"] = int(torch.unique(inp["ids_c"]).numel())
         sets.append(inp)
     ops = ["decompress", "project_grad", "compress", "expand_grad"]
+    # the gradient projection takes its range split through a workspace
+    # allocated once per basis width (None where the split does not pay)
+    wsp = {}
 
-    def step(s, Ub, evs=None):
+    def ws_for(Ub, split=True):
+        w = Ub.shape[1]
+        if not split:
+            return None
+        if w not in wsp:
+            wsp[w] = ssn.project_grad_workspace(N, d, k, dev, ldu=w, dtype=act)
+        return wsp[w]
+
+    def step(s, Ub, evs=None, split=True):
         if evs:
             evs[0].record()
         ssn.decompress(s["Zin"], s["ids"], E, Ub, out=s["Y"])
         if evs:
             evs[1].record()
-        ssn.project_grad(s["G"], Ub, out=s["GZ"], k=k)
+        ssn.project_grad(s["G"], Ub, out=s["GZ"], k=k, workspace=ws_for(Ub, split))
         if evs:
             evs[2].record()
         ssn.compress(s["X"], s["ids_c"], E, Ub, out=s["Z"], k=k)
@@ -705,14 +716,14 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         if evs:
             evs[4].record()
 
-    def measure(Ub):
+    def measure(Ub, split=True):
         """(ms per step, per-op mean ms) on basis Ub."""
         for i in range(warmup):
-            step(sets[i % nsets], Ub)
+            step(sets[i % nsets], Ub, split=split)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for i in range(steps):
-            step(sets[i % nsets], Ub)
+            step(sets[i % nsets], Ub, split=split)
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3 / steps
         # per-op times: R back-to-back calls of one op (rotating input sets)
@@ -724,7 +735,8 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
         R = max(20, nsets)
         calls = {
             "decompress": lambda s: ssn.decompress(s["Zin"], s["ids"], E, Ub, out=s["Y"]),
-            "project_grad": lambda s: ssn.project_grad(s["G"], Ub, out=s["GZ"], k=k),
+            "project_grad": lambda s: ssn.project_grad(s["G"], Ub, out=s["GZ"], k=k,
+                                                       workspace=ws_for(Ub, split)),
             "compress": lambda s: ssn.compress(s["X"], s["ids_c"], E, Ub, out=s["Z"], k=k),
             "expand_grad": lambda s: ssn.expand_grad(s["GZin"], Ub, out=s["GX"]),
         }
@@ -768,7 +780,7 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
 
     def step_projected(s):
         ssn.decompress(s["Zin"], s["ids"], E, Ub, out=s["Y"])
-        ssn.project_grad(s["G"], Ub, out=s["GZ"], k=k)
+        ssn.project_grad(s["G"], Ub, out=s["GZ"], k=k, workspace=ws_for(Ub))
         ssn.compress_projected(s["X"], s["ids_c"], P, Ub, out=s["Z"])
         ssn.expand_grad(s["GZin"], Ub, out=s["GX"])
 
@@ -795,6 +807,15 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
            "step_with_projected_compress": {
                "what": "the same step with compress as X U - P[ids], P = E U [V, k] float32 formed once",
                "ms_per_step": round(pms, 5), "tokens_per_s": round(N / (pms * 1e-3), 1)}}
+    wsb = wsp.get(Ub.shape[1])
+    out["project_grad_entry"] = (
+        f"ssn_project_grad_ws: d split into ranges through a {wsb.numel() / 2**20:.1f} MiB workspace "
+        "allocated once" if wsb is not None else "ssn_project_grad_ex (no range split at this shape)")
+    if wsb is not None:
+        # the same step with the gradient projection in one launch, no workspace
+        nms, nop = measure(Ub, split=False)
+        out["without_range_split"] = {"ms_per_step": round(nms, 5),
+                                      "project_grad_ms": round(nop["project_grad"], 5)}
     if pad_ms is not None:
         out["pad_basis_ms"] = round(pad_ms, 5)
         ums, uop = measure(U)
@@ -802,7 +823,7 @@ def time_codec_config(cfg, steps: int, warmup: int, dev):
             "what": f"the same step on U [{d}, {k}] as stored (k % 16 != 0: odd-width U rows)",
             "ms_per_step": round(ums, 5), "tokens_per_s": round(N / (ums * 1e-3), 1),
             "per_op_ms": {op: round(v, 5) for op, v in uop.items()}}
-    del sets, base, U, E, Ub, P
+    del sets, base, U, E, Ub, P, wsp
     torch.cuda.empty_cache()
     return out
 

@@ -185,6 +185,33 @@ ssn_status_t ssn_project_grad_ex(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t
                                  void *stream);
 
 /*
+ * ssn_project_grad_ws -- ssn_project_grad_ex with a caller-owned device
+ * workspace, for few tokens (the paper's per-call microbatches of 4096 tokens
+ * per coalesced batch, sections 3.3.1 and 5.2).  With few tokens every
+ * compute unit owns few rows of G and reads all of U; with the workspace d is
+ * split into up to 4 ranges whose partial products (float32) go to the
+ * workspace, and a second kernel adds them in range order into GZ.
+ *   workspace: device memory of workspace_bytes bytes (any contents),
+ *     16-byte aligned, not overlapping G, U or GZ (else SSN_ERR_ALIGN /
+ *     SSN_ERR_ALIAS); workspace_bytes > 0 with workspace NULL is
+ *     SSN_ERR_NULL.  ssn_project_grad_workspace_bytes(dtype, N, d, k, ldu)
+ *     is the size that allows every split; it is 0 for the shapes where the
+ *     split does not pay (float32 storage, more than 16384 tokens, or U
+ *     below 512 KiB), and there the call is ssn_project_grad_ex.  A smaller
+ *     workspace (or NULL with 0 bytes) allows fewer ranges or none.
+ *   Calls that share a workspace must not overlap in time.
+ * The result is within the projection's accuracy of ssn_project_grad_ex's;
+ * the sum over d is grouped by range, so the last bits may differ from it
+ * and depend on the number of ranges taken (fixed for a shape, a workspace
+ * size and a device).  Repeated calls are bitwise reproducible.
+ */
+size_t ssn_project_grad_workspace_bytes(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k,
+                                        int64_t ldu);
+ssn_status_t ssn_project_grad_ws(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
+                                 int64_t k, const void *G, const void *U, int64_t ldu, void *GZ,
+                                 void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * ssn_pad_basis -- the padded layout of the basis used by the `_ex` entry
  * points above, made once per basis (the basis is fixed for the run):
  *   Up[i, c] = U[i, c] for c < k,  Up[i, c] = 0 for k <= c < ldu

@@ -947,11 +947,11 @@ bool decompress_uses_mfma(int dtype, int64_t d, int64_t k) {
 // of d (grid.y), each writing its partial product to ws [S][N][k].
 template <int KP, bool KFULL>
 static hipError_t launch_rows_ranges(int64_t N, int d, int k, const void* X, const void* U, float* ws,
-                                     int S, hipStream_t st) {
+                                     int S, hipStream_t st, int kz) {
   const int64_t blocks = (N + 127) / 128;
   hipLaunchKernelGGL((compress_rows_bf16<KP, false, KFULL, 8, 1, true, false, true, 4, false>),
                      dim3((unsigned)blocks, (unsigned)S), dim3(512), 0, st, (const uint16_t*)X,
-                     nullptr, nullptr, (const uint16_t*)U, ws, N, d, k, (int64_t)1, nullptr, nullptr, k);
+                     nullptr, nullptr, (const uint16_t*)U, ws, N, d, k, (int64_t)1, nullptr, nullptr, kz);
   return hipGetLastError();
 }
 
@@ -1133,15 +1133,45 @@ static hipError_t launch_split(int64_t N, int d, int k, int64_t V, const void* X
   return launch_split_kp<8, HAS_E, HAS_P>(p.P, p.TTW, N, d, k, V, X, ids, E, U, Z, Pt, st, p.S, Zb, kz);
 }
 
-// Sum of S partial results [S][n], in range order (deterministic).
+// Sum of S partial results [S][n], in range order (deterministic), into out
+// (float32) or outb (bf16, rounded once to nearest even).  VEC: n is a
+// multiple of 4 and the pointers are aligned for 16-byte partial and output
+// pieces (8-byte for bf16), four sums per thread.
+template <bool VEC>
 __global__ __launch_bounds__(256) void sum_partials(const float* __restrict__ ws,
-                                                    float* __restrict__ out, int64_t n, int S) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    float v = ws[i];
-    for (int j = 1; j < S; ++j) v += ws[(int64_t)j * n + i];
-    out[i] = v;
+                                                    float* __restrict__ out,
+                                                    uint16_t* __restrict__ outb, int64_t n, int S) {
+  constexpr int W = VEC ? 4 : 1;
+  for (int64_t i = W * (blockIdx.x * (int64_t)blockDim.x + threadIdx.x); i < n;
+       i += (int64_t)W * gridDim.x * blockDim.x) {
+    if constexpr (VEC) {
+      f32x4 v = *(const f32x4*)(ws + i);
+      for (int j = 1; j < S; ++j) v += *(const f32x4*)(ws + (int64_t)j * n + i);
+      if (outb)
+        *(u32x2*)(outb + i) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+      else
+        *(f32x4*)(out + i) = v;
+    } else {
+      float v = ws[i];
+      for (int j = 1; j < S; ++j) v += ws[(int64_t)j * n + i];
+      if (outb)
+        outb[i] = (uint16_t)f32_to_bf16(v);
+      else
+        out[i] = v;
+    }
   }
+}
+
+static hipError_t launch_sum_partials(const float* ws, float* out, uint16_t* outb, int64_t n, int S,
+                                      hipStream_t st) {
+  const bool vec = n % 4 == 0 && al16(ws) && (outb ? ((uintptr_t)outb & 7u) == 0 : al16(out));
+  const int64_t per = vec ? 4 * 256 : 256;
+  const int64_t blocks = (n + per - 1) / per < 2048 ? (n + per - 1) / per : 2048;
+  if (vec)
+    hipLaunchKernelGGL(sum_partials<true>, dim3((unsigned)blocks), dim3(256), 0, st, ws, out, outb, n, S);
+  else
+    hipLaunchKernelGGL(sum_partials<false>, dim3((unsigned)blocks), dim3(256), 0, st, ws, out, outb, n, S);
+  return hipGetLastError();
 }
 
 // Up[i, c] = U[i, c] for c < k, 0 for k <= c < ldu: the basis with zero
@@ -1236,36 +1266,34 @@ static int rows_ranges(int64_t N, int64_t d, int64_t k, int smax) {
 }
 
 hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, const void* X,
-                                 const void* U, float* Z, float* ws, int smax, hipStream_t st) {
+                                 const void* U, float* Z, float* ws, int smax, hipStream_t st,
+                                 uint16_t* Zb, int kz) {
+  const int kzv = (kz <= 0 || kz > k) ? (int)k : kz;
+  const void* zout = Zb ? (const void*)Zb : (const void*)Z;
+  auto sum_ranges = [&](int S) { return launch_sum_partials(ws, Z, Zb, N * kzv, S, st); };
   const int rs = (smax > 1 && ws && dtype == kBF16 && k <= 128 && al16(X) && al16(U) && al16(ws) &&
                   d <= INT32_MAX)
                      ? rows_ranges(N, d, k, smax)
                      : 0;
   if (rs > 1) {
     hipError_t e;
-    if (k == 32) e = launch_rows_ranges<2, true>(N, (int)d, (int)k, X, U, ws, rs, st);
-    else if (k == 64) e = launch_rows_ranges<4, true>(N, (int)d, (int)k, X, U, ws, rs, st);
-    else e = launch_rows_ranges<8, true>(N, (int)d, (int)k, X, U, ws, rs, st);
+    if (k == 32) e = launch_rows_ranges<2, true>(N, (int)d, (int)k, X, U, ws, rs, st, kzv);
+    else if (k == 64) e = launch_rows_ranges<4, true>(N, (int)d, (int)k, X, U, ws, rs, st, kzv);
+    else e = launch_rows_ranges<8, true>(N, (int)d, (int)k, X, U, ws, rs, st, kzv);
     if (e != hipSuccess) return e;
-    const int64_t n = N * k;
-    const int64_t blocks = (n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048;
-    hipLaunchKernelGGL(sum_partials, dim3((unsigned)blocks), dim3(256), 0, st, ws, Z, n, rs);
-    return hipGetLastError();
+    return sum_ranges(rs);
   }
-  if (smax > 1 && ws && compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(Z) &&
-      compress_uses_split(N, d, k, false)) {
+  if (smax > 1 && ws && compress_uses_mfma(dtype, d, k) && al16(X) && al16(U) && al16(ws) &&
+      al16(zout) && compress_uses_split(N, d, k, false)) {
     const SplitPlan sp = split_plan(N, (int)d, (int)k, false, smax < 4 ? smax : 4);
     if (sp.S > 1) {
       hipError_t e = launch_split<false, false>(N, (int)d, (int)k, 1, X, nullptr, nullptr, U, ws,
-                                                nullptr, st, sp, nullptr, (int)k);
+                                                nullptr, st, sp, nullptr, kzv);
       if (e != hipSuccess) return e;
-      const int64_t n = N * k;
-      const int64_t blocks = (n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048;
-      hipLaunchKernelGGL(sum_partials, dim3((unsigned)blocks), dim3(256), 0, st, ws, Z, n, sp.S);
-      return hipGetLastError();
+      return sum_ranges(sp.S);
     }
   }
-  return launch_compress(dtype, N, d, k, 1, X, nullptr, nullptr, U, Z, nullptr, st, nullptr, 0);
+  return launch_compress(dtype, N, d, k, 1, X, nullptr, nullptr, U, Z, nullptr, st, Zb, kzv);
 }
 
 // 8 token tiles (128 tokens) per block, each of the 8 waves sweeping the

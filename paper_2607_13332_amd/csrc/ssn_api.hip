@@ -196,6 +196,57 @@ ssn_status_t ssn_project_grad(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k
   return ssn_project_grad_ex(dtype, SSN_F32, N, d, k, G, U, k, GZ, stream);
 }
 
+// The range-split projection (partial products [S][N][k] float32 in the
+// workspace, S <= kRangeMax, then a range sum).  It pays where U is large
+// against each compute unit's rows of G: bf16 storage, at most 16384 tokens
+// and U of 512 KiB or more.  Measured on MI355X (cold G, back-to-back calls,
+// both kernels): N = 4096 / 8192 / 12288 at d = 5120, U padded to 64 columns:
+// 18.8 / 26.8 / 44.8 us -> 17.2 / 23.6 / 36.3 us; N = 4096 at d = 4096, k =
+// 64: 16.2 -> 15.4 us; at d = 2048 (U of 192 KiB) it gained nothing at 4096
+// and 8192 tokens and lost at 12288 (19.5 -> 26.0 us).
+constexpr int64_t kRangeMax = 4;
+static bool ranges_pay(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t ldu) {
+  return dtype == SSN_BF16 && N <= 16384 && d * ldu * 2 >= (int64_t)512 << 10;
+}
+
+size_t ssn_project_grad_workspace_bytes(ssn_dtype_t dtype, int64_t N, int64_t d, int64_t k,
+                                        int64_t ldu) {
+  if (!valid_dtype(dtype) || N < 1 || d < 1 || k < 1 || k > d || !ldu_ok(k, ldu)) return 0;
+  if (!mul_ok(N, k) || !mul_ok(d, ldu) || !ranges_pay(dtype, N, d, ldu)) return 0;
+  return (size_t)(kRangeMax * N * k * 4);
+}
+
+ssn_status_t ssn_project_grad_ws(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t N, int64_t d,
+                                 int64_t k, const void* G, const void* U, int64_t ldu, void* GZ,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
+  if (N < 0 || d < 1 || k < 1 || k > d || !ldu_ok(k, ldu)) return SSN_ERR_SHAPE;
+  if (!mul_ok(N, d) || !mul_ok(d, ldu) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
+  if (workspace_bytes > (size_t)INT64_MAX) return SSN_ERR_SHAPE;
+  if (N == 0) return SSN_OK;
+  if (!G || !U || !GZ || (workspace_bytes > 0 && !workspace)) return SSN_ERR_NULL;
+  const int64_t s = elem_size(dtype), zs = elem_size(z_dtype);
+  if (!aligned_to(G, s) || !aligned_to(U, s) || !aligned_to(GZ, zs) ||
+      (workspace && !aligned_to(workspace, 16)))
+    return SSN_ERR_ALIGN;
+  const Span out = span(GZ, N * k * zs);
+  if (overlap(out, span(G, N * d * s)) || overlap(out, span(U, d * ldu * s))) return SSN_ERR_ALIAS;
+  if (workspace_bytes > 0) {
+    const Span w = span(workspace, (int64_t)workspace_bytes);
+    if (overlap(w, out) || overlap(w, span(G, N * d * s)) || overlap(w, span(U, d * ldu * s)))
+      return SSN_ERR_ALIAS;
+  }
+  int64_t smax = 1;
+  if (workspace && ranges_pay(dtype, N, d, ldu)) {
+    smax = (int64_t)workspace_bytes / (N * k * 4);
+    smax = smax < kRangeMax ? smax : kRangeMax;
+  }
+  if (smax <= 1) return ssn_project_grad_ex(dtype, z_dtype, N, d, k, G, U, ldu, GZ, stream);
+  return launch_status(ssn::launch_project_ranges(dtype, N, d, ldu, G, U, z_f32(z_dtype, GZ),
+                                                  (float*)workspace, (int)smax, (hipStream_t)stream,
+                                                  z_b16(z_dtype, GZ), kz_of(k, ldu)));
+}
+
 ssn_status_t ssn_pad_basis(ssn_dtype_t dtype, int64_t d, int64_t k, int64_t ldu, const void* U,
                            void* Up, void* stream) {
   if (!valid_dtype(dtype)) return SSN_ERR_DTYPE;

@@ -55,10 +55,13 @@ hipError_t launch_compress(int dtype, int64_t N, int64_t d, int64_t k, int64_t V
                            const int32_t* ids, const void* E, const void* U, float* Z,
                            const float* P, hipStream_t st, uint16_t* Zb = nullptr, int kz = 0);
 // Z = X.U (no E, no P).  With few tokens it may split d into up to smax
-// ranges whose partial products go to ws [S][N][k] (float32, S <= smax,
-// written before Z) and are summed into Z; ws NULL or smax <= 1: one launch.
+// ranges whose partial products go to ws [S][N][kz] (float32, S <= smax,
+// written before the result) and a second kernel adds them in range order
+// into Z (float32) or Zb (bf16, rounded once); ws NULL or smax <= 1: one
+// launch.  kz as for launch_compress.
 hipError_t launch_project_ranges(int dtype, int64_t N, int64_t d, int64_t k, const void* X,
-                                 const void* U, float* Z, float* ws, int smax, hipStream_t st);
+                                 const void* U, float* Z, float* ws, int smax, hipStream_t st,
+                                 uint16_t* Zb = nullptr, int kz = 0);
 // E non-NULL: Y = E[ids] + Z U^T; gather_z: Y = Z[ids] U^T; else Y = Z U^T.
 // Zb non-NULL: the coordinates are read from Zb in bf16 and Z is unused.
 // 0 < kz < k: Z rows hold kz coordinates for the first kz of the k columns

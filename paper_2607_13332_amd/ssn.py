@@ -57,6 +57,11 @@ def _declare(lib):
     lib.ssn_project_grad_ex.restype = ctypes.c_int
     lib.ssn_project_grad_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
                                         _c_p, _c_p, _c_i64, _c_p, _c_p]
+    lib.ssn_project_grad_workspace_bytes.restype = ctypes.c_size_t
+    lib.ssn_project_grad_workspace_bytes.argtypes = [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_i64]
+    lib.ssn_project_grad_ws.restype = ctypes.c_int
+    lib.ssn_project_grad_ws.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
+                                        _c_p, _c_p, _c_i64, _c_p, _c_p, ctypes.c_size_t, _c_p]
     lib.ssn_compress_projected_ex.restype = ctypes.c_int
     lib.ssn_compress_projected_ex.argtypes = [ctypes.c_int, ctypes.c_int, _c_i64, _c_i64, _c_i64,
                                               _c_i64, _c_p, _c_p, _c_p, _c_p, _c_i64, _c_p, _c_p]
@@ -234,9 +239,11 @@ def expand_grad(GZ: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] =
 
 def project_grad(G: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] = None,
                  stream=None, z_dtype: torch.dtype = torch.float32,
-                 k: Optional[int] = None) -> torch.Tensor:
+                 k: Optional[int] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """G_Z = G U ([N, k] in z_dtype: float32, or bfloat16 rounded once).
-    k < U.shape[1]: U is a zero-padded basis whose first k columns are used."""
+    k < U.shape[1]: U is a zero-padded basis whose first k columns are used.
+    workspace: a 1-D uint8 device tensor, e.g. from project_grad_workspace()
+    (ssn_project_grad_ws: d split into ranges with few tokens)."""
     N, d = G.shape
     ldu = U.shape[1]
     k = ldu if k is None else int(k)
@@ -246,10 +253,33 @@ def project_grad(G: torch.Tensor, U: torch.Tensor, out: Optional[torch.Tensor] =
         out = torch.empty((N, k), dtype=z_dtype, device=G.device)
     _same_device(G, U, out)
     t = G.dtype
-    _check("ssn_project_grad_ex", lib().ssn_project_grad_ex(
+    if workspace is None:
+        _check("ssn_project_grad_ex", lib().ssn_project_grad_ex(
+            _dt_code(t), _dt_code(z_dtype), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2), ldu,
+            _dev(out, "out", z_dtype, 2), _stream(stream)))
+        return out
+    _same_device(G, workspace)
+    _check("ssn_project_grad_ws", lib().ssn_project_grad_ws(
         _dt_code(t), _dt_code(z_dtype), N, d, k, _dev(G, "G", t, 2), _dev(U, "U", t, 2), ldu,
-        _dev(out, "out", z_dtype, 2), _stream(stream)))
+        _dev(out, "out", z_dtype, 2), _dev(workspace, "workspace", torch.uint8, 1),
+        workspace.numel(), _stream(stream)))
     return out
+
+
+def project_grad_workspace_bytes(N: int, d: int, k: int, ldu: Optional[int] = None,
+                                 dtype: torch.dtype = torch.bfloat16) -> int:
+    """Workspace size that lets ssn_project_grad_ws split d into every range
+    count it may take for this shape (0: no split for this shape)."""
+    ldu = k if ldu is None else int(ldu)
+    return int(lib().ssn_project_grad_workspace_bytes(_dt_code(dtype), N, d, k, ldu))
+
+
+def project_grad_workspace(N: int, d: int, k: int, device, ldu: Optional[int] = None,
+                           dtype: torch.dtype = torch.bfloat16) -> Optional[torch.Tensor]:
+    """A workspace for project_grad(..., workspace=...) at this shape (None
+    when the shape takes no split); calls that share it must not overlap."""
+    n = project_grad_workspace_bytes(N, d, k, ldu, dtype)
+    return torch.empty(n, dtype=torch.uint8, device=device) if n > 0 else None
 
 
 def check_ids(ids: torch.Tensor, V: int, out: Optional[torch.Tensor] = None,

@@ -31,7 +31,7 @@ hipError_t launch_decompress(int, int64_t, int64_t, int64_t, int64_t, const floa
 // two launches when the staging memory allows ranges (the real launcher
 // writes ws only then)
 hipError_t launch_project_ranges(int dtype, int64_t, int64_t, int64_t, const void*, const void*,
-                                 float*, float* ws, int smax, hipStream_t) {
+                                 float*, float* ws, int smax, hipStream_t, uint16_t*, int) {
   g_launches += (dtype == kBF16 && ws && smax >= 2) ? 2 : 1;
   return hipSuccess;
 }

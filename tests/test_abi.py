@@ -137,6 +137,33 @@ def test_project_grad_validation(ssn):
     assert f(1, 10, 64, 8, A, D, A + 8, None) == ERR_ALIAS
 
 
+def test_project_grad_workspace_validation(ssn):
+    L = ssn.lib()
+    w = L.ssn_project_grad_workspace_bytes
+    # up to 4 float32 partial products [N, k] where the split pays (bf16, at
+    # most 16384 tokens, U of 512 KiB or more)
+    assert w(1, 4096, 5120, 51, 64) == 4 * 4096 * 51 * 4
+    assert w(1, 16384, 4096, 64, 64) == 4 * 16384 * 64 * 4
+    assert w(1, 16385, 4096, 64, 64) == 0               # many tokens: no split
+    assert w(1, 4096, 2048, 40, 48) == 0                # U of 192 KiB: no split
+    assert w(0, 4096, 5120, 51, 64) == 0                # float32 storage: no split
+    assert w(1, 4096, 64, 65, 65) == 0 and w(7, 4096, 4096, 64, 64) == 0
+    assert w(1, 4096, 4096, 64, 63) == 0                # ldu < k
+    assert ssn.project_grad_workspace_bytes(4096, 4096, 64) == 4 * 4096 * 64 * 4
+    f = L.ssn_project_grad_ws
+    n = 4096
+    assert f(1, 0, 0, 64, 8, None, None, 8, None, None, 0, None) == OK       # N == 0 no-op
+    assert f(1, 7, 10, 64, 8, A, D, 8, F, C, n, None) == ERR_DTYPE
+    assert f(1, 0, 10, 64, 8, A, D, 4, F, C, n, None) == ERR_SHAPE          # ldu < k
+    assert f(1, 0, 10, 64, 8, A, D, 8, F, None, n, None) == ERR_NULL        # bytes, no pointer
+    assert f(1, 0, 10, 64, 8, None, D, 8, F, C, n, None) == ERR_NULL
+    assert f(1, 0, 10, 64, 8, A, D, 8, F, C + 4, n, None) == ERR_ALIGN      # 16-byte aligned
+    assert f(1, 0, 10, 64, 8, A, D, 8, F, A + 64, n, None) == ERR_ALIAS     # workspace on G
+    assert f(1, 0, 10, 64, 8, A, D, 8, F, F - 16, n, None) == ERR_ALIAS     # workspace on GZ
+    assert f(1, 0, 10, 64, 8, A, D, 8, F, D - 16, n, None) == ERR_ALIAS     # workspace on U
+    assert f(1, 0, 10, 64, 8, A, D, 8, A + 8, C, n, None) == ERR_ALIAS      # GZ on G
+
+
 def test_projected_table_validation(ssn):
     L = ssn.lib()
     t = L.ssn_project_table

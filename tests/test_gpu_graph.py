@@ -69,13 +69,20 @@ def test_wire_formats_capture():
     outs = {"Y": torch.empty((N, d), dtype=torch.bfloat16, device=DEV),
             "GZ": torch.empty((N, k), dtype=torch.bfloat16, device=DEV),
             "Z": torch.empty((N, k), dtype=torch.bfloat16, device=DEV),
-            "GX": torch.empty((N, d), dtype=torch.bfloat16, device=DEV)}
+            "GX": torch.empty((N, d), dtype=torch.bfloat16, device=DEV),
+            "GZw": torch.empty((N, k), device=DEV),
+            "GZwb": torch.empty((N, k), dtype=torch.bfloat16, device=DEV)}
+    # the range-split projection through the caller's workspace
+    ws = ssn.project_grad_workspace(N, d, k, DEV, ldu=ldu)
+    assert ws is not None
 
     def step(o):
         ssn.decompress(Zb, static["ids"], static["E"], Up, out=o["Y"])
         ssn.project_grad(static["G"], Up, out=o["GZ"], z_dtype=torch.bfloat16, k=k)
         ssn.compress(static["X"], static["ids"], static["E"], Up, out=o["Z"], z_dtype=torch.bfloat16, k=k)
         ssn.expand_grad(Zb, Up, out=o["GX"])
+        ssn.project_grad(static["G"], Up, out=o["GZw"], k=k, workspace=ws)
+        ssn.project_grad(static["G"], Up, out=o["GZwb"], z_dtype=torch.bfloat16, k=k, workspace=ws)
 
     Up[:, :k] = static["U"]
     step(outs)
@@ -96,6 +103,7 @@ def test_wire_formats_capture():
         torch.cuda.synchronize()
         for key in outs:
             assert torch.equal(got[key], ref[key]), f"replay {rep}: {key} differs from eager"
+        assert torch.equal(got["GZwb"], got["GZw"].to(torch.bfloat16))
 
 
 @pytest.mark.parametrize("N,din,d,k", [(1024, 2048, 1024, 51), (2048, 16384, 1024, 32)],

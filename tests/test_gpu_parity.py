@@ -446,6 +446,45 @@ def test_compress_split_shapes(N, d, k):
     assert torch.equal(ssn.project_grad(X, U), ssn.project_grad(X, U))
 
 
+RANGE_SHAPES = [  # (N, d, k, ldu): few tokens, d split into ranges through the workspace
+    (4096, 5120, 51, 64), (8192, 5120, 51, 64), (12288, 5120, 51, 64), (4096, 4096, 64, 64),
+    (16384, 4096, 64, 64), (3000, 5120, 51, 64), (1000, 8192, 64, 64), (17, 8192, 64, 64),
+    (200, 16384, 32, 32), (777, 4096, 128, 128), (4096, 2048, 40, 48),
+]
+
+
+@pytest.mark.parametrize("N,d,k,ldu", RANGE_SHAPES)
+def test_project_grad_workspace_ranges(N, d, k, ldu):
+    """ssn_project_grad_ws: the gradient projection with d split into ranges
+    whose float32 partials go to the caller's workspace (filled with garbage
+    first: its contents on entry do not matter).  The result matches the
+    oracle element by element, repeats bit for bit, and its bf16 form is the
+    float32 result rounded once; fewer ranges (a smaller workspace) stay
+    within the same bounds, and no room for two ranges gives the plain
+    projection's bits."""
+    print(f"[case] project_grad_ws N={N} d={d} k={k} ldu={ldu}", flush=True)
+    seed = 11 * N + d + k
+    Uh = I.store(I.gaussian_orthonormal_basis(d, k, seed), "bf16")
+    Gh = I.store(np.random.default_rng(seed).standard_normal((N, d)), "bf16")
+    G, U = dev(Gh, "bf16"), dev(Uh, "bf16")
+    Up = ssn.pad_basis(U, ldu) if ldu > k else U
+    need = ssn.project_grad_workspace_bytes(N, d, k, ldu)
+    assert (need > 0) == (d * ldu * 2 >= 512 << 10 and N <= 16384)
+    ws = torch.full((max(need, 16),), 0x7F, dtype=torch.uint8, device=DEV)
+    Z = ssn.project_grad(G, Up, k=k, workspace=ws)
+    Zb = ssn.project_grad(G, Up, k=k, workspace=ws, z_dtype=torch.bfloat16)
+    assert torch.equal(Z, ssn.project_grad(G, Up, k=k, workspace=ws))
+    assert torch.equal(Zb, Z.to(torch.bfloat16))
+    rows = np.arange(N) if N <= 4096 else sample_rows(N, 2048, seed)
+    ref, mag = O.project_grad(Gh[rows], Uh), mag_project(Gh[rows], Uh)
+    check("project_grad_ws", host(Z)[rows], ref, "bf16", "f32out", mag=mag)
+    if need:
+        Z2 = ssn.project_grad(G, Up, k=k, workspace=ws[:2 * N * k * 4])
+        check("project_grad_ws 2 ranges", host(Z2)[rows], ref, "bf16", "f32out", mag=mag)
+        Z1 = ssn.project_grad(G, Up, k=k, workspace=ws[:2 * N * k * 4 - 16])
+        assert torch.equal(Z1, ssn.project_grad(G, Up, k=k))
+
+
 WEIGHT_SHAPES = [  # (d, n, k)
     (256, 1, 64), (256, 100, 64), (512, 200, 40), (4096, 64, 128), (512, 197, 8), (96, 70, 32),
     (128, 300, 51), (64, 33, 16), (2048, 130, 96), (1024, 4096, 64),
