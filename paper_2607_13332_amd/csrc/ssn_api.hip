@@ -222,7 +222,9 @@ ssn_status_t ssn_project_grad_ws(ssn_dtype_t dtype, ssn_dtype_t z_dtype, int64_t
   if (!valid_dtype(dtype) || !valid_dtype(z_dtype)) return SSN_ERR_DTYPE;
   if (N < 0 || d < 1 || k < 1 || k > d || !ldu_ok(k, ldu)) return SSN_ERR_SHAPE;
   if (!mul_ok(N, d) || !mul_ok(d, ldu) || !mul_ok(N, k)) return SSN_ERR_SHAPE;
-  if (workspace_bytes > (size_t)INT64_MAX) return SSN_ERR_SHAPE;
+  if (workspace_bytes > (size_t)INT64_MAX ||
+      (uintptr_t)workspace + workspace_bytes < (uintptr_t)workspace)   // past the address space
+    return SSN_ERR_SHAPE;
   if (N == 0) return SSN_OK;
   if (!G || !U || !GZ || (workspace_bytes > 0 && !workspace)) return SSN_ERR_NULL;
   const int64_t s = elem_size(dtype), zs = elem_size(z_dtype);

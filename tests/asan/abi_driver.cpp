@@ -66,6 +66,9 @@ int main() {
             ssn_compress_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, X, ids, E, U, 64, Z, nullptr);
             ssn_decompress_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, Z, ids, E, U, 64, Y, nullptr);
             ssn_project_grad_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, X, U, BIG, Z, nullptr);
+            ssn_project_grad_workspace_bytes((ssn_dtype_t)dt, N, d, k, k);
+            for (size_t wb : {(size_t)0, (size_t)4096, (size_t)BIG, SIZE_MAX})
+              ssn_project_grad_ws((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, X, U, k, Z, T, wb, nullptr);
             ssn_compress_projected_ex((ssn_dtype_t)dt, (ssn_dtype_t)zt, N, d, k, 100, X, ids, T, U, k < BIG - 8 ? k + 5 : k, Z, nullptr);
           }
         }
@@ -90,6 +93,22 @@ int main() {
   EXPECT(ssn_decompress_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, 100, (char*)Y - 10 * 64 * 2 + 2, ids, E, U, 64, Y, nullptr), SSN_ERR_ALIAS);
   EXPECT(ssn_project_grad_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, X, U, 64, (char*)X - 10 * 64 * 2, nullptr), SSN_OK);
   EXPECT(ssn_project_grad_ex(SSN_BF16, SSN_BF16, 10, 4096, 64, X, U, 64, (char*)X - 10 * 64 * 2 + 2, nullptr), SSN_ERR_ALIAS);
+  // gradient projection with a workspace: the range split takes two launches
+  EXPECT(ssn_project_grad_workspace_bytes(SSN_BF16, 4096, 5120, 51, 64), (size_t)4 * 4096 * 51 * 4);
+  EXPECT(ssn_project_grad_workspace_bytes(SSN_F32, 4096, 5120, 51, 64), (size_t)0);
+  {
+    const size_t wb = ssn_project_grad_workspace_bytes(SSN_BF16, 4096, 5120, 51, 64);
+    const int before = g_launches;
+    EXPECT(ssn_project_grad_ws(SSN_BF16, SSN_F32, 4096, 5120, 51, X, U, 64, Z, T, wb, nullptr), SSN_OK);
+    if (g_launches != before + 2) ++g_fail;
+    EXPECT(ssn_project_grad_ws(SSN_BF16, SSN_F32, 4096, 5120, 51, X, U, 64, Z, nullptr, 0, nullptr), SSN_OK);
+    if (g_launches != before + 3) ++g_fail;
+  }
+  EXPECT(ssn_project_grad_ws(SSN_BF16, SSN_F32, 4096, 5120, 51, X, U, 64, Z, nullptr, 16, nullptr), SSN_ERR_NULL);
+  EXPECT(ssn_project_grad_ws(SSN_BF16, SSN_F32, 4096, 5120, 51, X, U, 64, Z, T, SIZE_MAX, nullptr), SSN_ERR_SHAPE);
+  EXPECT(ssn_project_grad_ws(SSN_BF16, SSN_F32, 4096, 5120, 51, X, U, 64, Z, P(UINTPTR_MAX - 15), 4096, nullptr), SSN_ERR_SHAPE);
+  EXPECT(ssn_project_grad_ws(SSN_BF16, SSN_F32, 4096, 5120, 51, X, U, 64, Z, (char*)T + 8, 4096, nullptr), SSN_ERR_ALIGN);
+  EXPECT(ssn_project_grad_ws(SSN_BF16, SSN_F32, 4096, 5120, 51, X, U, 64, Z, (char*)Z - 16, 4096, nullptr), SSN_ERR_ALIAS);
 
   // ---- weight re-projection: host arrays of every legal and illegal count ----
   for (int64_t count = -1; count <= SSN_MAX_BATCH + 2; ++count) {
