@@ -345,9 +345,15 @@ __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBa
     for (int i = 0; i < NP2; ++i) op[i] = w32_piece(cb, t0, tcount, tpb, tid + kW32Threads * i, R2, WP2);
     f32x4 ua[PD][2][KT];
     // chunk c parks its rows in output tile c % 2: the barrier after chunk
-    // c + 1 is parked orders the stores of chunk c before chunk c + 2 parks
-    auto body2 = [&](int c, auto Sc) {
+    // c + 1 is parked orders the stores of chunk c before chunk c + 2 parks.
+    // SM >= 0: this thread's pieces 0 .. SM - 1 are stored in every chunk and
+    // the others never (so the stores are unconditional and the wait for the
+    // next chunk's U operands, issued before them, leaves them in flight;
+    // with conditional stores the compiler cannot count them and drains
+    // them before the next chunk's MFMAs).  SM < 0: each piece tests itself.
+    auto body2 = [&](int c, auto Sc, auto SMc) {
       constexpr int S = decltype(Sc)::value;
+      constexpr int SM = decltype(SMc)::value;
       float* const ot = smem + (c & 1) * R2 * WP2M;
       if constexpr (NV > 0) {
         if constexpr (PD == 2) {
@@ -385,21 +391,52 @@ __global__ __launch_bounds__(kW32Threads) void project_weights_f32_mfma(ColumnBa
         }
       }
       __syncthreads();                          // the chunk's output rows are parked
+      if constexpr (SM >= 0) {
 #pragma unroll
-      for (int i = 0; i < NP2; ++i)
-        if (op[i].on && c * R2 + op[i].row < d)
+        for (int i = 0; i < SM; ++i)
           __builtin_nontemporal_store(*(const f32x4*)(ot + op[i].lofs),
                                       (f32x4*)(op[i].ptr + (int64_t)c * R2 * op[i].ld));
-    };
-    if constexpr (NV > 0) load_ua(0, ua[0]);
-    int c = 0;
-    if constexpr (PD == 2) {
-      for (; c + 1 < nch2; c += 2) {
-        body2(c, std::integral_constant<int, 0>{});
-        body2(c + 1, std::integral_constant<int, 1>{});
+      } else {
+#pragma unroll
+        for (int i = 0; i < NP2; ++i)
+          if (op[i].on && c * R2 + op[i].row < d)
+            __builtin_nontemporal_store(*(const f32x4*)(ot + op[i].lofs),
+                                        (f32x4*)(op[i].ptr + (int64_t)c * R2 * op[i].ld));
       }
+    };
+    auto pass2 = [&](auto SMc) {
+      if constexpr (NV > 0) load_ua(0, ua[0]);
+      int c = 0;
+      if constexpr (PD == 2) {
+        for (; c + 1 < nch2; c += 2) {
+          body2(c, std::integral_constant<int, 0>{}, SMc);
+          body2(c + 1, std::integral_constant<int, 1>{}, SMc);
+        }
+      } else if (nch2 > 0) {
+        // the first chunk apart: every entry to the loop then has the same
+        // stores in flight after the U loads it waits for
+        body2(0, std::integral_constant<int, 0>{}, SMc);
+        c = 1;
+      }
+      for (; c < nch2; ++c) body2(c, std::integral_constant<int, 0>{}, SMc);
+    };
+    // pieces on in every chunk: op[i].on, and the rows of the last chunk
+    // inside d (always when d is a multiple of the chunk)
+    int ns = 0;
+    bool prefix = true;
+#pragma unroll
+    for (int i = 0; i < NP2; ++i) {
+      const bool on = op[i].on && d % R2 == 0;
+      prefix = prefix && (on ? ns == i : true);
+      ns += on ? 1 : 0;
     }
-    for (; c < nch2; ++c) body2(c, std::integral_constant<int, 0>{});
+    if (__all(prefix && ns == NP2)) {
+      pass2(std::integral_constant<int, NP2>{});
+    } else if (NP2 > 1 && __all(prefix && ns == NP2 - 1)) {
+      pass2(std::integral_constant<int, (NP2 > 1 ? NP2 - 1 : 0)>{});
+    } else {
+      pass2(std::integral_constant<int, -1>{});
+    }
   };
   if (nv >= 3) {
     if constexpr (CT >= 3) run(std::integral_constant<int, 3>{});
