@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define SSN_ABI_VERSION 2
+#define SSN_ABI_VERSION 3
 /* Largest matrix count accepted by ssn_project_weights_batched. */
 #define SSN_MAX_BATCH 16
 /* Largest sender count accepted by ssn_sparta_average. */

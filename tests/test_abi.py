@@ -48,7 +48,7 @@ def test_every_declared_symbol_is_exported(ssn):
 
 def test_version_and_status_strings(ssn):
     L = ssn.lib()
-    assert L.ssn_abi_version() == 2
+    assert L.ssn_abi_version() == 3
     assert L.ssn_status_string(OK) == b"ok"
     assert L.ssn_status_string(ERR_ALIAS) == b"output overlaps an input"
     assert L.ssn_status_string(99) == b"unknown status"
